@@ -1,0 +1,401 @@
+/*
+ * HeadGuard CPU oracle -- TEST INFRASTRUCTURE ONLY (see hg_oracle.h).
+ *
+ * Plain scalar loops, one step per line of the method, in the order the paper
+ * describes it:
+ *   - per-token min-max: each token's range is its own minimum and maximum and
+ *     every entry rounds to the nearest of the 2^b evenly spaced levels
+ *     (§1, first paragraph; §4 "Quantization setup");
+ *   - KIVI-style: keys per channel, values per token (§2 "KV-cache
+ *     quantization"; §4);
+ *   - AKVQ-style: Hadamard rotation of the keys, then per-token (§2; §4);
+ *   - protection: selected heads keep their image keys (and values in K+V
+ *     mode) in BF16, text KV is never touched (§3 "Applying protection");
+ *   - 32 bits of metadata per quantized vector (§5.4, storage estimate).
+ * Where the paper is silent the readings are the ones stated in the header
+ * comment of each function.
+ *
+ * Build: gcc -O2 -fno-fast-math -ffp-contract=off -fPIC -shared -pthread
+ */
+#include "hg_oracle.h"
+
+#include <math.h>
+#include <pthread.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------ BF16 */
+
+static uint32_t f2u(float x) { uint32_t u; memcpy(&u, &x, 4); return u; }
+static float u2f(uint32_t u) { float x; memcpy(&x, &u, 4); return x; }
+
+float hgo_bf16_to_f32(uint16_t h) { return u2f((uint32_t)h << 16); }
+
+/* Round to nearest, ties to even, on the fp32 bit pattern (finite inputs). */
+uint16_t hgo_bf16_rne(float x) {
+  uint32_t u = f2u(x);
+  uint32_t hi = u >> 16, lo = u & 0xFFFFu;
+  if (lo > 0x8000u || (lo == 0x8000u && (hi & 1u))) hi += 1; /* magnitude up */
+  return (uint16_t)hi;
+}
+
+/* Round toward -infinity: drop the low half, then for a negative value with
+ * a nonzero dropped part step one BF16 unit further from zero. */
+uint16_t hgo_bf16_rd(float x) {
+  uint32_t u = f2u(x);
+  uint32_t hi = u >> 16, lo = u & 0xFFFFu;
+  if (lo != 0 && (u >> 31)) hi += 1;
+  return (uint16_t)hi;
+}
+
+/* Round toward +infinity: the mirror of hgo_bf16_rd. */
+uint16_t hgo_bf16_ru(float x) {
+  uint32_t u = f2u(x);
+  uint32_t hi = u >> 16, lo = u & 0xFFFFu;
+  if (lo != 0 && !(u >> 31)) hi += 1;
+  return (uint16_t)hi;
+}
+
+/* ------------------------------------------------------- the base quantizer
+ *
+ * Readings (the paper fixes none of these):
+ *  - levels: 2^b values m + k*S, k = 0..2^b-1, spanning the group's range;
+ *  - metadata: min stored as BF16 rounded down, scale as BF16 rounded up, so
+ *    the stored grid still covers [min, max]; 16 + 16 = 32 bits per group;
+ *    a zero of either sign is stored as +0;
+ *  - a positive scale below 2^-126 is raised to 2^-126 so 1/S is finite;
+ *  - zero range (S == 0): every code is 0 and the group reconstructs to m;
+ *  - code = clamp(rint((v - m) * (1/S)), 0, 2^b-1), rint ties to even, with
+ *    one correctly rounded reciprocal per group and no fused multiply-add.
+ */
+uint32_t hgo_quantize_group(const float* v, int m, int stride, int bits,
+                            uint8_t* q, int qstride) {
+  float mn = v[0], mx = v[0];
+  for (int i = 1; i < m; ++i) {
+    float x = v[(size_t)i * stride];
+    if (x < mn) mn = x;
+    if (x > mx) mx = x;
+  }
+  uint16_t m16 = hgo_bf16_rd(mn);
+  if (m16 == 0x8000u) m16 = 0;
+  float mf = hgo_bf16_to_f32(m16);
+
+  int levels = (1 << bits) - 1;
+  float s = (mx - mf) / (float)levels;
+  uint16_t s16 = hgo_bf16_ru(s);
+  if (s16 == 0x8000u) s16 = 0;
+  if (s16 != 0 && hgo_bf16_to_f32(s16) < 0x1p-126f) s16 = 0x0080u; /* 2^-126 */
+  float S = hgo_bf16_to_f32(s16);
+
+  if (s16 == 0) {
+    for (int i = 0; i < m; ++i) q[(size_t)i * qstride] = 0;
+  } else {
+    float inv = 1.0f / S;
+    for (int i = 0; i < m; ++i) {
+      float t = (v[(size_t)i * stride] - mf) * inv;
+      float r = rintf(t);
+      if (r < 0.0f) r = 0.0f;
+      if (r > (float)levels) r = (float)levels;
+      q[(size_t)i * qstride] = (uint8_t)(unsigned)r;
+    }
+  }
+  return (uint32_t)s16 | ((uint32_t)m16 << 16);
+}
+
+float hgo_level(uint32_t meta, unsigned q) {
+  float S = hgo_bf16_to_f32((uint16_t)(meta & 0xFFFFu));
+  float m = hgo_bf16_to_f32((uint16_t)(meta >> 16));
+  float p = (float)q * S; /* exact: q < 2^8, S has 8 significant bits */
+  return p + m;
+}
+
+/* ------------------------------------------------- Walsh-Hadamard rotation
+ *
+ * Reading: the rotation is the normalized Walsh-Hadamard matrix in natural
+ * (Sylvester) order, H[i][j] = (-1)^popcount(i & j) / sqrt(D), applied as the
+ * fast transform in fp32 with butterfly spans 1, 2, 4, ..., D/2 (each
+ * butterfly rounds once), followed by one multiply by fp32(1/sqrt(D)).
+ */
+void hgo_fwht_raw(float* a, int D) {
+  for (int h = 1; h < D; h *= 2) {
+    for (int i = 0; i < D; i += 2 * h) {
+      for (int j = i; j < i + h; ++j) {
+        float p = a[j], q = a[j + h];
+        a[j] = p + q;
+        a[j + h] = p - q;
+      }
+    }
+  }
+}
+
+float hgo_fwht_scale(int D) { return (float)(1.0 / sqrt((double)D)); }
+
+void hgo_fwht_norm(float* a, int D) {
+  hgo_fwht_raw(a, D);
+  float c = hgo_fwht_scale(D);
+  for (int j = 0; j < D; ++j) a[j] = a[j] * c;
+}
+
+/* ------------------------------------------------------------------ routing */
+
+static int cfg_ok(const hgo_config* c) {
+  if (!c) return 0;
+  if (c->L <= 0 || c->B <= 0 || c->H <= 0 || c->T <= 0 || c->D <= 0) return 0;
+  if (c->img_start < 0 || c->img_len < 0 || c->img_start + c->img_len > c->T) return 0;
+  if (c->bits < 1 || c->bits > 8) return 0;
+  if ((c->D * c->bits) % 8 != 0) return 0;
+  if (c->base < HGO_MINMAX || c->base > HGO_AKVQ) return 0;
+  if (c->base == HGO_KIVI && c->kivi_group <= 0) return 0;
+  if (c->base == HGO_AKVQ && (c->D & (c->D - 1)) != 0) return 0;
+  return 1;
+}
+
+/* Protection (§3): K of a selected head is kept; V of a selected head is kept
+ * only in K+V mode.  Slots are ranks in row-major (l, h) order. */
+static int is_kept(const hgo_config* c, const uint8_t* mask, int X, int i) {
+  if (!mask[i]) return 0;
+  return X == 0 ? 1 : !c->keys_only;
+}
+
+int hgo_route(const hgo_config* c, const uint8_t* mask, int X, int l, int h,
+              int* is_protected, int* slot) {
+  if (!cfg_ok(c) || !mask || X < 0 || X > 1 || l < 0 || l >= c->L || h < 0 || h >= c->H)
+    return -1;
+  int i = l * c->H + h;
+  int kept = is_kept(c, mask, X, i);
+  int rank = 0;
+  for (int j = 0; j < i; ++j)
+    if (is_kept(c, mask, X, j) == kept) rank++;
+  *is_protected = kept;
+  *slot = rank;
+  return 0;
+}
+
+static int kivi_keys(const hgo_config* c, int X) { return c->base == HGO_KIVI && X == 0; }
+
+static uint64_t meta_words_per_slice(const hgo_config* c, int X) {
+  if (kivi_keys(c, X)) {
+    uint64_t ng = ((uint64_t)c->img_len + c->kivi_group - 1) / c->kivi_group;
+    return ng * (uint64_t)c->D;
+  }
+  return (uint64_t)c->img_len;
+}
+
+int hgo_sizes(const hgo_config* c, const uint8_t* mask, hgo_sizes_t* out) {
+  if (!cfg_ok(c) || !mask || !out) return -1;
+  int LH = c->L * c->H, P = 0;
+  for (int i = 0; i < LH; ++i) P += mask[i] ? 1 : 0;
+  int uk = LH - P;
+  int uv = c->keys_only ? LH : LH - P;
+  int pv = c->keys_only ? 0 : P;
+  uint64_t n = (uint64_t)c->img_len, B = (uint64_t)c->B, D = (uint64_t)c->D;
+  uint64_t row = D * (uint64_t)c->bits / 8;
+  out->n_protected = P;
+  out->n_unprot_k = uk;
+  out->n_unprot_v = uv;
+  out->codes_k = (uint64_t)uk * B * n * row;
+  out->codes_v = (uint64_t)uv * B * n * row;
+  out->meta_k = (uint64_t)uk * B * meta_words_per_slice(c, 0) * 4;
+  out->meta_v = (uint64_t)uv * B * meta_words_per_slice(c, 1) * 4;
+  out->side_k = (uint64_t)P * B * n * D * 2;
+  out->side_v = (uint64_t)pv * B * n * D * 2;
+  return 0;
+}
+
+/* ------------------------------------------------------ bit packing (LSB-first) */
+
+static void put_code(uint8_t* row, int bits, int i, unsigned q) {
+  for (int k = 0; k < bits; ++k) {
+    int pos = bits * i + k;
+    if ((q >> k) & 1u) row[pos / 8] |= (uint8_t)(1u << (pos % 8));
+  }
+}
+
+static unsigned get_code(const uint8_t* row, int bits, int i) {
+  unsigned q = 0;
+  for (int k = 0; k < bits; ++k) {
+    int pos = bits * i + k;
+    if ((row[pos / 8] >> (pos % 8)) & 1u) q |= 1u << k;
+  }
+  return q;
+}
+
+/* ------------------------------------------------------------ one slice */
+
+int hgo_quantize_slice(const hgo_config* c, int X, const uint16_t* rows,
+                       uint8_t* codes, uint32_t* meta) {
+  if (!cfg_ok(c) || X < 0 || X > 1) return -1;
+  int n = c->img_len, D = c->D, b = c->bits;
+  size_t row_bytes = (size_t)D * b / 8;
+  memset(codes, 0, (size_t)n * row_bytes);
+
+  float* v = (float*)malloc(sizeof(float) * (size_t)D * (kivi_keys(c, X) ? c->kivi_group : 1));
+  uint8_t* q = (uint8_t*)malloc((size_t)D * (kivi_keys(c, X) ? c->kivi_group : 1));
+  if (!v || !q) { free(v); free(q); return -1; }
+
+  if (kivi_keys(c, X)) {
+    /* Keys per channel: each channel's range over a group of G consecutive
+     * image tokens (the last group may be shorter). */
+    int G = c->kivi_group;
+    for (int g0 = 0, g = 0; g0 < n; g0 += G, ++g) {
+      int m = (n - g0 < G) ? n - g0 : G;
+      for (int d = 0; d < D; ++d) {
+        for (int t = 0; t < m; ++t) v[t] = hgo_bf16_to_f32(rows[(size_t)(g0 + t) * D + d]);
+        meta[(size_t)g * D + d] = hgo_quantize_group(v, m, 1, b, q, 1);
+        for (int t = 0; t < m; ++t) put_code(codes + (size_t)(g0 + t) * row_bytes, b, d, q[t]);
+      }
+    }
+  } else {
+    /* One group per token vector; AKVQ-style keys are rotated first. */
+    for (int t = 0; t < n; ++t) {
+      for (int d = 0; d < D; ++d) v[d] = hgo_bf16_to_f32(rows[(size_t)t * D + d]);
+      if (c->base == HGO_AKVQ && X == 0) hgo_fwht_norm(v, D);
+      meta[t] = hgo_quantize_group(v, D, 1, b, q, 1);
+      for (int d = 0; d < D; ++d) put_code(codes + (size_t)t * row_bytes, b, d, q[d]);
+    }
+  }
+  free(v);
+  free(q);
+  return 0;
+}
+
+int hgo_dequantize_slice(const hgo_config* c, int X, const uint8_t* codes,
+                         const uint32_t* meta, uint16_t* rows_out) {
+  if (!cfg_ok(c) || X < 0 || X > 1) return -1;
+  int n = c->img_len, D = c->D, b = c->bits;
+  size_t row_bytes = (size_t)D * b / 8;
+  float* y = (float*)malloc(sizeof(float) * (size_t)D);
+  if (!y) return -1;
+  for (int t = 0; t < n; ++t) {
+    const uint8_t* row = codes + (size_t)t * row_bytes;
+    for (int d = 0; d < D; ++d) {
+      uint32_t w = kivi_keys(c, X) ? meta[(size_t)(t / c->kivi_group) * D + d] : meta[t];
+      y[d] = hgo_level(w, get_code(row, b, d));
+    }
+    /* AKVQ-style keys come back to the original basis: H is symmetric and
+     * orthonormal, so the inverse rotation is the same transform. */
+    if (c->base == HGO_AKVQ && X == 0) hgo_fwht_norm(y, D);
+    for (int d = 0; d < D; ++d) rows_out[(size_t)t * D + d] = hgo_bf16_rne(y[d]);
+  }
+  free(y);
+  return 0;
+}
+
+/* ------------------------------------------------------------ whole cache */
+
+typedef struct {
+  const hgo_config* c;
+  const uint8_t* mask;
+  const uint16_t* in[2];
+  uint8_t* codes[2];
+  uint32_t* meta[2];
+  uint16_t* side[2];
+  uint16_t* out[2];
+  int dequant;
+  int tid, nthreads;
+  int status;
+} job_t;
+
+static void* run_slices(void* arg) {
+  job_t* j = (job_t*)arg;
+  const hgo_config* c = j->c;
+  int n = c->img_len, D = c->D;
+  size_t row_bytes = (size_t)D * c->bits / 8;
+  long nslices = 2L * c->L * c->B * c->H;
+  for (long s = j->tid; s < nslices; s += j->nthreads) {
+    int X = (int)(s / ((long)c->L * c->B * c->H));
+    long r = s % ((long)c->L * c->B * c->H);
+    int l = (int)(r / ((long)c->B * c->H));
+    int b = (int)((r / c->H) % c->B);
+    int h = (int)(r % c->H);
+    int prot, slot;
+    if (hgo_route(c, j->mask, X, l, h, &prot, &slot) != 0) { j->status = -1; return NULL; }
+    size_t cache_off = ((((size_t)l * c->B + b) * c->H + h) * c->T + c->img_start) * D;
+    size_t slab = (size_t)slot * c->B + b; /* [slot][B] */
+    uint16_t* side = j->side[X] ? j->side[X] + slab * n * D : NULL;
+    if (!j->dequant) {
+      const uint16_t* rows = j->in[X] + cache_off;
+      if (prot) {
+        memcpy(side, rows, (size_t)n * D * 2);
+      } else if (hgo_quantize_slice(c, X, rows, j->codes[X] + slab * n * row_bytes,
+                                    j->meta[X] + slab * meta_words_per_slice(c, X)) != 0) {
+        j->status = -1;
+        return NULL;
+      }
+    } else {
+      uint16_t* rows = j->out[X] + cache_off;
+      if (prot) {
+        memcpy(rows, side, (size_t)n * D * 2);
+      } else if (hgo_dequantize_slice(c, X, j->codes[X] + slab * n * row_bytes,
+                                      j->meta[X] + slab * meta_words_per_slice(c, X), rows) != 0) {
+        j->status = -1;
+        return NULL;
+      }
+    }
+  }
+  return NULL;
+}
+
+static int run_all(job_t* proto, int threads) {
+  if (threads < 1) threads = 1;
+  job_t* jobs = (job_t*)calloc((size_t)threads, sizeof(job_t));
+  pthread_t* th = (pthread_t*)calloc((size_t)threads, sizeof(pthread_t));
+  if (!jobs || !th) { free(jobs); free(th); return -1; }
+  for (int t = 0; t < threads; ++t) {
+    jobs[t] = *proto;
+    jobs[t].tid = t;
+    jobs[t].nthreads = threads;
+    jobs[t].status = 0;
+  }
+  int started = 0;
+  for (int t = 1; t < threads; ++t)
+    if (pthread_create(&th[t], NULL, run_slices, &jobs[t]) == 0) started = t; else break;
+  int status = 0;
+  if (started != threads - 1) {
+    /* Could not start every worker: fall back to doing all slices here. */
+    for (int t = 1; t <= started; ++t) pthread_join(th[t], NULL);
+    jobs[0].nthreads = 1;
+    run_slices(&jobs[0]);
+    status = jobs[0].status;
+  } else {
+    run_slices(&jobs[0]);
+    for (int t = 1; t < threads; ++t) pthread_join(th[t], NULL);
+    for (int t = 0; t < threads; ++t) if (jobs[t].status) status = -1;
+  }
+  free(jobs);
+  free(th);
+  return status;
+}
+
+int hgo_quantize(const hgo_config* c, const uint16_t* K, const uint16_t* V,
+                 const uint8_t* mask,
+                 uint8_t* codes_k, uint32_t* meta_k, uint16_t* side_k,
+                 uint8_t* codes_v, uint32_t* meta_v, uint16_t* side_v,
+                 int threads) {
+  if (!cfg_ok(c) || !K || !V || !mask) return -1;
+  job_t j;
+  memset(&j, 0, sizeof j);
+  j.c = c; j.mask = mask;
+  j.in[0] = K; j.in[1] = V;
+  j.codes[0] = codes_k; j.codes[1] = codes_v;
+  j.meta[0] = meta_k; j.meta[1] = meta_v;
+  j.side[0] = side_k; j.side[1] = side_v;
+  return run_all(&j, threads);
+}
+
+int hgo_dequantize(const hgo_config* c, const uint8_t* mask,
+                   const uint8_t* codes_k, const uint32_t* meta_k,
+                   const uint16_t* side_k,
+                   const uint8_t* codes_v, const uint32_t* meta_v,
+                   const uint16_t* side_v,
+                   uint16_t* K_out, uint16_t* V_out, int threads) {
+  if (!cfg_ok(c) || !mask || !K_out || !V_out) return -1;
+  job_t j;
+  memset(&j, 0, sizeof j);
+  j.c = c; j.mask = mask; j.dequant = 1;
+  j.codes[0] = (uint8_t*)codes_k; j.codes[1] = (uint8_t*)codes_v;
+  j.meta[0] = (uint32_t*)meta_k; j.meta[1] = (uint32_t*)meta_v;
+  j.side[0] = (uint16_t*)side_k; j.side[1] = (uint16_t*)side_v;
+  j.out[0] = K_out; j.out[1] = V_out;
+  return run_all(&j, threads);
+}

@@ -1,0 +1,90 @@
+"""The oracle's pins must catch plausible slips.  Each case plants one mistake
+in a copy of the oracle source (on the CPU, in a temporary directory), builds
+it, and runs the pin suites against the mutant: at least one pin must fail.
+The planted mistakes cover each step of the method: rounding directions and
+tie rules, the range, the scale and its levels, reconstruction, the
+Walsh-Hadamard butterflies and scale, routing ranks and K-only protection,
+KIVI-style group indexing, bit packing, the image-span offset and the
+buffer sizes."""
+import concurrent.futures as cf
+import os
+import shutil
+import subprocess
+import sys
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "hg_oracle.c")
+
+MUTANTS = [
+    ("rint_ties_away", "float r = rintf(t);", "float r = roundf(t);"),
+    ("rd_wrong_direction", "if (lo != 0 && (u >> 31)) hi += 1;", "if (lo != 0 && !(u >> 31)) hi += 1;"),
+    ("ru_truncates", "if (lo != 0 && !(u >> 31)) hi += 1;", "if (0) hi += 1;"),
+    ("rne_ties_away", "(lo == 0x8000u && (hi & 1u))", "(lo == 0x8000u)"),
+    ("min_sign", "if (x < mn) mn = x;", "if (x > mn) mn = x;"),
+    ("max_init", "float mn = v[0], mx = v[0];", "float mn = v[0], mx = 0.0f;"),
+    ("scale_uses_raw_min", "float s = (mx - mf) / (float)levels;", "float s = (mx - mn) / (float)levels;"),
+    ("levels_off_by_one", "int levels = (1 << bits) - 1;", "int levels = (1 << bits);"),
+    ("scale_round_nearest", "uint16_t s16 = hgo_bf16_ru(s);", "uint16_t s16 = hgo_bf16_rne(s);"),
+    ("min_round_nearest", "uint16_t m16 = hgo_bf16_rd(mn);", "uint16_t m16 = hgo_bf16_rne(mn);"),
+    ("clamp_off_by_one", "if (r > (float)levels) r = (float)levels;",
+     "if (r > (float)levels - 1) r = (float)levels - 1;"),
+    ("recon_sign", "return p + m;", "return p - m;"),
+    ("recon_meta_halves_swapped",
+     "float S = hgo_bf16_to_f32((uint16_t)(meta & 0xFFFFu));\n  float m = hgo_bf16_to_f32((uint16_t)(meta >> 16));",
+     "float S = hgo_bf16_to_f32((uint16_t)(meta >> 16));\n  float m = hgo_bf16_to_f32((uint16_t)(meta & 0xFFFFu));"),
+    ("fwht_sign", "a[j + h] = p - q;", "a[j + h] = q - p;"),
+    ("fwht_missing_stage", "for (int h = 1; h < D; h *= 2)", "for (int h = 1; h < D / 2; h *= 2)"),
+    ("fwht_missing_scale", "for (int j = 0; j < D; ++j) a[j] = a[j] * c;", "(void)c;"),
+    ("route_rank_counts_all", "if (is_kept(c, mask, X, j) == kept) rank++;", "rank++;"),
+    ("k_only_protects_values", "return X == 0 ? 1 : !c->keys_only;", "return 1;"),
+    ("kivi_meta_transposed", "meta[(size_t)g * D + d] = hgo_quantize_group(v, m, 1, b, q, 1);",
+     "meta[(size_t)d * ((n + G - 1) / G) + g] = hgo_quantize_group(v, m, 1, b, q, 1);"),
+    ("kivi_group_offset_dropped", "v[t] = hgo_bf16_to_f32(rows[(size_t)(g0 + t) * D + d]);",
+     "v[t] = hgo_bf16_to_f32(rows[(size_t)t * D + d]);"),
+    ("pack_msb_first", "if ((q >> k) & 1u) row[pos / 8] |= (uint8_t)(1u << (pos % 8));",
+     "if ((q >> k) & 1u) row[pos / 8] |= (uint8_t)(1u << (7 - pos % 8));"),
+    ("span_offset_dropped", "c->T + c->img_start) * D;", "c->T) * D;"),
+    ("akvq_no_inverse_rotation", "if (c->base == HGO_AKVQ && X == 0) hgo_fwht_norm(y, D);", "(void)0;"),
+    ("akvq_rotates_values", "if (c->base == HGO_AKVQ && X == 0) hgo_fwht_norm(v, D);",
+     "if (c->base == HGO_AKVQ) hgo_fwht_norm(v, D);"),
+    ("kivi_meta_size_per_token", "return ng * (uint64_t)c->D;", "return ng;"),
+    ("k_only_side_v_sized", "int pv = c->keys_only ? 0 : P;", "int pv = P;"),
+    ("negative_zero_min_kept", "if (m16 == 0x8000u) m16 = 0;", ""),
+    ("no_scale_floor", "if (s16 != 0 && hgo_bf16_to_f32(s16) < 0x1p-126f) s16 = 0x0080u; /* 2^-126 */", ""),
+    ("zero_range_not_special", "if (s16 == 0) {", "if (s16 == 0 && 0) {"),
+]
+
+
+def _run_mutant(name, old, new, tmp):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"{name}: pattern must occur exactly once"
+    d = os.path.join(tmp, name)
+    os.makedirs(d)
+    shutil.copy(os.path.join(ROOT, "oracle", "hg_oracle.h"), d)
+    with open(os.path.join(d, "hg_oracle.c"), "w") as f:
+        f.write(src.replace(old, new))
+    so = os.path.join(d, "lib.so")
+    subprocess.check_call(["gcc", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fPIC",
+                           "-shared", "-pthread", "-w", "-o", so,
+                           os.path.join(d, "hg_oracle.c"), "-lm"])
+    env = dict(os.environ, HG_ORACLE_LIB=so, OMP_NUM_THREADS="1")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_cache.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    return name, r.returncode
+
+
+def test_every_planted_mistake_fails_a_pin():
+    tmp = tempfile.mkdtemp(prefix="hg_mutants_")
+    try:
+        workers = max(1, min(8, (os.cpu_count() or 2)))
+        with cf.ThreadPoolExecutor(workers) as ex:
+            results = list(ex.map(lambda m: _run_mutant(*m, tmp), MUTANTS))
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+    survivors = [n for n, rc in results if rc == 0]
+    assert not survivors, f"mutants not caught by any pin: {survivors}"
