@@ -1,0 +1,209 @@
+"""Bench: one step = quantize+pack and dequantize of a whole synthetic KV cache
+(every layer, batch row and KV head; K and V) through libheadguard on one
+MI355X.  Prints one JSON line.
+
+Default workload: the Qwen2.5-VL-7B-shaped cache (28 layers x 8 rows x 4 KV
+heads x 1360 tokens x head_dim 128, 1296 image tokens, 2-bit per-token
+min-max, 14 of 112 heads protected, K+V), inputs resident in HBM.
+
+Algorithmic bytes per call: every image row of K and V is read once
+(2 bytes per element) and the packed outputs (codes, metadata, BF16 side
+store) are written once; dequantize moves the same bytes in the other
+direction.  Text rows are never touched.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
+QUANT_KERNEL = "quantize_kernel"
+KERNEL_SOURCES = ("paper_2609_35800_amd/csrc/quantize.hip", "paper_2609_35800_amd/csrc/hg_device.h",
+                  "paper_2609_35800_amd/csrc/hg_kernels.h")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen2.5-vl-7b")
+    ap.add_argument("--bits", type=int, default=None, help="override the workload's bit width")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="approximate CPU time budget of the oracle sample")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (for counter scaling)")
+    ap.add_argument("--quant-only", action="store_true",
+                    help="time only the quantize launches (for profiling that kernel)")
+    return ap.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(workload: str, bits: int):
+    """HBM bytes per quantize launch measured by rocprofv3 counters, if the
+    committed measurement was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{QUANT_KERNEL}_{workload}_b{bits}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def algorithmic_bytes(w, sizes) -> dict:
+    img_elems = w.L * w.B * w.H * w.img_len * w.D
+    read = 2 * img_elems * 2  # K and V image rows, BF16
+    write = sum(sizes[n] for n in ("codes_k", "meta_k", "side_k", "codes_v", "meta_v", "side_v"))
+    return {"quant": read + write, "dequant": read + write, "read": read, "write": write}
+
+
+def cpu_baseline(w, K, V, mask, budget_s: float):
+    """The CPU oracle on a bounded sample of the same workload: its first
+    layers (all batch rows and heads, K and V), quantize then dequantize."""
+    import oracle  # test infrastructure: the CPU baseline leg only
+    import synthkv
+    threads = max(1, min(os.cpu_count() or 1, 16))
+    # calibrate on one layer, then size the sample to the time budget
+    def run(nl):
+        sub = w.with_(L=nl)
+        cfg = oracle.make_config(**sub.config_fields())
+        m = np.ascontiguousarray(mask[: nl * w.H])
+        Kb = synthkv.bf16_bits(K[:nl])
+        Vb = synthkv.bf16_bits(V[:nl])
+        t0 = time.perf_counter()
+        pk = oracle.quantize(cfg, Kb, Vb, m, threads=threads)
+        Ko = np.zeros_like(Kb)
+        Vo = np.zeros_like(Vb)
+        oracle.dequantize(cfg, m, pk, Ko, Vo, threads=threads)
+        dt = time.perf_counter() - t0
+        sizes = {n: int(v.nbytes) for n, v in pk.items()}
+        return dt, algorithmic_bytes(sub, sizes)
+    dt1, _ = run(1)
+    nl = int(max(1, min(w.L, budget_s / max(dt1, 1e-3))))
+    dt, ab = run(nl)
+    total = ab["quant"] + ab["dequant"]
+    return {"value": round(total / dt / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{nl} of {w.L} layers of the same workload (all rows, heads, K and V), "
+                      f"quantize+dequantize, {dt:.2f} s wall",
+            # whole-cache image tokens scaled by the fraction of layers done
+            "image_tokens_per_s": round(w.B * w.img_len * nl / w.L / dt, 1)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
+              "(the quantizer's slices are independent; sharding is by KV head, layer or "
+              "batch row with no communication).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_35800_amd as hg
+    import synthkv
+
+    w = synthkv.WORKLOADS[args.workload]
+    if args.bits is not None:
+        w = w.with_(bits=args.bits)
+    mask = synthkv.protect_mask(w)
+    cfg = hg.make_config(**w.config_fields())
+    sizes = hg.hg_packed_sizes(cfg, mask)
+    ab = algorithmic_bytes(w, sizes)
+
+    K, V = synthkv.gen_kv(w, device="cuda")
+    packed = hg.alloc_packed(cfg, mask)
+    Ko = torch.empty_like(K)
+    Vo = torch.empty_like(V)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        hg.hg_quantize(cfg, K, V, mask, packed, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        if not args.quant_only:
+            hg.hg_dequantize(cfg, mask, packed, Ko, Vo, stream=stream)
+            if ev is not None:
+                ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    q_ms = [e[0].elapsed_time(e[1]) for e in events]
+    d_ms = [e[1].elapsed_time(e[2]) for e in events] if not args.quant_only else [0.0]
+    q_avg = float(np.mean(q_ms))
+    d_avg = float(np.mean(d_ms))
+    step_bytes = ab["quant"] + (0 if args.quant_only else ab["dequant"])
+    value = step_bytes * args.steps / elapsed / 1e9
+    q_gbps = ab["quant"] / (q_avg * 1e-3) / 1e9
+    d_gbps = ab["dequant"] / (d_avg * 1e-3) / 1e9 if not args.quant_only else None
+    traffic = traffic_from_profile(w.name, w.bits)
+
+    if args.copy_calibration:
+        n = 1 << 30
+        a = torch.empty(n, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+
+    out = {
+        "metric": "quantize+pack+dequant HBM GB/s (% of MI355X peak); image KV tokens/s",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded N(0,1) BF16 KV with outlier key channels; no model weights)",
+        "config": {"workload": w.name, "L": w.L, "B": w.B, "H_kv": w.H, "T": w.T, "D": w.D,
+                   "img_start": w.img_start, "img_len": w.img_len, "bits": w.bits,
+                   "base": w.base, "keys_only": w.keys_only, "protected_heads": int(mask.sum()),
+                   "parallelism": "single GPU"},
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
+        "image_tokens_per_s": round(w.B * w.img_len * args.steps / elapsed, 1),
+        "quantize": {"ms": round(q_avg, 4), "GBps": round(q_gbps, 1),
+                     "bytes": ab["quant"], "image_tokens_per_s": round(w.B * w.img_len / (q_avg * 1e-3), 1)},
+        "dequantize": None if args.quant_only else
+                      {"ms": round(d_avg, 4), "GBps": round(d_gbps, 1), "bytes": ab["dequant"]},
+        "roofline": {"bound": "hbm", "kernel": QUANT_KERNEL, "achieved": round(q_gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(q_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, K, V, mask, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,133 @@
+/*
+ * headguard.h -- C ABI of libheadguard, the MI355X (gfx950) head-masked
+ * low-bit image-KV quantizer of HeadGuard (arXiv 2609.35800).
+ *
+ * The operation (§3 "HeadGuard" and "Applying protection"; §4 "Quantization
+ * setup"): given a model's KV cache, the positions of its image tokens, a fixed
+ * protection mask over physical KV heads and a base quantizer, every image-token
+ * key/value vector of an unprotected head is quantized by the base to b bits;
+ * the protected heads keep their image keys (and values, in K+V mode) in BF16;
+ * text KV is left alone.  A compatible base must be able to skip individual
+ * heads (§3), which is what the mask routing does.
+ *
+ * Bases (§2 "KV-cache quantization", §4 "Quantization setup"):
+ *   HG_BASE_MINMAX  per-token min-max round-to-nearest for keys and values;
+ *   HG_BASE_KIVI    keys per channel over groups of `kivi_group` consecutive
+ *                   image tokens, values per token;
+ *   HG_BASE_AKVQ    keys rotated by the normalized Walsh-Hadamard matrix over
+ *                   head_dim, then per token; values per token, unrotated.
+ *
+ * Quantizer of one group of values v (a token vector, or one channel of a
+ * KIVI key group), all in IEEE fp32 with round-to-nearest-even:
+ *   m = BF16 rounded toward -inf of min(v)     (a zero is stored as +0)
+ *   s = (max(v) - m) / (2^b - 1)               (correctly rounded)
+ *   S = BF16 rounded toward +inf of s          (+0 if zero; at least 2^-126)
+ *   q = clamp(rint((v - m) * (1/S)), 0, 2^b-1) (rint ties to even; q = 0 if S = 0)
+ *   metadata word = bits(S) | bits(m) << 16    (32 bits per group, §5.4)
+ * Reconstruction: x^ = bf16_rne(q*S + m); for AKVQ keys the fp32 values
+ * q*S + m are rotated back (the transform is its own inverse) before the BF16
+ * rounding.  The rotation is the fast transform in fp32, butterfly spans
+ * 1, 2, ..., D/2, then one multiply by fp32(1/sqrt(D)).
+ *
+ * Layouts (little-endian, row-major, n = img_len):
+ *   K, V      BF16 [L][B][H][T][D], contiguous
+ *   codes_X   [slot][B][n][D*bits/8]  token-major, code of channel d at bits
+ *             [bits*d, bits*d + bits) of the token's row, least significant first
+ *   meta_X    u32 [slot][B][n]                 per-token groups
+ *             u32 [slot][B][ceil(n/G)][D]      KIVI keys, G = kivi_group
+ *   side_X    BF16 [p][B][n][D]  image rows of protected heads, bit-identical
+ * slot = rank of (l, h) in row-major order among the heads whose X is
+ * quantized; p = rank among the heads whose X is kept in BF16.  V is kept iff
+ * the head is protected and keys_only == 0.
+ *
+ * Ownership and synchronisation: the caller allocates every buffer.  Device
+ * buffers are device memory of the current HIP device; the mask is host
+ * memory read during the call only.  The library allocates nothing, keeps no
+ * state between calls and never synchronises: HG_OK means the work is
+ * enqueued on `stream`; device faults surface at the caller's next
+ * synchronisation.  Every argument check runs before any launch, so on error
+ * no output is touched.  Calls are thread-safe; the error detail is per thread.
+ *
+ * Preconditions not checked: inputs finite with |x| < 2^100; buffers at least
+ * the sizes hg_packed_sizes reports; no overlap between inputs and outputs.
+ */
+#ifndef HEADGUARD_H
+#define HEADGUARD_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { HG_BASE_MINMAX = 0, HG_BASE_KIVI = 1, HG_BASE_AKVQ = 2 } hg_base;
+
+enum {
+  HG_OK = 0,
+  HG_ERR_NULL = 1,      /* a required pointer is NULL                          */
+  HG_ERR_SHAPE = 2,     /* L, B, H, T not positive, or L*H > HG_MAX_HEADS      */
+  HG_ERR_SPAN = 3,      /* image span outside [0, T]                           */
+  HG_ERR_BITS = 4,      /* bits not in {2, 3, 4}                               */
+  HG_ERR_BASE = 5,      /* unknown base, or kivi_group unsupported             */
+  HG_ERR_HEADDIM = 6,   /* D not in {64, 128}                                  */
+  HG_ERR_ALIGN = 7,     /* a device pointer is not 16-byte aligned             */
+  HG_ERR_MASK = 8,      /* a mask entry is neither 0 nor 1                     */
+  HG_ERR_NO_DEVICE = 9, /* no usable HIP device                                */
+  HG_ERR_HIP = 10,      /* the HIP runtime reported an error (launch, pointer) */
+  HG_ERR_POINTER = 11   /* a buffer argument is not device memory              */
+};
+
+/* Largest L*H the mask routing holds in kernel arguments. */
+#define HG_MAX_HEADS 8192
+
+typedef struct {
+  int32_t L, B, H, T, D;       /* cache shape [L][B][H][T][D]                      */
+  int32_t img_start, img_len;  /* image span [img_start, img_start + img_len),
+                                  shared by every batch row; img_len may be 0      */
+  int32_t bits;                /* 2, 3 or 4                                        */
+  int32_t base;                /* hg_base                                          */
+  int32_t keys_only;           /* 1: protect K only; 0: protect K and V            */
+  int32_t kivi_group;          /* tokens per KIVI key group (32); ignored otherwise */
+} hg_config;
+
+typedef struct {
+  uint64_t codes_k, meta_k, side_k, codes_v, meta_v, side_v; /* bytes          */
+  int32_t n_protected;         /* heads with mask = 1                             */
+  int32_t n_unprot_k, n_unprot_v; /* heads whose K / V are quantized              */
+} hg_sizes;
+
+typedef struct {
+  void *codes_k, *meta_k, *side_k, *codes_v, *meta_v, *side_v; /* device */
+} hg_packed;
+
+/* Byte sizes of the six packed buffers (the storage model of §5.4).  Pure
+ * host computation; needs no device.  `protect_mask` is host uint8 [L*H],
+ * row-major (l, h), entries 0 or 1. */
+int hg_packed_sizes(const hg_config* cfg, const uint8_t* protect_mask, hg_sizes* out);
+
+/* Quantize and pack the image KV of the whole cache (§3, §4).
+ * K, V: device BF16 bit patterns, layout above.  `out` buffers: device memory
+ * of at least the hg_packed_sizes sizes; a buffer whose size is 0 may be NULL.
+ * Every device pointer must be 16-byte aligned (torch allocations are). */
+int hg_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
+                const uint8_t* protect_mask, const hg_packed* out, hipStream_t stream);
+
+/* Reconstruct the image rows of K_out, V_out (device BF16, same layout and
+ * shape as K, V) from the packed buffers (simulated quantization's
+ * reconstruction, §4).  Protected rows are copied back from the side store;
+ * text rows of K_out, V_out are not written. */
+int hg_dequantize(const hg_config* cfg, const uint8_t* protect_mask, const hg_packed* in,
+                  uint16_t* K_out, uint16_t* V_out, hipStream_t stream);
+
+/* Static name of a status code. */
+const char* hg_status_string(int status);
+
+/* Detail of the last non-OK status returned on the calling thread ("" if none). */
+const char* hg_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HEADGUARD_H */

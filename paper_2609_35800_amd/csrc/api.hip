@@ -1,0 +1,254 @@
+// Host side of libheadguard: argument checks, the packed-size closed form,
+// mask routing into kernel arguments, and kernel launch.  Declarations and
+// the contract of every entry point are in include/headguard.h.
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "headguard.h"
+#include "hg_kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+int ok() {
+  g_last_error.clear();
+  return HG_OK;
+}
+
+// Shape, span, bits, base and mask checks shared by every entry point.
+int check_config(const hg_config* c, const uint8_t* mask) {
+  if (!c) return fail(HG_ERR_NULL, "cfg is NULL");
+  if (!mask) return fail(HG_ERR_NULL, "protect_mask is NULL");
+  if (c->L <= 0 || c->B <= 0 || c->H <= 0 || c->T <= 0)
+    return fail(HG_ERR_SHAPE, "L, B, H, T must be positive (got %d, %d, %d, %d)", c->L, c->B, c->H, c->T);
+  if ((int64_t)c->L * c->H > HG_MAX_HEADS)
+    return fail(HG_ERR_SHAPE, "L*H = %lld exceeds %d", (long long)c->L * c->H, HG_MAX_HEADS);
+  if (c->D != 64 && c->D != 128) return fail(HG_ERR_HEADDIM, "head_dim %d not in {64, 128}", c->D);
+  if (c->img_start < 0 || c->img_len < 0 || (int64_t)c->img_start + c->img_len > c->T)
+    return fail(HG_ERR_SPAN, "image span [%d, %d + %d) outside [0, %d]", c->img_start, c->img_start,
+                c->img_len, c->T);
+  if (c->bits < 2 || c->bits > 4) return fail(HG_ERR_BITS, "bits %d not in {2, 3, 4}", c->bits);
+  if (c->base != HG_BASE_MINMAX && c->base != HG_BASE_KIVI && c->base != HG_BASE_AKVQ)
+    return fail(HG_ERR_BASE, "unknown base %d", c->base);
+  if (c->base == HG_BASE_KIVI && c->kivi_group != hg::kWaveTokens)
+    return fail(HG_ERR_BASE, "kivi_group %d unsupported (32)", c->kivi_group);
+  if (c->keys_only != 0 && c->keys_only != 1) return fail(HG_ERR_SHAPE, "keys_only must be 0 or 1");
+  const int LH = c->L * c->H;
+  for (int i = 0; i < LH; ++i)
+    if (mask[i] > 1) return fail(HG_ERR_MASK, "protect_mask[%d] = %u is neither 0 nor 1", i, mask[i]);
+  return HG_OK;
+}
+
+struct Counts {
+  int P, uk, uv, pv;
+  uint64_t n, row, meta_k_words, meta_v_words;
+};
+
+Counts counts(const hg_config* c, const uint8_t* mask) {
+  Counts k;
+  const int LH = c->L * c->H;
+  k.P = 0;
+  for (int i = 0; i < LH; ++i) k.P += mask[i];
+  k.uk = LH - k.P;
+  k.uv = c->keys_only ? LH : LH - k.P;
+  k.pv = c->keys_only ? 0 : k.P;
+  k.n = (uint64_t)c->img_len;
+  k.row = (uint64_t)c->D * c->bits / 8;
+  const uint64_t groups = (k.n + hg::kWaveTokens - 1) / hg::kWaveTokens;
+  k.meta_k_words = c->base == HG_BASE_KIVI ? groups * c->D : k.n;
+  k.meta_v_words = k.n;
+  return k;
+}
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
+
+int check_device_ptr(const void* p, const char* name) {
+  hipPointerAttribute_t attr;
+  hipError_t e = hipPointerGetAttributes(&attr, p);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(HG_ERR_POINTER, "%s is not device memory (%s)", name, hipGetErrorString(e));
+  }
+  if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged)
+    return fail(HG_ERR_POINTER, "%s is not device memory (memory type %d)", name, (int)attr.type);
+  return HG_OK;
+}
+
+int check_device() {
+  int n = 0;
+  hipError_t e = hipGetDeviceCount(&n);
+  if (e != hipSuccess || n <= 0) {
+    (void)hipGetLastError();
+    return fail(HG_ERR_NO_DEVICE, "no HIP device (%s)", hipGetErrorString(e));
+  }
+  return HG_OK;
+}
+
+// Buffers the call reads or writes, with their sizes, for NULL, alignment and
+// device-memory checks.
+struct Buf {
+  const void* p;
+  uint64_t bytes;
+  uintptr_t align;
+  const char* name;
+};
+
+int check_buffers(const Buf* bufs, int nb) {
+  for (int i = 0; i < nb; ++i) {
+    if (bufs[i].bytes == 0) continue;
+    if (!bufs[i].p) return fail(HG_ERR_NULL, "%s is NULL but %llu bytes are needed", bufs[i].name,
+                                (unsigned long long)bufs[i].bytes);
+    if (!aligned(bufs[i].p, bufs[i].align))
+      return fail(HG_ERR_ALIGN, "%s is not %u-byte aligned", bufs[i].name, (unsigned)bufs[i].align);
+  }
+  for (int i = 0; i < nb; ++i) {
+    if (bufs[i].bytes == 0) continue;
+    int s = check_device_ptr(bufs[i].p, bufs[i].name);
+    if (s) return s;
+  }
+  return HG_OK;
+}
+
+void fill_params(hg::Params& p, const hg_config* c, const uint8_t* mask) {
+  memset(&p, 0, sizeof p);
+  p.L = c->L;
+  p.B = c->B;
+  p.H = c->H;
+  p.T = c->T;
+  p.s0 = c->img_start;
+  p.n = c->img_len;
+  p.keys_only = c->keys_only;
+  p.ngroups = (c->img_len + hg::kWaveTokens - 1) / hg::kWaveTokens;
+  p.tiles = (c->img_len + hg::kBlockTokens - 1) / hg::kBlockTokens;
+  const int LH = c->L * c->H;
+  uint32_t running = 0;
+  for (int w = 0; w < (LH + 31) / 32; ++w) {
+    uint32_t word = 0;
+    for (int b = 0; b < 32 && 32 * w + b < LH; ++b) word |= (uint32_t)(mask[32 * w + b] & 1u) << b;
+    p.route.mask[w] = word;
+    p.route.prefix[w] = (uint16_t)running;
+    running += (uint32_t)__builtin_popcount(word);
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* hg_status_string(int s) {
+  switch (s) {
+    case HG_OK: return "HG_OK";
+    case HG_ERR_NULL: return "HG_ERR_NULL";
+    case HG_ERR_SHAPE: return "HG_ERR_SHAPE";
+    case HG_ERR_SPAN: return "HG_ERR_SPAN";
+    case HG_ERR_BITS: return "HG_ERR_BITS";
+    case HG_ERR_BASE: return "HG_ERR_BASE";
+    case HG_ERR_HEADDIM: return "HG_ERR_HEADDIM";
+    case HG_ERR_ALIGN: return "HG_ERR_ALIGN";
+    case HG_ERR_MASK: return "HG_ERR_MASK";
+    case HG_ERR_NO_DEVICE: return "HG_ERR_NO_DEVICE";
+    case HG_ERR_HIP: return "HG_ERR_HIP";
+    case HG_ERR_POINTER: return "HG_ERR_POINTER";
+    default: return "HG_ERR_UNKNOWN";
+  }
+}
+
+const char* hg_last_error(void) { return g_last_error.c_str(); }
+
+int hg_packed_sizes(const hg_config* cfg, const uint8_t* mask, hg_sizes* out) {
+  if (!out) return fail(HG_ERR_NULL, "out is NULL");
+  int s = check_config(cfg, mask);
+  if (s) return s;
+  const Counts k = counts(cfg, mask);
+  const uint64_t B = (uint64_t)cfg->B, D = (uint64_t)cfg->D;
+  out->n_protected = k.P;
+  out->n_unprot_k = k.uk;
+  out->n_unprot_v = k.uv;
+  out->codes_k = (uint64_t)k.uk * B * k.n * k.row;
+  out->codes_v = (uint64_t)k.uv * B * k.n * k.row;
+  out->meta_k = (uint64_t)k.uk * B * k.meta_k_words * 4;
+  out->meta_v = (uint64_t)k.uv * B * k.meta_v_words * 4;
+  out->side_k = (uint64_t)k.P * B * k.n * D * 2;
+  out->side_v = (uint64_t)k.pv * B * k.n * D * 2;
+  return ok();
+}
+
+static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uint16_t* V,
+               const uint8_t* mask, const hg_packed* pk, hipStream_t stream) {
+  int s = check_config(cfg, mask);
+  if (s) return s;
+  if (!pk) return fail(HG_ERR_NULL, "packed buffer descriptor is NULL");
+  hg_sizes z;
+  hg_packed_sizes(cfg, mask, &z);
+  const uint64_t cache_bytes = (uint64_t)cfg->L * cfg->B * cfg->H * cfg->T * cfg->D * 2;
+  const uint64_t need = cfg->img_len > 0 ? cache_bytes : 0;
+  const Buf bufs[] = {
+      {K, need, 16, quantize ? "K" : "K_out"},
+      {V, need, 16, quantize ? "V" : "V_out"},
+      {pk->codes_k, z.codes_k, 16, "codes_k"},
+      {pk->meta_k, z.meta_k, 16, "meta_k"},
+      {pk->side_k, z.side_k, 16, "side_k"},
+      {pk->codes_v, z.codes_v, 16, "codes_v"},
+      {pk->meta_v, z.meta_v, 16, "meta_v"},
+      {pk->side_v, z.side_v, 16, "side_v"},
+  };
+  s = check_device();
+  if (s) return s;
+  s = check_buffers(bufs, (int)(sizeof bufs / sizeof bufs[0]));
+  if (s) return s;
+  if (cfg->img_len == 0) return ok();
+
+  hg::Params p;
+  fill_params(p, cfg, mask);
+  p.cache[0] = K;
+  p.cache[1] = V;
+  p.codes[0] = (uint8_t*)pk->codes_k;
+  p.codes[1] = (uint8_t*)pk->codes_v;
+  p.meta[0] = (uint32_t*)pk->meta_k;
+  p.meta[1] = (uint32_t*)pk->meta_v;
+  p.side[0] = (uint16_t*)pk->side_k;
+  p.side[1] = (uint16_t*)pk->side_v;
+  const uint64_t slices = (uint64_t)cfg->L * cfg->B * cfg->H;
+  const uint64_t blocks_k = slices * (uint64_t)p.tiles;
+  if (2 * blocks_k > 0x7FFFFFFFull)
+    return fail(HG_ERR_SHAPE, "grid of %llu workgroups too large", (unsigned long long)(2 * blocks_k));
+  p.blocks_k = (uint32_t)blocks_k;
+  hipError_t e = quantize ? hg::launch_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream)
+                          : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream);
+  if (e != hipSuccess) return fail(HG_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int hg_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, const uint8_t* mask,
+                const hg_packed* out, hipStream_t stream) {
+  if (!K || !V) {
+    if (cfg && cfg->img_len != 0) return fail(HG_ERR_NULL, "K or V is NULL");
+  }
+  return run(true, cfg, K, V, mask, out, stream);
+}
+
+int hg_dequantize(const hg_config* cfg, const uint8_t* mask, const hg_packed* in, uint16_t* K_out,
+                  uint16_t* V_out, hipStream_t stream) {
+  if (!K_out || !V_out) {
+    if (cfg && cfg->img_len != 0) return fail(HG_ERR_NULL, "K_out or V_out is NULL");
+  }
+  return run(false, cfg, K_out, V_out, mask, in, stream);
+}
+
+}  // extern "C"

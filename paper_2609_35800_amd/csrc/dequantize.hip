@@ -1,0 +1,187 @@
+// Dequantize kernels for gfx950, one instantiation per (base, head_dim,
+// bits): the reconstruction of simulated quantization (HeadGuard §4,
+// Quantization setup: entries are rounded to the base's levels and rebuilt as
+// floating-point values for attention).  x^ = bf16_rne(q*S + m); q*S is exact
+// (q < 16, S has 8 significant bits), so the fma equals the separate multiply
+// and add.  AKVQ keys are rotated back in fp32 before the BF16 rounding.
+// Protected rows come back from the side store; text rows are not written.
+//
+// Same work decomposition as the quantize kernels: a workgroup owns one
+// (tensor, l, b, h) slice and 128 image tokens, a wavefront 32 of them.
+
+#include "hg_device.h"
+#include "hg_kernels.h"
+
+namespace hg {
+
+template <int D, int BITS, bool ROTATE>
+__device__ __forceinline__ void dequantize_tokens(const uint8_t* __restrict__ codes,
+                                                  const uint32_t* __restrict__ meta,
+                                                  uint16_t* __restrict__ rows,
+                                                  int t_first, int n, int lane) {
+  constexpr int E = D / 4;
+  constexpr int NV = E / 8;
+  constexpr int ROW = D * BITS / 8;
+  constexpr int PIECE = E * BITS / 8;
+  const int j = lane & 3;
+  const int q = lane >> 2;
+
+  // Tokens past the span's end read the last token (their results are not
+  // stored), so every load is unconditional.
+  Packed<E, BITS> pk[2];
+  uint32_t mw[2];
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int t = min(t_first + pass * 16 + q, n - 1);
+    pk[pass] = load_packed<E, BITS>(codes + (size_t)t * ROW + j * PIECE);
+    mw[pass] = meta[t];
+  }
+
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int t = t_first + pass * 16 + q;
+    const float S = bf16_as_float(mw[pass] & 0xFFFFu);
+    const float m = bf16_as_float(mw[pass] >> 16);
+    uint32_t c[E];
+    unpack_codes<E, BITS>(pk[pass], c);
+    float y[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) y[e] = __builtin_fmaf((float)c[e], S, m);
+    if constexpr (ROTATE) fwht_quad<E>(y, j, fwht_scale<D>());
+    if (t < n) {
+      u32x4* dst = (u32x4*)(rows + (size_t)t * D + j * E);
+#pragma unroll
+      for (int k = 0; k < NV; ++k) {
+        u32x4 v = {pack_bf16x2(y[8 * k + 0], y[8 * k + 1]), pack_bf16x2(y[8 * k + 2], y[8 * k + 3]),
+                   pack_bf16x2(y[8 * k + 4], y[8 * k + 5]), pack_bf16x2(y[8 * k + 6], y[8 * k + 7])};
+        store_nt(dst + k, v);
+      }
+    }
+  }
+}
+
+template <int D, int BITS>
+__device__ __forceinline__ void dequantize_kivi_keys(const uint8_t* __restrict__ codes,
+                                                     const uint32_t* __restrict__ meta,
+                                                     uint16_t* __restrict__ rows,
+                                                     int g_first, int n, int lane) {
+  constexpr int LPR = D / 8;
+  constexpr int RPL = 64 / LPR;
+  constexpr int NL = kWaveTokens / RPL;
+  constexpr int ROW = D * BITS / 8;
+  const int c8 = lane % LPR;
+  const int r = lane / LPR;
+
+  const u32x4* mp = (const u32x4*)(meta + (size_t)(g_first / kWaveTokens) * D + 8 * c8);
+  const u32x4 m0 = mp[0], m1 = mp[1];
+  const uint32_t mw[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+  float S[8], m[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    S[e] = bf16_as_float(mw[e] & 0xFFFFu);
+    m[e] = bf16_as_float(mw[e] >> 16);
+  }
+
+  Packed<8, BITS> pk[NL];
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    const int t = min(g_first + r + RPL * k, n - 1);
+    pk[k] = load_packed<8, BITS>(codes + (size_t)t * ROW + c8 * BITS);
+  }
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    const int t = g_first + r + RPL * k;
+    uint32_t c[8];
+    unpack_codes<8, BITS>(pk[k], c);
+    float y[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf((float)c[e], S[e], m[e]);
+    if (t < n) {
+      u32x4 v = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
+                 pack_bf16x2(y[6], y[7])};
+      store_nt((u32x4*)(rows + (size_t)t * D + 8 * c8), v);
+    }
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void restore_rows(const uint16_t* __restrict__ side, uint16_t* __restrict__ rows,
+                                             int t_first, int n, int lane) {
+  constexpr int VPT = D / 8;
+  const int nvec = min(kWaveTokens, n - t_first) * VPT;
+  const u32x4* s = (const u32x4*)(side + (size_t)t_first * D);
+  u32x4* d = (u32x4*)(rows + (size_t)t_first * D);
+  constexpr int kMax = kWaveTokens * VPT / 64;
+  u32x4 v[kMax];
+#pragma unroll
+  for (int k = 0; k < kMax; ++k) v[k] = s[min(lane + 64 * k, nvec - 1)];
+#pragma unroll
+  for (int k = 0; k < kMax; ++k) {
+    const int i = lane + 64 * k;
+    if (i < nvec) store_nt(d + i, v[k]);
+  }
+}
+
+template <int BASE, int D, int BITS>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWaves))) void dequantize_kernel(const Params p) {
+  const Slice sl = decode_block(p, blockIdx.x);
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int t_first = sl.tile * kBlockTokens + wave * kWaveTokens;
+  if (t_first >= p.n) return;
+
+  uint16_t* rows = const_cast<uint16_t*>(p.cache[sl.X]) + ((size_t)sl.s * p.T + p.s0) * D;
+  const size_t slab = (size_t)sl.slot * p.B + sl.b;
+
+  if (sl.kept) {
+    restore_rows<D>(p.side[sl.X] + slab * p.n * D, rows, t_first, p.n, lane);
+    return;
+  }
+  const uint8_t* codes = p.codes[sl.X] + slab * p.n * (D * BITS / 8);
+  if (BASE == HG_BASE_KIVI && sl.X == 0) {
+    dequantize_kivi_keys<D, BITS>(codes, p.meta[0] + slab * p.ngroups * D, rows, t_first, p.n, lane);
+  } else {
+    const uint32_t* meta = p.meta[sl.X] + slab * p.n;
+    if (BASE == HG_BASE_AKVQ && sl.X == 0)
+      dequantize_tokens<D, BITS, true>(codes, meta, rows, t_first, p.n, lane);
+    else
+      dequantize_tokens<D, BITS, false>(codes, meta, rows, t_first, p.n, lane);
+  }
+}
+
+template <int BASE, int D, int BITS>
+static hipError_t launch_d(const Params& p, uint32_t blocks, hipStream_t stream) {
+  hipLaunchKernelGGL((dequantize_kernel<BASE, D, BITS>), dim3(blocks), dim3(kThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+template <int BASE, int D>
+static hipError_t launch_d_bits(const Params& p, int bits, uint32_t blocks, hipStream_t stream) {
+  switch (bits) {
+    case 2: return launch_d<BASE, D, 2>(p, blocks, stream);
+    case 3: return launch_d<BASE, D, 3>(p, blocks, stream);
+    case 4: return launch_d<BASE, D, 4>(p, blocks, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int BASE>
+static hipError_t launch_d_dim(const Params& p, int D, int bits, uint32_t blocks, hipStream_t stream) {
+  switch (D) {
+    case 64: return launch_d_bits<BASE, 64>(p, bits, blocks, stream);
+    case 128: return launch_d_bits<BASE, 128>(p, bits, blocks, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_dequantize(const Params& p, int base, int D, int bits, uint32_t blocks,
+                             hipStream_t stream) {
+  switch (base) {
+    case HG_BASE_MINMAX: return launch_d_dim<HG_BASE_MINMAX>(p, D, bits, blocks, stream);
+    case HG_BASE_KIVI: return launch_d_dim<HG_BASE_KIVI>(p, D, bits, blocks, stream);
+    case HG_BASE_AKVQ: return launch_d_dim<HG_BASE_AKVQ>(p, D, bits, blocks, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace hg

@@ -1,0 +1,265 @@
+// Device helpers for the gfx950 quantizer kernels: BF16 conversions with
+// directed rounding, quad-level DPP exchanges, the per-group scale rule, the
+// in-register/quad Walsh-Hadamard transform and LSB-first bit packing.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hg {
+
+// Native clang vectors: nontemporal builtins and wide loads/stores need them.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+// 12-byte pieces sit at 4-byte aligned offsets: declare that alignment.
+typedef uint32_t u32x3 __attribute__((ext_vector_type(3), aligned(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// ------------------------------------------------------------------ BF16
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+__device__ __forceinline__ float bf16_as_float(uint32_t h) { return __uint_as_float(h << 16); }
+
+// Round toward -inf / +inf to a BF16 bit pattern (finite inputs).  Truncating
+// the low half rounds toward zero; a value with a nonzero low half on the far
+// side of zero then moves one BF16 unit away from zero.
+__device__ __forceinline__ uint32_t bf16_round_down(float x) {
+  uint32_t u = __float_as_uint(x);
+  uint32_t step = ((u & 0xFFFFu) != 0u) & (u >> 31);
+  return (u >> 16) + step;
+}
+__device__ __forceinline__ uint32_t bf16_round_up(float x) {
+  uint32_t u = __float_as_uint(x);
+  uint32_t step = ((u & 0xFFFFu) != 0u) & ((u >> 31) ^ 1u);
+  return (u >> 16) + step;
+}
+// Round to nearest, ties to even: adding 0x7FFF plus the kept LSB carries into
+// the kept half exactly when the dropped half is above one half, or equal to
+// one half with an odd kept half.
+__device__ __forceinline__ uint32_t bf16_round_nearest(float x) {
+  uint32_t u = __float_as_uint(x);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return bf16_round_nearest(lo) | (bf16_round_nearest(hi) << 16);
+}
+
+// ------------------------------------------------------- quad DPP exchange
+
+// quad_perm controls: lane i of each group of four reads lane i^1 / i^2.
+constexpr int kQuadXor1 = 0xB1;  // [1,0,3,2]
+constexpr int kQuadXor2 = 0x4E;  // [2,3,0,1]
+
+template <int CTRL>
+__device__ __forceinline__ float quad_swap(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ float quad_min(float v) {
+  v = fminf(v, quad_swap<kQuadXor1>(v));
+  return fminf(v, quad_swap<kQuadXor2>(v));
+}
+__device__ __forceinline__ float quad_max(float v) {
+  v = fmaxf(v, quad_swap<kQuadXor1>(v));
+  return fmaxf(v, quad_swap<kQuadXor2>(v));
+}
+
+// --------------------------------------------------------- group scale rule
+
+// Metadata of a group with range [mn, mx] at LEVELS = 2^b - 1:
+// m = BF16 round-down of mn, S = BF16 round-up of (mx - m)/LEVELS, zeros
+// stored as +0, a positive S raised to at least 2^-126 (BF16 0x0080) so that
+// 1/S stays finite.  `inv` is the correctly rounded 1/S, or 0 when S == 0.
+struct GroupScale {
+  float m, inv;
+  uint32_t meta;
+};
+
+template <int LEVELS>
+__device__ __forceinline__ GroupScale group_scale(float mn, float mx) {
+  uint32_t m16 = bf16_round_down(mn);
+  m16 = (m16 == 0x8000u) ? 0u : m16;
+  float m = bf16_as_float(m16);
+  float s = (mx - m) / (float)LEVELS;          // IEEE division, correctly rounded
+  uint32_t s16 = bf16_round_up(s);
+  s16 = (s16 == 0x8000u) ? 0u : s16;
+  s16 = (s16 != 0u && s16 < 0x0080u) ? 0x0080u : s16;
+  float S = bf16_as_float(s16);
+  float inv = 1.0f / (s16 ? S : 1.0f);         // IEEE division, correctly rounded
+  GroupScale g;
+  g.m = m;
+  g.inv = s16 ? inv : 0.0f;
+  g.meta = s16 | (m16 << 16);
+  return g;
+}
+
+// Code of one element: clamp(rint((v - m) * inv), 0, LEVELS), in this order of
+// fp32 operations (no contraction).
+template <int LEVELS>
+__device__ __forceinline__ uint32_t code_of(float v, const GroupScale& g) {
+  float t = (v - g.m) * g.inv;
+  float r = __builtin_rintf(t);
+  r = fminf(fmaxf(r, 0.0f), (float)LEVELS);
+  return (uint32_t)r;
+}
+
+// ------------------------------------------------- Walsh-Hadamard transform
+
+// fp32(1/sqrt(D)) for the supported power-of-two head dims: 1/8 exactly, and
+// 1/sqrt(128) = 0.08838834764... rounded to nearest fp32.
+template <int D>
+__device__ __forceinline__ constexpr float fwht_scale() {
+  static_assert(D == 64 || D == 128, "head_dim");
+  return D == 64 ? 0.125f : 0x1.6a09e6p-4f;
+}
+
+// Butterflies of spans 1 .. E/2 inside one lane's E contiguous elements.
+template <int E>
+__device__ __forceinline__ void fwht_lane(float (&x)[E]) {
+#pragma unroll
+  for (int h = 1; h < E; h *= 2) {
+#pragma unroll
+    for (int i = 0; i < E; i += 2 * h) {
+#pragma unroll
+      for (int k = i; k < i + h; ++k) {
+        float p = x[k], q = x[k + h];
+        x[k] = p + q;
+        x[k + h] = p - q;
+      }
+    }
+  }
+}
+
+// One butterfly stage whose partner elements live in lane j ^ (CTRL's xor):
+// the lower lane keeps p + q, the upper lane p - q (partner - own).  With the
+// sign folded into an exact multiply-by-one, both are one correctly rounded
+// fma.
+template <int E, int CTRL>
+__device__ __forceinline__ void fwht_cross(float (&x)[E], bool upper) {
+  const float sgn = upper ? -1.0f : 1.0f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    float partner = quad_swap<CTRL>(x[e]);
+    x[e] = __builtin_fmaf(x[e], sgn, partner);
+  }
+}
+
+// Full transform over D = 4E elements held by a lane quad (lane j holds
+// elements [E*j, E*j + E)): spans 1..E/2 in registers, then E (lane ^ 1) and
+// 2E (lane ^ 2), then the scale c.  Same butterfly order as spans 1..D/2.
+template <int E>
+__device__ __forceinline__ void fwht_quad(float (&x)[E], int j, float c) {
+  fwht_lane<E>(x);
+  fwht_cross<E, kQuadXor1>(x, (j & 1) != 0);
+  fwht_cross<E, kQuadXor2>(x, (j & 2) != 0);
+#pragma unroll
+  for (int e = 0; e < E; ++e) x[e] = x[e] * c;
+}
+
+// ------------------------------------------------------------ bit packing
+
+// Packs N codes of BITS bits each, LSB-first, into W = ceil(N*BITS/32) words.
+template <int N, int BITS>
+struct Packed {
+  static constexpr int kBits = N * BITS;
+  static constexpr int W = (kBits + 31) / 32;
+  uint32_t w[W];
+};
+
+template <int N, int BITS>
+__device__ __forceinline__ Packed<N, BITS> pack_codes(const uint32_t (&q)[N]) {
+  Packed<N, BITS> p;
+#pragma unroll
+  for (int i = 0; i < Packed<N, BITS>::W; ++i) p.w[i] = 0u;
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    const int pos = e * BITS;
+    p.w[pos / 32] |= q[e] << (pos % 32);
+    if ((pos % 32) + BITS > 32) p.w[pos / 32 + 1] |= q[e] >> (32 - pos % 32);
+  }
+  return p;
+}
+
+template <int N, int BITS>
+__device__ __forceinline__ void unpack_codes(const Packed<N, BITS>& p, uint32_t (&q)[N]) {
+  constexpr uint32_t kMask = (1u << BITS) - 1u;
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    const int pos = e * BITS;
+    uint32_t v = p.w[pos / 32] >> (pos % 32);
+    if ((pos % 32) + BITS > 32) v |= p.w[pos / 32 + 1] << (32 - pos % 32);
+    q[e] = v & kMask;
+  }
+}
+
+// Stores / loads of a lane's packed piece at a byte address whose alignment is
+// that of the piece: whole dwords for 32/64/96/128-bit pieces, 16-bit halves
+// for 48-bit pieces.
+template <int N, int BITS>
+__device__ __forceinline__ void store_packed(uint8_t* dst, const Packed<N, BITS>& p) {
+  constexpr int kBits = N * BITS;
+  if constexpr (kBits == 16) {
+    __builtin_nontemporal_store((uint16_t)p.w[0], (uint16_t*)dst);
+  } else if constexpr (kBits == 24) {
+    dst[0] = (uint8_t)p.w[0];
+    dst[1] = (uint8_t)(p.w[0] >> 8);
+    dst[2] = (uint8_t)(p.w[0] >> 16);
+  } else if constexpr (kBits == 32) {
+    __builtin_nontemporal_store(p.w[0], (uint32_t*)dst);
+  } else if constexpr (kBits == 48) {
+    uint16_t* d = (uint16_t*)dst;
+    __builtin_nontemporal_store((uint16_t)p.w[0], d);
+    __builtin_nontemporal_store((uint16_t)(p.w[0] >> 16), d + 1);
+    __builtin_nontemporal_store((uint16_t)p.w[1], d + 2);
+  } else if constexpr (kBits == 64) {
+    u32x2 v = {p.w[0], p.w[1]};
+    __builtin_nontemporal_store(v, (u32x2*)dst);
+  } else if constexpr (kBits == 96) {
+    u32x3 v = {p.w[0], p.w[1], p.w[2]};
+    __builtin_nontemporal_store(v, (u32x3*)dst);
+  } else {
+    static_assert(kBits == 128, "unsupported packed piece");
+    u32x4 v = {p.w[0], p.w[1], p.w[2], p.w[3]};
+    __builtin_nontemporal_store(v, (u32x4*)dst);
+  }
+}
+
+template <int N, int BITS>
+__device__ __forceinline__ Packed<N, BITS> load_packed(const uint8_t* src) {
+  constexpr int kBits = N * BITS;
+  Packed<N, BITS> p;
+  if constexpr (kBits == 16) {
+    p.w[0] = *(const uint16_t*)src;
+  } else if constexpr (kBits == 24) {
+    p.w[0] = (uint32_t)src[0] | ((uint32_t)src[1] << 8) | ((uint32_t)src[2] << 16);
+  } else if constexpr (kBits == 32) {
+    p.w[0] = *(const uint32_t*)src;
+  } else if constexpr (kBits == 48) {
+    const uint16_t* s = (const uint16_t*)src;
+    p.w[0] = (uint32_t)s[0] | ((uint32_t)s[1] << 16);
+    p.w[1] = s[2];
+  } else if constexpr (kBits == 64) {
+    u32x2 v = *(const u32x2*)src;
+    p.w[0] = v.x;
+    p.w[1] = v.y;
+  } else if constexpr (kBits == 96) {
+    u32x3 v = *(const u32x3*)src;
+    p.w[0] = v.x;
+    p.w[1] = v.y;
+    p.w[2] = v.z;
+  } else {
+    static_assert(kBits == 128, "unsupported packed piece");
+    u32x4 v = *(const u32x4*)src;
+    p.w[0] = v.x;
+    p.w[1] = v.y;
+    p.w[2] = v.z;
+    p.w[3] = v.w;
+  }
+  return p;
+}
+
+__device__ __forceinline__ void store_nt(u32x4* dst, u32x4 v) {
+  __builtin_nontemporal_store(v, dst);
+}
+
+}  // namespace hg

@@ -1,0 +1,90 @@
+// Kernel parameter block and launchers shared by the host API and the
+// quantize / dequantize kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "headguard.h"
+
+namespace hg {
+
+constexpr int kThreads = 256;        // 4 wavefronts of 64
+constexpr int kWaveTokens = 32;      // tokens per wavefront tile
+constexpr int kBlockTokens = 128;    // tokens per workgroup tile (4 x 32)
+// Register budget: at least this many wavefronts per SIMD, so enough 16-byte
+// loads are in flight per CU to cover HBM latency.
+constexpr int kMinWaves = 4;
+constexpr int kMaskWords = HG_MAX_HEADS / 32;
+
+// Mask routing in kernel arguments: bit i of `mask` marks protected head
+// i = l*H + h; `prefix[w]` counts protected heads in words before w, so the
+// rank of i among protected heads is prefix[i/32] + popcount of the lower
+// bits of word i/32 (§3: a base must be able to skip individual heads).
+struct Route {
+  uint32_t mask[kMaskWords];
+  uint16_t prefix[kMaskWords];
+};
+
+// One launch covers K (tensor 0) and V (tensor 1): blocks [0, blocks_k) take
+// K tiles, the rest V tiles.  Each block takes one (tensor, l, b, h) slice
+// and kBlockTokens consecutive image tokens of it.
+struct Params {
+  const uint16_t* cache[2];  // quantize: K, V input; dequantize: K_out, V_out
+  uint8_t* codes[2];
+  uint32_t* meta[2];
+  uint16_t* side[2];
+  int32_t L, B, H, T;
+  int32_t s0, n;             // image span
+  int32_t keys_only;
+  int32_t ngroups;           // KIVI key groups per slice
+  int32_t tiles;             // kBlockTokens tiles per slice
+  uint32_t blocks_k;         // blocks of tensor K
+  Route route;
+};
+
+// Dispatch over (base, D, bits); return hipSuccess or the launch error.
+hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
+                           hipStream_t stream);
+hipError_t launch_dequantize(const Params& p, int base, int D, int bits, uint32_t blocks,
+                             hipStream_t stream);
+
+// Slice decoding shared by the kernels: which tensor, slice and tile a block
+// owns, whether the slice is kept in BF16, and its slot in the packed buffers.
+struct Slice {
+  int X;            // 0 = K, 1 = V
+  int tile;         // token tile within the slice
+  uint32_t s;       // (l*B + b)*H + h
+  int b;
+  bool kept;        // kept in BF16 (protected)
+  uint32_t slot;    // rank among kept heads if kept, else among quantized heads
+};
+
+__device__ __forceinline__ Slice decode_block(const Params& p, uint32_t bid) {
+  Slice r;
+  r.X = bid >= p.blocks_k ? 1 : 0;
+  uint32_t rel = bid - (r.X ? p.blocks_k : 0u);
+  r.tile = (int)(rel % (uint32_t)p.tiles);
+  r.s = rel / (uint32_t)p.tiles;
+  const uint32_t h = r.s % (uint32_t)p.H;
+  const uint32_t lb = r.s / (uint32_t)p.H;
+  r.b = (int)(lb % (uint32_t)p.B);
+  const uint32_t l = lb / (uint32_t)p.B;
+  const uint32_t i = l * (uint32_t)p.H + h;
+  const uint32_t w = p.route.mask[i >> 5];
+  const bool masked = (w >> (i & 31u)) & 1u;
+  const uint32_t rank = (uint32_t)p.route.prefix[i >> 5] +
+                        (uint32_t)__builtin_popcount(w & ((1u << (i & 31u)) - 1u));
+  const bool v_kept_allowed = (r.X == 0) || !p.keys_only;
+  r.kept = masked && v_kept_allowed;
+  if (r.kept) {
+    r.slot = rank;
+  } else if (r.X == 1 && p.keys_only) {
+    r.slot = i;  // K-only mode: every V head is quantized
+  } else {
+    r.slot = i - rank;
+  }
+  return r;
+}
+
+}  // namespace hg

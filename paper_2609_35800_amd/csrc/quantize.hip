@@ -1,0 +1,244 @@
+// Fused quantize + pack kernels for gfx950, one instantiation per
+// (base, head_dim, bits).  HeadGuard §3 (Applying protection) and §4
+// (Quantization setup): every image-token K/V vector of an unprotected head
+// goes through the base quantizer, protected heads' image rows are copied to
+// the BF16 side store, text rows are never read.
+//
+// Work decomposition: a 256-thread workgroup owns one (tensor, l, b, h) slice
+// and 128 consecutive image tokens of it; each wavefront owns 32 tokens.
+//  - Per-token groups (min-max K and V, KIVI V, AKVQ K and V): a lane quad
+//    holds one token vector, lane j the D/4 contiguous elements
+//    [j*D/4, (j+1)*D/4) loaded with 16-byte loads; the range is reduced with
+//    two quad DPP exchanges; a lane's codes form one contiguous piece of the
+//    packed row.  A wavefront covers 16 tokens per pass, two passes.
+//  - KIVI keys: the wavefront holds one 32-token group; lanes cover D/8
+//    channel octets per token row and 64/(D/8) token rows per load, so the
+//    per-channel range over tokens is an in-register reduction plus
+//    cross-row shuffles.
+//  - AKVQ keys: the normalized Walsh-Hadamard rotation runs on the quad before
+//    the range reduction: spans 1..D/8 in registers, D/4 and D/2 by DPP.
+//  - Protected slices: 16-byte copies of the image rows to the side store.
+// All per-group arithmetic is IEEE fp32 (no contraction), the same operations
+// in the same order as the reference definition.
+
+#include "hg_device.h"
+#include "hg_kernels.h"
+
+namespace hg {
+
+// ---------------------------------------------------------- per-token path
+
+template <int D, int BITS, bool ROTATE>
+__device__ __forceinline__ void quantize_tokens(const uint16_t* __restrict__ rows,
+                                                uint8_t* __restrict__ codes,
+                                                uint32_t* __restrict__ meta,
+                                                int t_first, int n, int lane) {
+  constexpr int E = D / 4;             // elements per lane
+  constexpr int NV = E / 8;            // 16-byte loads per lane per token
+  constexpr int LEVELS = (1 << BITS) - 1;
+  constexpr int ROW = D * BITS / 8;    // packed bytes per token
+  constexpr int PIECE = E * BITS / 8;  // packed bytes per lane
+  const int j = lane & 3;
+  const int q = lane >> 2;
+
+  // Tokens past the span's end load the last token instead (their results are
+  // not stored), so every load is unconditional.
+  u32x4 raw[2][NV];
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int t = min(t_first + pass * 16 + q, n - 1);
+    const u32x4* src = (const u32x4*)(rows + (size_t)t * D + j * E);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) raw[pass][k] = src[k];
+  }
+
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int t = t_first + pass * 16 + q;
+    float x[E];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      x[8 * k + 0] = bf16_lo(raw[pass][k].x);
+      x[8 * k + 1] = bf16_hi(raw[pass][k].x);
+      x[8 * k + 2] = bf16_lo(raw[pass][k].y);
+      x[8 * k + 3] = bf16_hi(raw[pass][k].y);
+      x[8 * k + 4] = bf16_lo(raw[pass][k].z);
+      x[8 * k + 5] = bf16_hi(raw[pass][k].z);
+      x[8 * k + 6] = bf16_lo(raw[pass][k].w);
+      x[8 * k + 7] = bf16_hi(raw[pass][k].w);
+    }
+    if constexpr (ROTATE) fwht_quad<E>(x, j, fwht_scale<D>());
+
+    float mn = x[0], mx = x[0];
+#pragma unroll
+    for (int e = 1; e < E; ++e) {
+      mn = fminf(mn, x[e]);
+      mx = fmaxf(mx, x[e]);
+    }
+    mn = quad_min(mn);
+    mx = quad_max(mx);
+    const GroupScale g = group_scale<LEVELS>(mn, mx);
+
+    uint32_t c[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) c[e] = code_of<LEVELS>(x[e], g);
+    const Packed<E, BITS> pk = pack_codes<E, BITS>(c);
+    if (t < n) {
+      store_packed<E, BITS>(codes + (size_t)t * ROW + j * PIECE, pk);
+      if (j == 0) __builtin_nontemporal_store(g.meta, meta + t);
+    }
+  }
+}
+
+// ---------------------------------------------------------- KIVI key groups
+
+template <int D, int BITS>
+__device__ __forceinline__ void quantize_kivi_keys(const uint16_t* __restrict__ rows,
+                                                   uint8_t* __restrict__ codes,
+                                                   uint32_t* __restrict__ meta,
+                                                   int g_first, int n, int lane) {
+  constexpr int LPR = D / 8;                 // lanes per token row (8 channels each)
+  constexpr int RPL = 64 / LPR;              // token rows per load
+  constexpr int NL = kWaveTokens / RPL;      // loads per lane
+  constexpr int LEVELS = (1 << BITS) - 1;
+  constexpr int ROW = D * BITS / 8;
+  const int c8 = lane % LPR;                 // channel octet
+  const int r = lane / LPR;                  // token row within a load
+
+  u32x4 raw[NL];
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    const int t = min(g_first + r + RPL * k, n - 1);  // past-the-end rows: excluded below
+    raw[k] = *(const u32x4*)(rows + (size_t)t * D + 8 * c8);
+  }
+
+  float x[NL][8];
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    x[k][0] = bf16_lo(raw[k].x); x[k][1] = bf16_hi(raw[k].x);
+    x[k][2] = bf16_lo(raw[k].y); x[k][3] = bf16_hi(raw[k].y);
+    x[k][4] = bf16_lo(raw[k].z); x[k][5] = bf16_hi(raw[k].z);
+    x[k][6] = bf16_lo(raw[k].w); x[k][7] = bf16_hi(raw[k].w);
+  }
+
+  GroupScale g[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    float mn = __builtin_inff(), mx = -__builtin_inff();
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      const bool ok = g_first + r + RPL * k < n;
+      mn = fminf(mn, ok ? x[k][e] : __builtin_inff());
+      mx = fmaxf(mx, ok ? x[k][e] : -__builtin_inff());
+    }
+#pragma unroll
+    for (int off = LPR; off < 64; off *= 2) {
+      mn = fminf(mn, __shfl_xor(mn, off));
+      mx = fmaxf(mx, __shfl_xor(mx, off));
+    }
+    g[e] = group_scale<LEVELS>(mn, mx);
+  }
+
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    const int t = g_first + r + RPL * k;
+    uint32_t cq[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cq[e] = code_of<LEVELS>(x[k][e], g[e]);
+    const Packed<8, BITS> pk = pack_codes<8, BITS>(cq);
+    if (t < n) store_packed<8, BITS>(codes + (size_t)t * ROW + c8 * BITS, pk);
+  }
+  if (r == 0) {
+    uint32_t* m = meta + (size_t)(g_first / kWaveTokens) * D + 8 * c8;
+    __builtin_nontemporal_store(u32x4{g[0].meta, g[1].meta, g[2].meta, g[3].meta}, (u32x4*)m);
+    __builtin_nontemporal_store(u32x4{g[4].meta, g[5].meta, g[6].meta, g[7].meta}, (u32x4*)m + 1);
+  }
+}
+
+// ---------------------------------------------------------- protected copy
+
+template <int D>
+__device__ __forceinline__ void copy_rows(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
+                                          int t_first, int n, int lane) {
+  constexpr int VPT = D / 8;  // 16-byte vectors per token
+  const int ntok = min(kWaveTokens, n - t_first);
+  const int nvec = ntok * VPT;
+  const u32x4* s = (const u32x4*)(src + (size_t)t_first * D);
+  u32x4* d = (u32x4*)(dst + (size_t)t_first * D);
+  constexpr int kMax = kWaveTokens * VPT / 64;
+  u32x4 v[kMax];
+#pragma unroll
+  for (int k = 0; k < kMax; ++k) v[k] = s[min(lane + 64 * k, nvec - 1)];
+#pragma unroll
+  for (int k = 0; k < kMax; ++k) {
+    const int i = lane + 64 * k;
+    if (i < nvec) store_nt(d + i, v[k]);
+  }
+}
+
+// ---------------------------------------------------------------- kernel
+
+template <int BASE, int D, int BITS>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWaves))) void quantize_kernel(const Params p) {
+  const Slice sl = decode_block(p, blockIdx.x);
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int t_first = sl.tile * kBlockTokens + wave * kWaveTokens;
+  if (t_first >= p.n) return;
+
+  const uint16_t* rows = p.cache[sl.X] + ((size_t)sl.s * p.T + p.s0) * D;
+  const size_t slab = (size_t)sl.slot * p.B + sl.b;  // [slot][B]
+
+  if (sl.kept) {
+    copy_rows<D>(rows, p.side[sl.X] + slab * p.n * D, t_first, p.n, lane);
+    return;
+  }
+  uint8_t* codes = p.codes[sl.X] + slab * p.n * (D * BITS / 8);
+  if (BASE == HG_BASE_KIVI && sl.X == 0) {
+    uint32_t* meta = p.meta[0] + slab * p.ngroups * D;
+    quantize_kivi_keys<D, BITS>(rows, codes, meta, t_first, p.n, lane);
+  } else {
+    uint32_t* meta = p.meta[sl.X] + slab * p.n;
+    if (BASE == HG_BASE_AKVQ && sl.X == 0)
+      quantize_tokens<D, BITS, true>(rows, codes, meta, t_first, p.n, lane);
+    else
+      quantize_tokens<D, BITS, false>(rows, codes, meta, t_first, p.n, lane);
+  }
+}
+
+template <int BASE, int D, int BITS>
+static hipError_t launch_q(const Params& p, uint32_t blocks, hipStream_t stream) {
+  hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS>), dim3(blocks), dim3(kThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+template <int BASE, int D>
+static hipError_t launch_q_bits(const Params& p, int bits, uint32_t blocks, hipStream_t stream) {
+  switch (bits) {
+    case 2: return launch_q<BASE, D, 2>(p, blocks, stream);
+    case 3: return launch_q<BASE, D, 3>(p, blocks, stream);
+    case 4: return launch_q<BASE, D, 4>(p, blocks, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int BASE>
+static hipError_t launch_q_dim(const Params& p, int D, int bits, uint32_t blocks, hipStream_t stream) {
+  switch (D) {
+    case 64: return launch_q_bits<BASE, 64>(p, bits, blocks, stream);
+    case 128: return launch_q_bits<BASE, 128>(p, bits, blocks, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
+                           hipStream_t stream) {
+  switch (base) {
+    case HG_BASE_MINMAX: return launch_q_dim<HG_BASE_MINMAX>(p, D, bits, blocks, stream);
+    case HG_BASE_KIVI: return launch_q_dim<HG_BASE_KIVI>(p, D, bits, blocks, stream);
+    case HG_BASE_AKVQ: return launch_q_dim<HG_BASE_AKVQ>(p, D, bits, blocks, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace hg

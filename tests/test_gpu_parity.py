@@ -1,0 +1,128 @@
+"""GPU parity: the HIP library against the CPU oracle on the same seeded BF16
+bytes.  Packed codes, metadata and the BF16 side store must be bit-exact;
+dequantized BF16 within 1 BF16 ulp (expected: 0).  Text rows must stay
+untouched and canary bytes after every output buffer intact.
+
+Small shapes are compared element by element and span several 128-token
+workgroup tiles with ragged tails; every base, head_dim, bit width and
+protection mode is covered, with special values (constant tokens, signed
+zeros, tiny/subnormal ranges, exact ties, large magnitudes) and degenerate
+masks and spans."""
+import numpy as np
+import pytest
+import torch
+
+import synthkv
+from hgtest import compare_full, f32_of_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def _assert_exact(rep, tag):
+    bad = {k: v for k, v in rep.items() if k.endswith("_mismatch") and v}
+    assert rep["canaries"], f"{tag}: canary bytes overwritten"
+    assert not bad, f"{tag}: packed mismatches {bad}"
+    assert rep["K_ulp"] <= 1 and rep["V_ulp"] <= 1, f"{tag}: dequant ulp {rep}"
+    # the reconstruction rule is exact on both sides: report any ulp drift
+    assert rep["K_exact"] and rep["V_exact"], f"{tag}: dequant not bit-exact {rep}"
+
+
+def small(base, D=128, bits=2, keys_only=0, img_len=300, img_start=7, text=13, L=2, B=2, H=3,
+          n_protected=2, seed=0):
+    return synthkv.Workload(f"{base}-D{D}-b{bits}-ko{keys_only}-n{img_len}", L=L, B=B, H=H,
+                            T=img_start + img_len + text, D=D, img_start=img_start,
+                            img_len=img_len, bits=bits, base=base, keys_only=keys_only,
+                            n_protected=n_protected, k_outliers=4, k_outlier_scale=10.0,
+                            kivi_group=32, seed=seed)
+
+
+CASES = [small(b, D, bits, ko)
+         for b in ("minmax", "kivi", "akvq") for D in (64, 128) for bits in (2, 3, 4)
+         for ko in (0, 1)]
+
+
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def test_small_parity(w):
+    K, V = synthkv.gen_kv(w)
+    rep = compare_full(w, K, V, synthkv.protect_mask(w))
+    _assert_exact(rep, w.name)
+
+
+def test_tiny_workload():
+    w = synthkv.WORKLOADS["tiny"]
+    K, V = synthkv.gen_kv(w)
+    _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), "tiny")
+
+
+@pytest.mark.parametrize("base", ["minmax", "kivi", "akvq"])
+@pytest.mark.parametrize("img_len", [1, 5, 31, 32, 33, 127, 128, 129, 257])
+def test_ragged_spans(base, img_len):
+    w = small(base, img_len=img_len, img_start=3, text=2, L=1, B=2, H=2, n_protected=1)
+    K, V = synthkv.gen_kv(w)
+    _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), w.name)
+
+
+@pytest.mark.parametrize("base", ["minmax", "kivi", "akvq"])
+@pytest.mark.parametrize("which", ["none", "all"])
+@pytest.mark.parametrize("keys_only", [0, 1])
+def test_degenerate_masks(base, which, keys_only):
+    w = small(base, keys_only=keys_only, img_len=100)
+    K, V = synthkv.gen_kv(w)
+    mask = np.full(w.L * w.H, 1 if which == "all" else 0, np.uint8)
+    rep = compare_full(w, K, V, mask)
+    _assert_exact(rep, f"{base}-{which}")
+
+
+def _special_values(w, K, V):
+    """Plant constant tokens, signed zeros, tiny ranges, ties and large values."""
+    s = w.img_start
+    bf = torch.bfloat16
+    for X in (K, V):
+        X[0, 0, 0, s + 0] = 1.5                                  # constant token
+        X[0, 0, 0, s + 1] = 0.0                                  # all +0
+        X[0, 0, 0, s + 2] = -0.0                                 # all -0
+        X[0, 0, 0, s + 3, ::2] = -0.0                            # mixed zeros
+        X[0, 0, 0, s + 4] = torch.linspace(1e-38, 3e-38, w.D).to(bf)   # tiny range
+        X[0, 0, 0, s + 5] = torch.linspace(-2e-39, 2e-39, w.D).to(bf)  # subnormal span
+        X[0, 0, 0, s + 6] = (torch.arange(w.D) % 8).to(bf) * 0.5      # exact ties
+        X[0, 0, 0, s + 7] = torch.linspace(-1e29, 8e28, w.D).to(bf)    # large (< 2^100)
+        X[0, 0, 0, s + 8] = 0.0
+        X[0, 0, 0, s + 8, 5] = 1e-40                             # one denormal
+        # the same token in a KIVI group: per-channel constants
+        X[0, 1, 1, s + 32:s + 64] = X[0, 1, 1, s + 32:s + 33]
+    return K, V
+
+
+@pytest.mark.parametrize("base", ["minmax", "kivi", "akvq"])
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_special_values(base, bits):
+    w = small(base, bits=bits, img_len=96, n_protected=0)
+    K, V = synthkv.gen_kv(w)
+    K, V = _special_values(w, K, V)
+    rep = compare_full(w, K, V, np.zeros(w.L * w.H, np.uint8))
+    _assert_exact(rep, f"special-{base}-{bits}")
+
+
+def test_empty_span_is_a_noop():
+    import paper_2609_35800_amd as hg
+    w = small("minmax", img_len=0, img_start=4, text=8)
+    K, V = synthkv.gen_kv(w)
+    rep = compare_full(w, K, V, synthkv.protect_mask(w))
+    _assert_exact(rep, "empty")
+    cfg = hg.make_config(**w.config_fields())
+    assert all(v == 0 for k, v in hg.hg_packed_sizes(cfg, synthkv.protect_mask(w)).items()
+               if k in hg.BUFFERS)
+
+
+def test_side_stream_and_determinism():
+    """Same bytes on a non-default stream and on a second run."""
+    from hgtest import gpu_run
+    w = small("akvq", img_len=200)
+    K, V = synthkv.gen_kv(w)
+    mask = synthkv.protect_mask(w)
+    s = torch.cuda.Stream()
+    a = gpu_run(w, K, V, mask, stream=s)
+    b = gpu_run(w, K, V, mask)
+    for n in a[0]:
+        assert np.array_equal(a[0][n], b[0][n])
+    assert np.array_equal(a[1], b[1]) and np.array_equal(a[2], b[2])
