@@ -6,56 +6,53 @@
 // and add.  AKVQ keys are rotated back in fp32 before the BF16 rounding.
 // Protected rows come back from the side store; text rows are not written.
 //
-// Same work decomposition as the quantize kernels: a workgroup owns one
-// (tensor, l, b, h) slice and 128 image tokens, a wavefront 32 of them.
+// Same tiling as the quantize kernels (a workgroup owns one (tensor, l, b, h)
+// slice and 128 image tokens, a wavefront 32 of them), but every path holds a
+// token row across D/8 lanes so that stores are whole contiguous rows.
 
 #include "hg_device.h"
 #include "hg_kernels.h"
 
 namespace hg {
 
+// Per-token groups.  A token row is held by D/8 lanes, lane c holding
+// channels [8c, 8c + 8), so each 16-byte store instruction of the wavefront
+// writes 64/(D/8) whole consecutive token rows (one contiguous 1 KiB run for
+// D = 128).  AKVQ keys are rotated back across the row's lanes first.
 template <int D, int BITS, bool ROTATE>
 __device__ __forceinline__ void dequantize_tokens(const uint8_t* __restrict__ codes,
                                                   const uint32_t* __restrict__ meta,
                                                   uint16_t* __restrict__ rows,
                                                   int t_first, int n, int lane) {
-  constexpr int E = D / 4;
-  constexpr int NV = E / 8;
+  constexpr int LPT = D / 8;               // lanes per token row
+  constexpr int TPI = 64 / LPT;            // token rows per instruction
+  constexpr int NP = kWaveTokens / TPI;    // instructions per wavefront tile
   constexpr int ROW = D * BITS / 8;
-  constexpr int PIECE = E * BITS / 8;
-  const int j = lane & 3;
-  const int q = lane >> 2;
+  constexpr uint32_t kMask = (1u << BITS) - 1u;
+  const int c = lane % LPT;
+  const int r = lane / LPT;
 
-  // Tokens past the span's end read the last token (their results are not
-  // stored), so every load is unconditional.
-  Packed<E, BITS> pk[2];
-  uint32_t mw[2];
+  // Past-the-end tokens read the last token (not stored): loads unconditional.
+  uint32_t pc[NP], mw[NP];
 #pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-    const int t = min(t_first + pass * 16 + q, n - 1);
-    pk[pass] = load_packed<E, BITS>(codes + (size_t)t * ROW + j * PIECE);
-    mw[pass] = meta[t];
+  for (int k = 0; k < NP; ++k) {
+    const int t = min(t_first + r + TPI * k, n - 1);
+    pc[k] = load_piece8<BITS, ROW>(codes + (size_t)t * ROW, c);
+    mw[k] = meta[t];
   }
-
 #pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-    const int t = t_first + pass * 16 + q;
-    const float S = bf16_as_float(mw[pass] & 0xFFFFu);
-    const float m = bf16_as_float(mw[pass] >> 16);
-    uint32_t c[E];
-    unpack_codes<E, BITS>(pk[pass], c);
-    float y[E];
+  for (int k = 0; k < NP; ++k) {
+    const int t = t_first + r + TPI * k;
+    const float S = bf16_as_float(mw[k] & 0xFFFFu);
+    const float m = bf16_as_float(mw[k] >> 16);
+    float y[8];
 #pragma unroll
-    for (int e = 0; e < E; ++e) y[e] = __builtin_fmaf((float)c[e], S, m);
-    if constexpr (ROTATE) fwht_quad<E>(y, j, fwht_scale<D>());
+    for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf((float)((pc[k] >> (BITS * e)) & kMask), S, m);
+    if constexpr (ROTATE) fwht_row<D>(y, c);
     if (t < n) {
-      u32x4* dst = (u32x4*)(rows + (size_t)t * D + j * E);
-#pragma unroll
-      for (int k = 0; k < NV; ++k) {
-        u32x4 v = {pack_bf16x2(y[8 * k + 0], y[8 * k + 1]), pack_bf16x2(y[8 * k + 2], y[8 * k + 3]),
-                   pack_bf16x2(y[8 * k + 4], y[8 * k + 5]), pack_bf16x2(y[8 * k + 6], y[8 * k + 7])};
-        store_nt(dst + k, v);
-      }
+      u32x4 v = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
+                 pack_bf16x2(y[6], y[7])};
+      store_nt((u32x4*)(rows + (size_t)t * D + 8 * c), v);
     }
   }
 }
@@ -82,20 +79,19 @@ __device__ __forceinline__ void dequantize_kivi_keys(const uint8_t* __restrict__
     m[e] = bf16_as_float(mw[e] >> 16);
   }
 
-  Packed<8, BITS> pk[NL];
+  constexpr uint32_t kMask = (1u << BITS) - 1u;
+  uint32_t pc[NL];
 #pragma unroll
   for (int k = 0; k < NL; ++k) {
     const int t = min(g_first + r + RPL * k, n - 1);
-    pk[k] = load_packed<8, BITS>(codes + (size_t)t * ROW + c8 * BITS);
+    pc[k] = load_piece8<BITS, ROW>(codes + (size_t)t * ROW, c8);
   }
 #pragma unroll
   for (int k = 0; k < NL; ++k) {
     const int t = g_first + r + RPL * k;
-    uint32_t c[8];
-    unpack_codes<8, BITS>(pk[k], c);
     float y[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf((float)c[e], S[e], m[e]);
+    for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf((float)((pc[k] >> (BITS * e)) & kMask), S[e], m[e]);
     if (t < n) {
       u32x4 v = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
                  pack_bf16x2(y[6], y[7])};

@@ -156,6 +156,58 @@ __device__ __forceinline__ void fwht_quad(float (&x)[E], int j, float c) {
   for (int e = 0; e < E; ++e) x[e] = x[e] * c;
 }
 
+// Row-level exchanges for a token held by a row of R = D/8 lanes (8 channels
+// per lane): partner lane = lane ^ m for m = 1, 2, 4, 8, all within one
+// 16-lane DPP row.  xor 4 composes quad reverse (lane ^ 3) with the
+// half-row mirror (lane ^ 7); xor 8 is a rotation of the row by 8.
+constexpr int kQuadRev = 0x1B;       // quad_perm [3,2,1,0]
+constexpr int kRowHalfMirror = 0x141;
+constexpr int kRowRor8 = 0x128;
+
+template <int M>
+__device__ __forceinline__ float row_xor(float v) {
+  if constexpr (M == 1) return quad_swap<kQuadXor1>(v);
+  else if constexpr (M == 2) return quad_swap<kQuadXor2>(v);
+  else if constexpr (M == 4) return quad_swap<kRowHalfMirror>(quad_swap<kQuadRev>(v));
+  else {
+    static_assert(M == 8, "row exchange");
+    return quad_swap<kRowRor8>(v);
+  }
+}
+
+// Butterfly stage with partners in lane c ^ M (c = lane within the row).
+template <int M>
+__device__ __forceinline__ void fwht_row_stage(float (&x)[8], int c) {
+  const float sgn = (c & M) ? -1.0f : 1.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = __builtin_fmaf(x[e], sgn, row_xor<M>(x[e]));
+}
+
+// Full transform over D = 8R elements held by a row of R lanes (lane c holds
+// elements [8c, 8c + 8)): spans 1, 2, 4 in registers, then 8, 16, ... by
+// exchanges with lanes c ^ 1, c ^ 2, ..., then the scale.  Same butterfly
+// order as spans 1..D/2.
+template <int D>
+__device__ __forceinline__ void fwht_row(float (&x)[8], int c) {
+  fwht_lane<8>(x);
+  fwht_row_stage<1>(x, c);
+  fwht_row_stage<2>(x, c);
+  fwht_row_stage<4>(x, c);
+  if constexpr (D == 128) fwht_row_stage<8>(x, c);
+  static_assert(D == 64 || D == 128, "head_dim");
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = x[e] * fwht_scale<D>();
+}
+
+// BF16 round-to-nearest-even of two fp32 values, packed low/high, by the
+// hardware conversion (v_cvt_pk_bf16_f32).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2_hw(float lo, float hi) {
+  f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
 // ------------------------------------------------------------ bit packing
 
 // Packs N codes of BITS bits each, LSB-first, into W = ceil(N*BITS/32) words.
@@ -256,6 +308,25 @@ __device__ __forceinline__ Packed<N, BITS> load_packed(const uint8_t* src) {
     p.w[3] = v.w;
   }
   return p;
+}
+
+// The 8 codes of channels [8c, 8c + 8) of a packed token row: BITS bytes at
+// byte offset BITS*c.  Three-byte pieces are read as the two aligned dwords
+// around them (the second clamped to the row) and funnel-shifted.
+template <int BITS, int ROW>
+__device__ __forceinline__ uint32_t load_piece8(const uint8_t* row, int c) {
+  if constexpr (BITS == 2) {
+    return *(const uint16_t*)(row + 2 * c);
+  } else if constexpr (BITS == 4) {
+    return *(const uint32_t*)(row + 4 * c);
+  } else {
+    static_assert(BITS == 3 && ROW % 4 == 0, "piece");
+    const int o = 3 * c;
+    const uint32_t* w = (const uint32_t*)row;
+    const uint32_t lo = w[o >> 2];
+    const uint32_t hi = w[min((o >> 2) + 1, ROW / 4 - 1)];
+    return __builtin_amdgcn_alignbyte(hi, lo, (uint32_t)(o & 3)) & 0xFFFFFFu;
+  }
 }
 
 __device__ __forceinline__ void store_nt(u32x4* dst, u32x4 v) {
