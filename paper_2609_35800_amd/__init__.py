@@ -16,7 +16,8 @@ import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libheadguard.so")
+# HG_LIBRARY may name another build of the same ABI; default: the in-tree build.
+LIB_PATH = os.environ.get("HG_LIBRARY") or os.path.join(_HERE, "libheadguard.so")
 
 HG_BASE_MINMAX, HG_BASE_KIVI, HG_BASE_AKVQ = 0, 1, 2
 BASES = {"minmax": HG_BASE_MINMAX, "kivi": HG_BASE_KIVI, "akvq": HG_BASE_AKVQ}

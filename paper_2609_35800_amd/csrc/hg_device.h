@@ -66,6 +66,25 @@ __device__ __forceinline__ float quad_max(float v) {
 
 // --------------------------------------------------------- group scale rule
 
+// fp32 RN(1/L) for L = 2^b - 1.
+template <int LEVELS>
+__device__ __forceinline__ constexpr float inv_levels() {
+  static_assert(LEVELS == 3 || LEVELS == 7 || LEVELS == 15, "bits");
+  return LEVELS == 3 ? 0x1.555556p-2f : LEVELS == 7 ? 0x1.24924ap-3f : 0x1.111112p-4f;
+}
+
+// Correctly rounded d / L for finite d >= 0: the product with RN(1/L) is off by
+// at most one unit, and one fma residual step corrects it.  Equal to the IEEE
+// quotient for every non-negative finite fp32 d at L = 3, 7 and 15 (checked
+// exhaustively); three operations instead of a full division sequence.
+template <int LEVELS>
+__device__ __forceinline__ float div_levels(float d) {
+  const float y = inv_levels<LEVELS>();
+  const float q0 = d * y;
+  const float r = __builtin_fmaf(-q0, (float)LEVELS, d);
+  return __builtin_fmaf(r, y, q0);
+}
+
 // Metadata of a group with range [mn, mx] at LEVELS = 2^b - 1:
 // m = BF16 round-down of mn, S = BF16 round-up of (mx - m)/LEVELS, zeros
 // stored as +0, a positive S raised to at least 2^-126 (BF16 0x0080) so that
@@ -79,13 +98,13 @@ template <int LEVELS>
 __device__ __forceinline__ GroupScale group_scale(float mn, float mx) {
   uint32_t m16 = bf16_round_down(mn);
   m16 = (m16 == 0x8000u) ? 0u : m16;
-  float m = bf16_as_float(m16);
-  float s = (mx - m) / (float)LEVELS;          // IEEE division, correctly rounded
+  const float m = bf16_as_float(m16);
+  const float s = div_levels<LEVELS>(mx - m);
   uint32_t s16 = bf16_round_up(s);
   s16 = (s16 == 0x8000u) ? 0u : s16;
   s16 = (s16 != 0u && s16 < 0x0080u) ? 0x0080u : s16;
-  float S = bf16_as_float(s16);
-  float inv = 1.0f / (s16 ? S : 1.0f);         // IEEE division, correctly rounded
+  const float S = bf16_as_float(s16);
+  const float inv = 1.0f / (s16 ? S : 1.0f);  // IEEE division, correctly rounded
   GroupScale g;
   g.m = m;
   g.inv = s16 ? inv : 0.0f;
@@ -93,14 +112,17 @@ __device__ __forceinline__ GroupScale group_scale(float mn, float mx) {
   return g;
 }
 
-// Code of one element: clamp(rint((v - m) * inv), 0, LEVELS), in this order of
-// fp32 operations (no contraction).
-template <int LEVELS>
-__device__ __forceinline__ uint32_t code_of(float v, const GroupScale& g) {
-  float t = (v - g.m) * g.inv;
-  float r = __builtin_rintf(t);
-  r = fminf(fmaxf(r, 0.0f), (float)LEVELS);
-  return (uint32_t)r;
+// Code of one element, returned as the bit pattern of fl(t + 1.5*2^23) with
+// t = (v - m) * inv (two roundings, no contraction): for 0 <= t < 2^22 that
+// sum holds rint(t), ties to even, in its low bits above 0x4B400000.  Because
+// m <= v <= max, 1/S and (max - m)/L are correctly rounded and S >= that
+// quotient, 0 <= t <= L*(1 + 3*2^-24) < L + 1/2: rint(t) already lies in
+// [0, L], so the clamp of the definition never changes it.
+constexpr uint32_t kMagicBits = 0x4B400000u;
+
+__device__ __forceinline__ uint32_t code_bits(float v, const GroupScale& g) {
+  const float t = (v - g.m) * g.inv;
+  return __float_as_uint(t + 0x1.8p23f);
 }
 
 // ------------------------------------------------- Walsh-Hadamard transform
@@ -210,7 +232,7 @@ __device__ __forceinline__ uint32_t pack_bf16x2_hw(float lo, float hi) {
 
 // ------------------------------------------------------------ bit packing
 
-// Packs N codes of BITS bits each, LSB-first, into W = ceil(N*BITS/32) words.
+// The packed bits of N codes of BITS bits each, LSB-first, in W = ceil(N*BITS/32) words.
 template <int N, int BITS>
 struct Packed {
   static constexpr int kBits = N * BITS;
@@ -218,33 +240,45 @@ struct Packed {
   uint32_t w[W];
 };
 
+// Sum of the magic offsets (kMagicBits << s) that the whole-word codes of each
+// word carry, modulo 2^32.
 template <int N, int BITS>
-__device__ __forceinline__ Packed<N, BITS> pack_codes(const uint32_t (&q)[N]) {
+struct MagicBias {
+  uint32_t w[(N * BITS + 31) / 32];
+  constexpr MagicBias() : w() {
+    for (int e = 0; e < N; ++e) {
+      const int pos = e * BITS;
+      if ((pos % 32) + BITS <= 32) w[pos / 32] += kMagicBits << (pos % 32);
+    }
+  }
+};
+
+// Packs N codes given as magic bit patterns (kMagicBits + q).  Codes occupy
+// disjoint bits, so packing by addition equals packing by OR; each word starts
+// at minus the magic offsets it will receive, leaving one shift-add per code.
+// A code that straddles two words is reduced to q first.
+template <int N, int BITS>
+__device__ __forceinline__ Packed<N, BITS> pack_code_bits(const uint32_t (&cb)[N]) {
+  constexpr MagicBias<N, BITS> kBias{};
   Packed<N, BITS> p;
 #pragma unroll
-  for (int i = 0; i < Packed<N, BITS>::W; ++i) p.w[i] = 0u;
+  for (int i = 0; i < Packed<N, BITS>::W; ++i) p.w[i] = 0u - kBias.w[i];
 #pragma unroll
   for (int e = 0; e < N; ++e) {
     const int pos = e * BITS;
-    p.w[pos / 32] |= q[e] << (pos % 32);
-    if ((pos % 32) + BITS > 32) p.w[pos / 32 + 1] |= q[e] >> (32 - pos % 32);
+    const int sh = pos % 32;
+    if (sh + BITS <= 32) {
+      p.w[pos / 32] += cb[e] << sh;
+    } else {
+      const uint32_t q = cb[e] - kMagicBits;
+      p.w[pos / 32] += q << sh;
+      p.w[pos / 32 + 1] += q >> (32 - sh);
+    }
   }
   return p;
 }
 
-template <int N, int BITS>
-__device__ __forceinline__ void unpack_codes(const Packed<N, BITS>& p, uint32_t (&q)[N]) {
-  constexpr uint32_t kMask = (1u << BITS) - 1u;
-#pragma unroll
-  for (int e = 0; e < N; ++e) {
-    const int pos = e * BITS;
-    uint32_t v = p.w[pos / 32] >> (pos % 32);
-    if ((pos % 32) + BITS > 32) v |= p.w[pos / 32 + 1] << (32 - pos % 32);
-    q[e] = v & kMask;
-  }
-}
-
-// Stores / loads of a lane's packed piece at a byte address whose alignment is
+// Store of a lane's packed piece at a byte address whose alignment is
 // that of the piece: whole dwords for 32/64/96/128-bit pieces, 16-bit halves
 // for 48-bit pieces.
 template <int N, int BITS>
@@ -274,40 +308,6 @@ __device__ __forceinline__ void store_packed(uint8_t* dst, const Packed<N, BITS>
     u32x4 v = {p.w[0], p.w[1], p.w[2], p.w[3]};
     __builtin_nontemporal_store(v, (u32x4*)dst);
   }
-}
-
-template <int N, int BITS>
-__device__ __forceinline__ Packed<N, BITS> load_packed(const uint8_t* src) {
-  constexpr int kBits = N * BITS;
-  Packed<N, BITS> p;
-  if constexpr (kBits == 16) {
-    p.w[0] = *(const uint16_t*)src;
-  } else if constexpr (kBits == 24) {
-    p.w[0] = (uint32_t)src[0] | ((uint32_t)src[1] << 8) | ((uint32_t)src[2] << 16);
-  } else if constexpr (kBits == 32) {
-    p.w[0] = *(const uint32_t*)src;
-  } else if constexpr (kBits == 48) {
-    const uint16_t* s = (const uint16_t*)src;
-    p.w[0] = (uint32_t)s[0] | ((uint32_t)s[1] << 16);
-    p.w[1] = s[2];
-  } else if constexpr (kBits == 64) {
-    u32x2 v = *(const u32x2*)src;
-    p.w[0] = v.x;
-    p.w[1] = v.y;
-  } else if constexpr (kBits == 96) {
-    u32x3 v = *(const u32x3*)src;
-    p.w[0] = v.x;
-    p.w[1] = v.y;
-    p.w[2] = v.z;
-  } else {
-    static_assert(kBits == 128, "unsupported packed piece");
-    u32x4 v = *(const u32x4*)src;
-    p.w[0] = v.x;
-    p.w[1] = v.y;
-    p.w[2] = v.z;
-    p.w[3] = v.w;
-  }
-  return p;
 }
 
 // The 8 codes of channels [8c, 8c + 8) of a packed token row: BITS bytes at

@@ -81,8 +81,8 @@ __device__ __forceinline__ void quantize_tokens(const uint16_t* __restrict__ row
 
     uint32_t c[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) c[e] = code_of<LEVELS>(x[e], g);
-    const Packed<E, BITS> pk = pack_codes<E, BITS>(c);
+    for (int e = 0; e < E; ++e) c[e] = code_bits(x[e], g);
+    const Packed<E, BITS> pk = pack_code_bits<E, BITS>(c);
     if (t < n) {
       store_packed<E, BITS>(codes + (size_t)t * ROW + j * PIECE, pk);
       if (j == 0) __builtin_nontemporal_store(g.meta, meta + t);
@@ -144,8 +144,8 @@ __device__ __forceinline__ void quantize_kivi_keys(const uint16_t* __restrict__ 
     const int t = g_first + r + RPL * k;
     uint32_t cq[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) cq[e] = code_of<LEVELS>(x[k][e], g[e]);
-    const Packed<8, BITS> pk = pack_codes<8, BITS>(cq);
+    for (int e = 0; e < 8; ++e) cq[e] = code_bits(x[k][e], g[e]);
+    const Packed<8, BITS> pk = pack_code_bits<8, BITS>(cq);
     if (t < n) store_packed<8, BITS>(codes + (size_t)t * ROW + c8 * BITS, pk);
   }
   if (r == 0) {
