@@ -3,7 +3,8 @@
 // Quantization setup: entries are rounded to the base's levels and rebuilt as
 // floating-point values for attention).  x^ = bf16_rne(q*S + m); q*S is exact
 // (q < 16, S has 8 significant bits), so the fma equals the separate multiply
-// and add.  AKVQ keys are rotated back in fp32 before the BF16 rounding.
+// and add; the BF16 rounding is the hardware conversion (round to nearest
+// even, subnormals kept).  AKVQ keys are rotated back in fp32 before the BF16 rounding.
 // Protected rows come back from the side store; text rows are not written.
 //
 // Same tiling as the quantize kernels (a workgroup owns one (tensor, l, b, h)
@@ -50,8 +51,8 @@ __device__ __forceinline__ void dequantize_tokens(const uint8_t* __restrict__ co
     for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf((float)((pc[k] >> (BITS * e)) & kMask), S, m);
     if constexpr (ROTATE) fwht_row<D>(y, c);
     if (t < n) {
-      u32x4 v = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
-                 pack_bf16x2(y[6], y[7])};
+      u32x4 v = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
+                 pack_bf16x2_hw(y[6], y[7])};
       store_nt((u32x4*)(rows + (size_t)t * D + 8 * c), v);
     }
   }
@@ -93,8 +94,8 @@ __device__ __forceinline__ void dequantize_kivi_keys(const uint8_t* __restrict__
 #pragma unroll
     for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf((float)((pc[k] >> (BITS * e)) & kMask), S[e], m[e]);
     if (t < n) {
-      u32x4 v = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
-                 pack_bf16x2(y[6], y[7])};
+      u32x4 v = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
+                 pack_bf16x2_hw(y[6], y[7])};
       store_nt((u32x4*)(rows + (size_t)t * D + 8 * c8), v);
     }
   }

@@ -85,6 +85,16 @@ __device__ __forceinline__ float div_levels(float d) {
   return __builtin_fmaf(r, y, q0);
 }
 
+// Correctly rounded 1/S for a BF16 scale S in [2^-126, 2^101]: the hardware
+// reciprocal (within one unit) refined by one fma Newton step.  Equal to the
+// IEEE quotient 1/S for every such S (checked exhaustively over all BF16
+// values in the range).
+__device__ __forceinline__ float rcp_scale(float S) {
+  const float r0 = __builtin_amdgcn_rcpf(S);
+  const float e = __builtin_fmaf(-S, r0, 1.0f);
+  return __builtin_fmaf(r0, e, r0);
+}
+
 // Metadata of a group with range [mn, mx] at LEVELS = 2^b - 1:
 // m = BF16 round-down of mn, S = BF16 round-up of (mx - m)/LEVELS, zeros
 // stored as +0, a positive S raised to at least 2^-126 (BF16 0x0080) so that
@@ -104,7 +114,7 @@ __device__ __forceinline__ GroupScale group_scale(float mn, float mx) {
   s16 = (s16 == 0x8000u) ? 0u : s16;
   s16 = (s16 != 0u && s16 < 0x0080u) ? 0x0080u : s16;
   const float S = bf16_as_float(s16);
-  const float inv = 1.0f / (s16 ? S : 1.0f);  // IEEE division, correctly rounded
+  const float inv = rcp_scale(s16 ? S : 1.0f);  // correctly rounded 1/S
   GroupScale g;
   g.m = m;
   g.inv = s16 ? inv : 0.0f;
@@ -152,18 +162,25 @@ __device__ __forceinline__ void fwht_lane(float (&x)[E]) {
   }
 }
 
-// One butterfly stage whose partner elements live in lane j ^ (CTRL's xor):
-// the lower lane keeps p + q, the upper lane p - q (partner - own).  With the
-// sign folded into an exact multiply-by-one, both are one correctly rounded
-// fma.
-template <int E, int CTRL>
-__device__ __forceinline__ void fwht_cross(float (&x)[E], bool upper) {
-  const float sgn = upper ? -1.0f : 1.0f;
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    float partner = quad_swap<CTRL>(x[e]);
-    x[e] = __builtin_fmaf(x[e], sgn, partner);
-  }
+// Cross-lane butterfly stages carry a per-lane sign so that each stage is one
+// fma with a DPP operand.  Pairs are (lane, lane ^ M); the lower lane must
+// end with p + q and the upper with p - q (p the lower's value).  Each lane
+// computes v' = fma(partner, s, v) with s = +1 in the lower and -1 in the
+// upper lane: the lower gets p + q, the upper q - p = -(p - q).  The upper
+// lane thus holds its value negated; as stages use distinct lane bits, a lane
+// ends holding (-1)^popcount(lane & stage bits) times its value, and the final
+// multiply by c uses c with that sign.  Negation is exact and round to nearest
+// is symmetric, so every nonzero value equals the plain butterfly's bit for
+// bit.  An exact-zero difference is +0 in either operand order, so a carried
+// lane can end with -0 where the plain transform has +0; the final scale is
+// therefore fma(v, c*sign, +0), which turns -0 into +0 and leaves every other
+// product as the plain multiply rounds it.  The plain transform never yields
+// -0 from inputs without -0 (dequantized levels q*S + m are never -0); in the
+// quantizer the sign of a zero changes neither the range (its min is stored
+// as +0 when zero) nor any code.
+template <int CTRL>
+__device__ __forceinline__ float butterfly_fma(float v, float s) {
+  return __builtin_fmaf(quad_swap<CTRL>(v), s, v);
 }
 
 // Full transform over D = 4E elements held by a lane quad (lane j holds
@@ -172,10 +189,15 @@ __device__ __forceinline__ void fwht_cross(float (&x)[E], bool upper) {
 template <int E>
 __device__ __forceinline__ void fwht_quad(float (&x)[E], int j, float c) {
   fwht_lane<E>(x);
-  fwht_cross<E, kQuadXor1>(x, (j & 1) != 0);
-  fwht_cross<E, kQuadXor2>(x, (j & 2) != 0);
+  const float s1 = (j & 1) ? -1.0f : 1.0f;
+  const float s2 = (j & 2) ? -1.0f : 1.0f;
 #pragma unroll
-  for (int e = 0; e < E; ++e) x[e] = x[e] * c;
+  for (int e = 0; e < E; ++e) x[e] = butterfly_fma<kQuadXor1>(x[e], s1);
+#pragma unroll
+  for (int e = 0; e < E; ++e) x[e] = butterfly_fma<kQuadXor2>(x[e], s2);
+  const float cs = c * s1 * s2;  // c with the carried sign, exact
+#pragma unroll
+  for (int e = 0; e < E; ++e) x[e] = __builtin_fmaf(x[e], cs, 0.0f);
 }
 
 // Row-level exchanges for a token held by a row of R = D/8 lanes (8 channels
@@ -197,28 +219,32 @@ __device__ __forceinline__ float row_xor(float v) {
   }
 }
 
-// Butterfly stage with partners in lane c ^ M (c = lane within the row).
-template <int M>
-__device__ __forceinline__ void fwht_row_stage(float (&x)[8], int c) {
-  const float sgn = (c & M) ? -1.0f : 1.0f;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) x[e] = __builtin_fmaf(x[e], sgn, row_xor<M>(x[e]));
-}
-
 // Full transform over D = 8R elements held by a row of R lanes (lane c holds
 // elements [8c, 8c + 8)): spans 1, 2, 4 in registers, then 8, 16, ... by
-// exchanges with lanes c ^ 1, c ^ 2, ..., then the scale.  Same butterfly
-// order as spans 1..D/2.
+// exchanges with lanes c ^ 1, c ^ 2, ..., each a sign-carrying fma stage (see
+// fwht_quad), then the scale.  Same butterfly order as spans 1..D/2.
+template <int M>
+__device__ __forceinline__ void fwht_row_stage(float (&x)[8], float s) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = __builtin_fmaf(row_xor<M>(x[e]), s, x[e]);
+}
+
 template <int D>
 __device__ __forceinline__ void fwht_row(float (&x)[8], int c) {
-  fwht_lane<8>(x);
-  fwht_row_stage<1>(x, c);
-  fwht_row_stage<2>(x, c);
-  fwht_row_stage<4>(x, c);
-  if constexpr (D == 128) fwht_row_stage<8>(x, c);
   static_assert(D == 64 || D == 128, "head_dim");
+  fwht_lane<8>(x);
+  const float s1 = (c & 1) ? -1.0f : 1.0f, s2 = (c & 2) ? -1.0f : 1.0f;
+  const float s4 = (c & 4) ? -1.0f : 1.0f, s8 = (c & 8) ? -1.0f : 1.0f;
+  fwht_row_stage<1>(x, s1);
+  fwht_row_stage<2>(x, s2);
+  fwht_row_stage<4>(x, s4);
+  float cs = fwht_scale<D>() * s1 * s2 * s4;
+  if constexpr (D == 128) {
+    fwht_row_stage<8>(x, s8);
+    cs = cs * s8;
+  }
 #pragma unroll
-  for (int e = 0; e < 8; ++e) x[e] = x[e] * fwht_scale<D>();
+  for (int e = 0; e < 8; ++e) x[e] = __builtin_fmaf(x[e], cs, 0.0f);
 }
 
 // BF16 round-to-nearest-even of two fp32 values, packed low/high, by the

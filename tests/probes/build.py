@@ -1,0 +1,22 @@
+"""Build the device arithmetic probes (test infrastructure) for gfx950."""
+import os
+import subprocess
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+LIB = os.path.join(HERE, "libhg_probes.so")
+
+
+def build() -> str:
+    import sys
+    sys.path.insert(0, ROOT)
+    from paper_2609_35800_amd.build import FLAGS
+    tmp = LIB + ".tmp"
+    subprocess.check_call([os.environ.get("HIPCC", "/opt/rocm/bin/hipcc"), *FLAGS, "-o", tmp,
+                           os.path.join(HERE, "hg_probes.hip")])
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build())

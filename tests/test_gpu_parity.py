@@ -85,7 +85,7 @@ def _special_values(w, K, V):
         X[0, 0, 0, s + 4] = torch.linspace(1e-38, 3e-38, w.D).to(bf)   # tiny range
         X[0, 0, 0, s + 5] = torch.linspace(-2e-39, 2e-39, w.D).to(bf)  # subnormal span
         X[0, 0, 0, s + 6] = (torch.arange(w.D) % 8).to(bf) * 0.5      # exact ties
-        X[0, 0, 0, s + 7] = torch.linspace(-1e29, 8e28, w.D).to(bf)    # large (< 2^100)
+        X[0, 0, 0, s + 7] = torch.linspace(-7e28, 5e28, w.D).to(bf)    # large (< 2^96)
         X[0, 0, 0, s + 8] = 0.0
         X[0, 0, 0, s + 8, 5] = 1e-40                             # one denormal
         # the same token in a KIVI group: per-channel constants
