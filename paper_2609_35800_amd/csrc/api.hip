@@ -90,6 +90,7 @@ int check_device_ptr(const void* p, const char* name) {
   return HG_OK;
 }
 
+// Checks that a HIP device is present.
 int check_device() {
   int n = 0;
   hipError_t e = hipGetDeviceCount(&n);
@@ -142,7 +143,7 @@ void fill_params(hg::Params& p, const hg_config* c, const uint8_t* mask) {
     uint32_t word = 0;
     for (int b = 0; b < 32 && 32 * w + b < LH; ++b) word |= (uint32_t)(mask[32 * w + b] & 1u) << b;
     p.route.mask[w] = word;
-    p.route.prefix[w] = (uint16_t)running;
+    p.route.prefix[w] = running;
     running += (uint32_t)__builtin_popcount(word);
   }
 }

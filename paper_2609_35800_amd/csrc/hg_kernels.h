@@ -23,12 +23,12 @@ constexpr int kMaskWords = HG_MAX_HEADS / 32;
 // bits of word i/32 (§3: a base must be able to skip individual heads).
 struct Route {
   uint32_t mask[kMaskWords];
-  uint16_t prefix[kMaskWords];
+  uint32_t prefix[kMaskWords];  // 32-bit so the kernels read it with scalar loads
 };
 
 // One launch covers K (tensor 0) and V (tensor 1): blocks [0, blocks_k) take
-// K tiles, the rest V tiles.  Each block takes one (tensor, l, b, h) slice
-// and kBlockTokens consecutive image tokens of it.
+// K tiles, the rest V tiles.  Each block takes one (tensor, l, b, h) slice and
+// kBlockTokens consecutive image tokens of it.
 struct Params {
   const uint16_t* cache[2];  // quantize: K, V input; dequantize: K_out, V_out
   uint8_t* codes[2];
@@ -49,25 +49,19 @@ hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t 
 hipError_t launch_dequantize(const Params& p, int base, int D, int bits, uint32_t blocks,
                              hipStream_t stream);
 
-// Slice decoding shared by the kernels: which tensor, slice and tile a block
-// owns, whether the slice is kept in BF16, and its slot in the packed buffers.
-struct Slice {
-  int X;            // 0 = K, 1 = V
-  int tile;         // token tile within the slice
-  uint32_t s;       // (l*B + b)*H + h
+// Routing of one (tensor, slice): whether it is kept in BF16 and its slot in
+// the packed buffers (rank among kept heads if kept, else among quantized
+// heads).  Wave-uniform scalar work.
+struct SliceRoute {
   int b;
-  bool kept;        // kept in BF16 (protected)
-  uint32_t slot;    // rank among kept heads if kept, else among quantized heads
+  bool kept;
+  uint32_t slot;
 };
 
-__device__ __forceinline__ Slice decode_block(const Params& p, uint32_t bid) {
-  Slice r;
-  r.X = bid >= p.blocks_k ? 1 : 0;
-  uint32_t rel = bid - (r.X ? p.blocks_k : 0u);
-  r.tile = (int)(rel % (uint32_t)p.tiles);
-  r.s = rel / (uint32_t)p.tiles;
-  const uint32_t h = r.s % (uint32_t)p.H;
-  const uint32_t lb = r.s / (uint32_t)p.H;
+__device__ __forceinline__ SliceRoute route_slice(const Params& p, int X, uint32_t s) {
+  SliceRoute r;
+  const uint32_t h = s % (uint32_t)p.H;
+  const uint32_t lb = s / (uint32_t)p.H;
   r.b = (int)(lb % (uint32_t)p.B);
   const uint32_t l = lb / (uint32_t)p.B;
   const uint32_t i = l * (uint32_t)p.H + h;
@@ -75,15 +69,37 @@ __device__ __forceinline__ Slice decode_block(const Params& p, uint32_t bid) {
   const bool masked = (w >> (i & 31u)) & 1u;
   const uint32_t rank = (uint32_t)p.route.prefix[i >> 5] +
                         (uint32_t)__builtin_popcount(w & ((1u << (i & 31u)) - 1u));
-  const bool v_kept_allowed = (r.X == 0) || !p.keys_only;
-  r.kept = masked && v_kept_allowed;
+  r.kept = masked && (X == 0 || !p.keys_only);
   if (r.kept) {
     r.slot = rank;
-  } else if (r.X == 1 && p.keys_only) {
+  } else if (X == 1 && p.keys_only) {
     r.slot = i;  // K-only mode: every V head is quantized
   } else {
     r.slot = i - rank;
   }
+  return r;
+}
+
+// Block decoding: tensor, slice, token tile and routing of a workgroup.
+struct Slice {
+  int X;            // 0 = K, 1 = V
+  int tile;         // token tile within the slice
+  uint32_t s;       // (l*B + b)*H + h
+  int b;
+  bool kept;
+  uint32_t slot;
+};
+
+__device__ __forceinline__ Slice decode_block(const Params& p, uint32_t bid) {
+  Slice r;
+  r.X = bid >= p.blocks_k ? 1 : 0;
+  const uint32_t rel = bid - (r.X ? p.blocks_k : 0u);
+  r.tile = (int)(rel % (uint32_t)p.tiles);
+  r.s = rel / (uint32_t)p.tiles;
+  const SliceRoute sr = route_slice(p, r.X, r.s);
+  r.b = sr.b;
+  r.kept = sr.kept;
+  r.slot = sr.slot;
   return r;
 }
 
