@@ -1,0 +1,174 @@
+"""Host-side tests of the C ABI (include/headguard.h), runnable without a GPU:
+the library loads and exports every declared entry point; hg_packed_sizes
+agrees with the oracle's independent size computation and the paper's
+storage estimate (§5.4); every argument error is reported with its status
+before any device work; the product fails loudly without its library and
+never touches the oracle."""
+import ctypes as C
+import os
+import re
+import subprocess
+import sys
+import threading
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2609_35800_amd as hg
+from conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "headguard.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(hg_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert set(names) == {"hg_packed_sizes", "hg_quantize", "hg_dequantize",
+                          "hg_status_string", "hg_last_error"}
+    lib = C.CDLL(hg.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", hg.LIB_PATH], capture_output=True, text=True)
+    exported = set(re.findall(r"\bT (hg_\w+)", out.stdout))
+    assert set(names) <= exported
+
+
+def test_status_strings():
+    for i, name in enumerate(hg.STATUS):
+        assert hg.hg_status_string(i) == name
+    assert hg.hg_status_string(99) == "HG_ERR_UNKNOWN"
+
+
+def _cfg(**kw):
+    f = dict(L=2, B=3, H=4, T=40, D=128, img_start=5, img_len=30, bits=2, base=0,
+             keys_only=0, kivi_group=32)
+    f.update(kw)
+    return f
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_sizes_match_oracle(seed):
+    rng = np.random.default_rng(seed)
+    L, H = int(rng.integers(1, 9)), int(rng.integers(1, 9))
+    T = int(rng.integers(1, 300))
+    s0 = int(rng.integers(0, T))
+    f = _cfg(L=L, B=int(rng.integers(1, 5)), H=H, T=T, D=int(rng.choice([64, 128])),
+             img_start=s0, img_len=int(rng.integers(0, T - s0 + 1)), bits=int(rng.integers(2, 5)),
+             base=int(rng.integers(0, 3)), keys_only=int(rng.integers(0, 2)))
+    mask = (rng.random(L * H) < 0.2).astype(np.uint8)
+    got = hg.hg_packed_sizes(hg.make_config(**f), mask)
+    want = oracle.sizes(oracle.make_config(**f), mask)
+    assert got == want
+
+
+def test_storage_model_bits_per_element():
+    """§5.4: 2.25 / 3.97 / 3.11 bits per image element at D = 128, 2 bits, 1/8."""
+    mask = np.zeros(64, np.uint8)
+    mask[::8] = 1
+    for m, ko, want in ((np.zeros(64, np.uint8), 0, 2.25), (mask, 0, 3.96875), (mask, 1, 3.109375)):
+        s = hg.hg_packed_sizes(hg.make_config(**_cfg(L=8, H=8, B=1, T=16, img_start=0, img_len=16,
+                                                     keys_only=ko)), m)
+        total = sum(s[n] for n in hg.BUFFERS)
+        assert total * 8 / (2 * 64 * 16 * 128) == want
+
+
+BAD = [
+    (dict(L=0), hg.HG_ERR_SHAPE), (dict(B=-1), hg.HG_ERR_SHAPE), (dict(T=0), hg.HG_ERR_SHAPE),
+    (dict(L=128, H=65), hg.HG_ERR_SHAPE), (dict(keys_only=2), hg.HG_ERR_SHAPE),
+    (dict(D=96), hg.HG_ERR_HEADDIM), (dict(D=256), hg.HG_ERR_HEADDIM),
+    (dict(img_start=-1), hg.HG_ERR_SPAN), (dict(img_start=20, img_len=21), hg.HG_ERR_SPAN),
+    (dict(img_len=-3), hg.HG_ERR_SPAN),
+    (dict(bits=1), hg.HG_ERR_BITS), (dict(bits=5), hg.HG_ERR_BITS),
+    (dict(base=3), hg.HG_ERR_BASE), (dict(base=1, kivi_group=16), hg.HG_ERR_BASE),
+]
+
+
+@pytest.mark.parametrize("kw,status", BAD, ids=[str(b[0]) for b in BAD])
+def test_invalid_config(kw, status):
+    f = _cfg(**kw)
+    mask = np.zeros(max(f["L"], 1) * max(f["H"], 1), np.uint8)
+    cfg = hg.make_config(**f)
+    with pytest.raises(hg.HeadGuardError) as e:
+        hg.hg_packed_sizes(cfg, mask)
+    assert e.value.status == status
+    assert hg.hg_last_error()  # a detail message is set
+    lib = hg.library()
+    pk = hg.hg_packed()
+    rc = lib.hg_quantize(C.byref(cfg), 16, 16, mask.ctypes.data_as(C.c_void_p), C.byref(pk), None)
+    assert rc == status  # checked before any device work
+    rc = lib.hg_dequantize(C.byref(cfg), mask.ctypes.data_as(C.c_void_p), C.byref(pk), 16, 16, None)
+    assert rc == status
+
+
+def test_mask_values_and_nulls():
+    cfg = hg.make_config(**_cfg())
+    lib = hg.library()
+    bad = np.zeros(8, np.uint8)
+    bad[3] = 2
+    with pytest.raises(hg.HeadGuardError) as e:
+        hg.hg_packed_sizes(cfg, bad)
+    assert e.value.status == hg.HG_ERR_MASK
+    sizes = hg.hg_sizes()
+    assert lib.hg_packed_sizes(None, bad.ctypes.data_as(C.c_void_p), C.byref(sizes)) == hg.HG_ERR_NULL
+    assert lib.hg_packed_sizes(C.byref(cfg), None, C.byref(sizes)) == hg.HG_ERR_NULL
+    good = np.zeros(8, np.uint8)
+    assert lib.hg_packed_sizes(C.byref(cfg), good.ctypes.data_as(C.c_void_p), None) == hg.HG_ERR_NULL
+    pk = hg.hg_packed()
+    m = good.ctypes.data_as(C.c_void_p)
+    assert lib.hg_quantize(C.byref(cfg), None, 16, m, C.byref(pk), None) == hg.HG_ERR_NULL
+    assert lib.hg_quantize(C.byref(cfg), 16, 16, m, None, None) == hg.HG_ERR_NULL
+    assert lib.hg_dequantize(C.byref(cfg), m, C.byref(pk), None, 16, None) == hg.HG_ERR_NULL
+
+
+def test_no_device_is_reported_not_crashed():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    cfg = hg.make_config(**_cfg())
+    mask = np.zeros(8, np.uint8)
+    lib = hg.library()
+    pk = hg.hg_packed()
+    rc = lib.hg_quantize(C.byref(cfg), 16, 16, mask.ctypes.data_as(C.c_void_p), C.byref(pk), None)
+    assert rc == hg.HG_ERR_NO_DEVICE
+
+
+def test_error_detail_is_per_thread():
+    lib = hg.library()
+    cfg_bits = hg.make_config(**_cfg(bits=9))
+    cfg_span = hg.make_config(**_cfg(img_len=99))
+    mask = np.zeros(8, np.uint8)
+    seen = {}
+
+    def worker(name, cfg):
+        out = hg.hg_sizes()
+        for _ in range(200):
+            lib.hg_packed_sizes(C.byref(cfg), mask.ctypes.data_as(C.c_void_p), C.byref(out))
+        seen[name] = hg.hg_last_error()
+
+    ts = [threading.Thread(target=worker, args=("bits", cfg_bits)),
+          threading.Thread(target=worker, args=("span", cfg_span))]
+    [t.start() for t in ts]
+    [t.join() for t in ts]
+    assert "bits" in seen["bits"] and "span" in seen["span"]
+
+
+def test_missing_library_fails_loudly():
+    code = "import paper_2609_35800_amd"
+    env = dict(os.environ, HG_LIBRARY=os.path.join(ROOT, "no_such_libheadguard.so"))
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True)
+    assert r.returncode != 0 and "ImportError" in r.stderr
+
+
+def test_product_never_touches_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2609_35800_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in text.lower(), f
+                assert "hg_oracle" not in text and "hgo_" not in text, f

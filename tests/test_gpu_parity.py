@@ -126,3 +126,26 @@ def test_side_stream_and_determinism():
     for n in a[0]:
         assert np.array_equal(a[0][n], b[0][n])
     assert np.array_equal(a[1], b[1]) and np.array_equal(a[2], b[2])
+
+
+def test_pointer_errors_are_caught_before_launch():
+    """Host memory and misaligned device pointers are rejected with a status;
+    no kernel runs and the outputs keep their canaries."""
+    import paper_2609_35800_amd as hg
+    from hgtest import alloc_with_canary, canaries_intact
+    w = small("minmax", img_len=64)
+    K, V = synthkv.gen_kv(w)
+    mask = synthkv.protect_mask(w)
+    cfg = hg.make_config(**w.config_fields())
+    packed, raw = alloc_with_canary(hg.hg_packed_sizes(cfg, mask))
+    Kg, Vg = K.cuda(), V.cuda()
+    with pytest.raises(hg.HeadGuardError) as e:
+        hg.hg_quantize(cfg, K, Vg, mask, packed)  # K in host memory
+    assert e.value.status == hg.HG_ERR_POINTER
+    flat = torch.empty(Kg.numel() + 8, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(hg.HeadGuardError) as e:
+        hg.hg_quantize(cfg, flat[1:].data_ptr(), Vg, mask, packed)  # 2-byte offset
+    assert e.value.status == hg.HG_ERR_ALIGN
+    torch.cuda.synchronize()
+    assert canaries_intact(raw)
+    assert all(bool((packed[n] == 0xA5).all()) for n in packed if packed[n].numel())
