@@ -78,7 +78,8 @@ enum {
   HG_ERR_MASK = 8,      /* a mask entry is neither 0 nor 1                     */
   HG_ERR_NO_DEVICE = 9, /* no usable HIP device                                */
   HG_ERR_HIP = 10,      /* the HIP runtime reported an error (launch, pointer) */
-  HG_ERR_POINTER = 11   /* a buffer argument is not device memory              */
+  HG_ERR_POINTER = 11,  /* a buffer argument is not device memory              */
+  HG_ERR_VALUE = 12     /* a head score is not finite                          */
 };
 
 /* Largest L*H the mask routing holds in kernel arguments. */
@@ -122,6 +123,18 @@ int hg_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
  * text rows of K_out, V_out are not written. */
 int hg_dequantize(const hg_config* cfg, const uint8_t* protect_mask, const hg_packed* in,
                   uint16_t* K_out, uint16_t* V_out, hipStream_t stream);
+
+/* Head selection (§3 "Selecting physical KV heads", Eq. 2): the protection
+ * mask from offline sensitivity scores.  g and o are host fp64 arrays
+ * [L][Hq] of per-query-head image- and output-sensitivity scores (Eq. 1);
+ * query heads h*(Hq/Hkv) .. h*(Hq/Hkv) + Hq/Hkv - 1 share KV head h.  Each
+ * KV head's scores are the means over its query heads; each score is
+ * standardized over all L*Hkv KV heads (population deviation; a constant
+ * score gives 0); s = z(g) + z(o); the K heads with the largest s are marked
+ * in mask_out (host uint8 [L*Hkv], row-major (l, h)), ties to the lower index.
+ * The paper's main budget is K = round(L*Hkv/8).  Pure host computation. */
+int hg_select_heads(const double* g, const double* o, int32_t L, int32_t Hq, int32_t Hkv,
+                    int32_t K, uint8_t* mask_out);
 
 /* Static name of a status code. */
 const char* hg_status_string(int status);

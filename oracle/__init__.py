@@ -72,8 +72,9 @@ def lib():
         L.hgo_dequantize_slice.argtypes = [C.POINTER(Config), C.c_int, P, P, P]
         L.hgo_quantize.argtypes = [C.POINTER(Config), P, P, P, P, P, P, P, P, P, C.c_int]
         L.hgo_dequantize.argtypes = [C.POINTER(Config), P, P, P, P, P, P, P, P, P, C.c_int]
+        L.hgo_select_heads.argtypes = [P, P, C.c_int, C.c_int, C.c_int, C.c_int, P]
         for f in ("hgo_route", "hgo_sizes", "hgo_quantize_slice", "hgo_dequantize_slice",
-                  "hgo_quantize", "hgo_dequantize"):
+                  "hgo_quantize", "hgo_dequantize", "hgo_select_heads"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -214,3 +215,14 @@ def dequantize(cfg: Config, mask: np.ndarray, packed: Dict[str, np.ndarray],
                               _ptr(K_out), _ptr(V_out), int(threads))
     if rc:
         raise ValueError("hgo_dequantize failed")
+
+
+def select_heads(g: np.ndarray, o: np.ndarray, Hkv: int, K: int) -> np.ndarray:
+    """Protection mask uint8 [L*Hkv] from per-query-head scores g, o [L][Hq]."""
+    g = np.ascontiguousarray(g, dtype=np.float64)
+    o = np.ascontiguousarray(o, dtype=np.float64)
+    L, Hq = g.shape
+    mask = np.zeros(L * Hkv, dtype=np.uint8)
+    if lib().hgo_select_heads(_ptr(g), _ptr(o), L, Hq, Hkv, int(K), _ptr(mask)):
+        raise ValueError("hgo_select_heads: bad arguments")
+    return mask

@@ -399,3 +399,56 @@ int hgo_dequantize(const hgo_config* c, const uint8_t* mask,
   j.out[0] = K_out; j.out[1] = V_out;
   return run_all(&j, threads);
 }
+
+/* ------------------------------------------------------------ head selection
+ *
+ * §3 "Selecting physical KV heads", Eq. 2.  Readings: a query head hq belongs
+ * to the KV head hq / (Hq/Hkv) (consecutive query heads share a KV head);
+ * z() uses the population standard deviation over all L*Hkv KV heads, and a
+ * zero deviation gives z = 0; TopK breaks ties toward the lower head index.
+ */
+static void zscore(double* x, int n) {
+  double mean = 0.0, var = 0.0;
+  for (int i = 0; i < n; ++i) mean += x[i];
+  mean /= n;
+  for (int i = 0; i < n; ++i) var += (x[i] - mean) * (x[i] - mean);
+  var /= n;
+  double sd = sqrt(var);
+  for (int i = 0; i < n; ++i) x[i] = sd > 0.0 ? (x[i] - mean) / sd : 0.0;
+}
+
+int hgo_select_heads(const double* g, const double* o, int L, int Hq, int Hkv, int K,
+                     uint8_t* mask) {
+  if (!g || !o || !mask || L <= 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv != 0 || K < 0) return -1;
+  int n = L * Hkv, rep = Hq / Hkv;
+  double* gb = (double*)calloc((size_t)n, sizeof(double));
+  double* ob = (double*)calloc((size_t)n, sizeof(double));
+  double* sc = (double*)calloc((size_t)n, sizeof(double));
+  if (!gb || !ob || !sc) { free(gb); free(ob); free(sc); return -1; }
+  /* GQA average of the query heads of each physical KV head */
+  for (int l = 0; l < L; ++l)
+    for (int hq = 0; hq < Hq; ++hq) {
+      int i = l * Hkv + hq / rep;
+      gb[i] += g[(size_t)l * Hq + hq];
+      ob[i] += o[(size_t)l * Hq + hq];
+    }
+  for (int i = 0; i < n; ++i) {
+    gb[i] /= rep;
+    ob[i] /= rep;
+  }
+  zscore(gb, n);
+  zscore(ob, n);
+  for (int i = 0; i < n; ++i) sc[i] = gb[i] + ob[i];
+  /* TopK: K times, take the largest remaining score (lowest index on ties) */
+  for (int i = 0; i < n; ++i) mask[i] = 0;
+  for (int k = 0; k < K && k < n; ++k) {
+    int best = -1;
+    for (int i = 0; i < n; ++i)
+      if (!mask[i] && (best < 0 || sc[i] > sc[best])) best = i;
+    mask[best] = 1;
+  }
+  free(gb);
+  free(ob);
+  free(sc);
+  return 0;
+}

@@ -97,6 +97,13 @@ int hgo_dequantize(const hgo_config* c, const uint8_t* mask,
                    const uint16_t* side_v,
                    uint16_t* K_out, uint16_t* V_out, int threads);
 
+/* Head selection (§3 Eq. 2): g, o are per-query-head scores [L][Hq] (fp64);
+ * query head hq belongs to KV head hq / (Hq/Hkv).  Writes mask[L*Hkv] with
+ * the K heads of largest s = z(mean g) + z(mean o) set (ties: lower index).
+ * Returns 0, or -1 on a bad argument. */
+int hgo_select_heads(const double* g, const double* o, int L, int Hq, int Hkv, int K,
+                     uint8_t* mask);
+
 #ifdef __cplusplus
 }
 #endif

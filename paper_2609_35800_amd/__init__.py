@@ -23,7 +23,7 @@ HG_BASE_MINMAX, HG_BASE_KIVI, HG_BASE_AKVQ = 0, 1, 2
 BASES = {"minmax": HG_BASE_MINMAX, "kivi": HG_BASE_KIVI, "akvq": HG_BASE_AKVQ}
 STATUS = ("HG_OK", "HG_ERR_NULL", "HG_ERR_SHAPE", "HG_ERR_SPAN", "HG_ERR_BITS", "HG_ERR_BASE",
           "HG_ERR_HEADDIM", "HG_ERR_ALIGN", "HG_ERR_MASK", "HG_ERR_NO_DEVICE", "HG_ERR_HIP",
-          "HG_ERR_POINTER")
+          "HG_ERR_POINTER", "HG_ERR_VALUE")
 for _i, _n in enumerate(STATUS):
     globals()[_n] = _i
 BUFFERS = ("codes_k", "meta_k", "side_k", "codes_v", "meta_v", "side_v")
@@ -61,7 +61,8 @@ def _load():
     lib.hg_packed_sizes.argtypes = [C.POINTER(hg_config), P, C.POINTER(hg_sizes)]
     lib.hg_quantize.argtypes = [C.POINTER(hg_config), P, P, P, C.POINTER(hg_packed), P]
     lib.hg_dequantize.argtypes = [C.POINTER(hg_config), P, C.POINTER(hg_packed), P, P, P]
-    for f in ("hg_packed_sizes", "hg_quantize", "hg_dequantize"):
+    lib.hg_select_heads.argtypes = [P, P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, P]
+    for f in ("hg_packed_sizes", "hg_quantize", "hg_dequantize", "hg_select_heads"):
         getattr(lib, f).restype = C.c_int
     lib.hg_status_string.argtypes = [C.c_int]
     lib.hg_status_string.restype = C.c_char_p
@@ -155,3 +156,23 @@ def alloc_packed(cfg: hg_config, protect_mask, device="cuda") -> Dict[str, torch
     """Device buffers of the sizes hg_packed_sizes reports (uint8 tensors)."""
     sz = hg_packed_sizes(cfg, protect_mask)
     return {n: torch.empty(sz[n], dtype=torch.uint8, device=device) for n in BUFFERS}
+
+
+# ------------------------------------------------------------ head selection
+
+def hg_select_heads(g, o, Hkv: int, K: int) -> np.ndarray:
+    """Protection mask uint8 [L*Hkv] from per-query-head scores g, o [L][Hq]."""
+    g = np.ascontiguousarray(g, dtype=np.float64)
+    o = np.ascontiguousarray(o, dtype=np.float64)
+    if g.shape != o.shape or g.ndim != 2:
+        raise ValueError("g and o must both be [L, Hq]")
+    L, Hq = g.shape
+    mask = np.zeros(L * Hkv, dtype=np.uint8)
+    _check(_lib.hg_select_heads(g.ctypes.data_as(C.c_void_p), o.ctypes.data_as(C.c_void_p),
+                                L, Hq, Hkv, int(K), mask.ctypes.data_as(C.c_void_p)))
+    return mask
+
+
+def head_budget(n_kv: int, fraction: float = 1.0 / 8.0) -> int:
+    """K = round(n_kv * fraction), halves rounded up (the paper's budget rule)."""
+    return int(np.floor(n_kv * fraction + 0.5))

@@ -150,6 +150,15 @@ void fill_params(hg::Params& p, const hg_config* c, const uint8_t* mask) {
 
 }  // namespace
 
+namespace hg {
+// Records the detail of a status for hg_last_error (used by the other host
+// sources of the library).
+int set_error(int status, const char* msg) {
+  g_last_error = status == HG_OK ? "" : msg;
+  return status;
+}
+}  // namespace hg
+
 extern "C" {
 
 const char* hg_status_string(int s) {
@@ -166,6 +175,7 @@ const char* hg_status_string(int s) {
     case HG_ERR_NO_DEVICE: return "HG_ERR_NO_DEVICE";
     case HG_ERR_HIP: return "HG_ERR_HIP";
     case HG_ERR_POINTER: return "HG_ERR_POINTER";
+    case HG_ERR_VALUE: return "HG_ERR_VALUE";
     default: return "HG_ERR_UNKNOWN";
   }
 }

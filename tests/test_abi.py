@@ -28,8 +28,8 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert set(names) == {"hg_packed_sizes", "hg_quantize", "hg_dequantize",
-                          "hg_status_string", "hg_last_error"}
+    assert {"hg_packed_sizes", "hg_quantize", "hg_dequantize", "hg_select_heads",
+            "hg_status_string", "hg_last_error"} <= set(names)
     lib = C.CDLL(hg.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n

@@ -4,8 +4,8 @@ it, and runs the pin suites against the mutant: at least one pin must fail.
 The planted mistakes cover each step of the method: rounding directions and
 tie rules, the range, the scale and its levels, reconstruction, the
 Walsh-Hadamard butterflies and scale, routing ranks and K-only protection,
-KIVI-style group indexing, bit packing, the image-span offset and the
-buffer sizes."""
+KIVI-style group indexing, bit packing, the image-span offset, the buffer
+sizes, and the head selection's sum, grouping, standardization and ties."""
 import concurrent.futures as cf
 import os
 import shutil
@@ -55,6 +55,12 @@ MUTANTS = [
     ("negative_zero_min_kept", "if (m16 == 0x8000u) m16 = 0;", ""),
     ("no_scale_floor", "if (s16 != 0 && hgo_bf16_to_f32(s16) < 0x1p-126f) s16 = 0x0080u; /* 2^-126 */", ""),
     ("zero_range_not_special", "if (s16 == 0) {", "if (s16 == 0 && 0) {"),
+    ("select_difference", "sc[i] = gb[i] + ob[i];", "sc[i] = gb[i] - ob[i];"),
+    ("select_interleaved_groups", "int i = l * Hkv + hq / rep;", "int i = l * Hkv + hq % Hkv;"),
+    ("select_g_not_standardized", "zscore(gb, n);", ""),
+    ("select_ties_to_upper", "if (!mask[i] && (best < 0 || sc[i] > sc[best])) best = i;",
+     "if (!mask[i] && (best < 0 || sc[i] >= sc[best])) best = i;"),
+    ("select_mean_off_by_one", "  mean /= n;", "  mean /= n + 1;"),
 ]
 
 
@@ -73,7 +79,8 @@ def _run_mutant(name, old, new, tmp):
     env = dict(os.environ, HG_ORACLE_LIB=so, OMP_NUM_THREADS="1")
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(ROOT, "tests", "test_oracle_pins.py"),
-                        os.path.join(ROOT, "tests", "test_oracle_cache.py")],
+                        os.path.join(ROOT, "tests", "test_oracle_cache.py"),
+                        os.path.join(ROOT, "tests", "test_select_pins.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     return name, r.returncode
 
