@@ -43,6 +43,9 @@ def parse():
                     help="also run a plain 1 GiB device copy (for counter scaling)")
     ap.add_argument("--quant-only", action="store_true",
                     help="time only the quantize launches (for profiling that kernel)")
+    ap.add_argument("--op", default="step", choices=["step", "fakequant"],
+                    help="step: quantize+pack then dequantize (the default line); "
+                         "fakequant: the one-pass simulated quantization alone")
     return ap.parse_args()
 
 
@@ -115,6 +118,41 @@ def cpu_baseline(w, K, V, mask, budget_s: float):
             "image_tokens_per_s": round(w.B * w.img_len * nl / w.L / per_pass, 1)}
 
 
+def bench_fakequant(args, hg, w, cfg, mask, K, V):
+    """One-pass simulated quantization, out of place: every image row of K and
+    V is read once and written once (protected rows copied)."""
+    import torch
+    Ko, Vo = torch.empty_like(K), torch.empty_like(V)
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo, stream=stream)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for e0, e1 in ev:
+        e0.record(stream)
+        hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo, stream=stream)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    nbytes = 2 * (2 * w.L * w.B * w.H * w.img_len * w.D * 2)
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "fake-quantize (one-pass simulated quantization) HBM GB/s",
+        "value": round(nbytes * args.steps / elapsed / 1e9, 2), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded N(0,1) BF16 KV with outlier key channels; no model weights)",
+        "config": {"workload": w.name, "bits": w.bits, "base": w.base, "keys_only": w.keys_only},
+        "image_tokens_per_s": round(w.B * w.img_len / (ms * 1e-3), 1),
+        "roofline": {"bound": "hbm", "kernel": "fake_quantize_kernel", "achieved": round(gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                     "bytes_per_launch": nbytes, "ms": round(ms, 4)},
+    }), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -136,6 +174,8 @@ def main():
     ab = algorithmic_bytes(w, sizes)
 
     K, V = synthkv.gen_kv(w, device="cuda")
+    if args.op == "fakequant":
+        return bench_fakequant(args, hg, w, cfg, mask, K, V)
     packed = hg.alloc_packed(cfg, mask)
     Ko = torch.empty_like(K)
     Vo = torch.empty_like(V)

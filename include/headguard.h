@@ -136,6 +136,17 @@ int hg_dequantize(const hg_config* cfg, const uint8_t* protect_mask, const hg_pa
 int hg_select_heads(const double* g, const double* o, int32_t L, int32_t Hq, int32_t Hkv,
                     int32_t K, uint8_t* mask_out);
 
+/* Simulated quantization in one pass (§4 Quantization setup: low-precision
+ * entries are rounded to the base's levels and reconstructed as floating-point
+ * values): writes to the image rows of K_out, V_out exactly what hg_quantize
+ * followed by hg_dequantize would, without packed buffers.  K_out may be K
+ * (in place) and V_out may be V; otherwise they must not overlap them.  Kept
+ * rows are copied (left alone in place); text rows are not written.  Device
+ * pointers 16-byte aligned. */
+int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
+                     const uint8_t* protect_mask, uint16_t* K_out, uint16_t* V_out,
+                     hipStream_t stream);
+
 /* Static name of a status code. */
 const char* hg_status_string(int status);
 

@@ -62,7 +62,9 @@ def _load():
     lib.hg_quantize.argtypes = [C.POINTER(hg_config), P, P, P, C.POINTER(hg_packed), P]
     lib.hg_dequantize.argtypes = [C.POINTER(hg_config), P, C.POINTER(hg_packed), P, P, P]
     lib.hg_select_heads.argtypes = [P, P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, P]
-    for f in ("hg_packed_sizes", "hg_quantize", "hg_dequantize", "hg_select_heads"):
+    lib.hg_fake_quantize.argtypes = [C.POINTER(hg_config), P, P, P, P, P, P]
+    for f in ("hg_packed_sizes", "hg_quantize", "hg_dequantize", "hg_select_heads",
+              "hg_fake_quantize"):
         getattr(lib, f).restype = C.c_int
     lib.hg_status_string.argtypes = [C.c_int]
     lib.hg_status_string.restype = C.c_char_p
@@ -148,6 +150,15 @@ def hg_dequantize(cfg: hg_config, protect_mask, packed: Dict[str, torch.Tensor],
     pk = _packed_struct(packed)
     _check(_lib.hg_dequantize(C.byref(cfg), m.ctypes.data_as(C.c_void_p), C.byref(pk),
                               _ptr(K_out), _ptr(V_out), _stream(stream)))
+
+
+def hg_fake_quantize(cfg: hg_config, K: torch.Tensor, V: torch.Tensor, protect_mask,
+                     K_out: torch.Tensor, V_out: torch.Tensor, stream=None) -> None:
+    """Enqueue the one-pass quantize-and-reconstruct of the image rows of K, V
+    into K_out, V_out (which may be K, V themselves)."""
+    m = _mask_arg(protect_mask)
+    _check(_lib.hg_fake_quantize(C.byref(cfg), _ptr(K), _ptr(V), m.ctypes.data_as(C.c_void_p),
+                                 _ptr(K_out), _ptr(V_out), _stream(stream)))
 
 
 # ------------------------------------------------------------ allocation helper

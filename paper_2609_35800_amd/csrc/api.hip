@@ -246,6 +246,40 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
   return ok();
 }
 
+int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, const uint8_t* mask,
+                     uint16_t* K_out, uint16_t* V_out, hipStream_t stream) {
+  int s = check_config(cfg, mask);
+  if (s) return s;
+  const uint64_t cache_bytes = (uint64_t)cfg->L * cfg->B * cfg->H * cfg->T * cfg->D * 2;
+  const uint64_t need = cfg->img_len > 0 ? cache_bytes : 0;
+  if (need && (!K || !V || !K_out || !V_out)) return fail(HG_ERR_NULL, "K, V, K_out and V_out are required");
+  for (int X = 0; X < 2; ++X) {
+    const uintptr_t a = (uintptr_t)(X ? V : K), b = (uintptr_t)(X ? V_out : K_out);
+    if (need && a != b && a < b + need && b < a + need)
+      return fail(HG_ERR_POINTER, "%s_out partially overlaps %s (must be the same buffer or disjoint)",
+                  X ? "V" : "K", X ? "V" : "K");
+  }
+  const Buf bufs[] = {{K, need, 16, "K"}, {V, need, 16, "V"}, {K_out, need, 16, "K_out"}, {V_out, need, 16, "V_out"}};
+  s = check_device();
+  if (s) return s;
+  s = check_buffers(bufs, 4);
+  if (s) return s;
+  if (cfg->img_len == 0) return ok();
+  hg::Params p;
+  fill_params(p, cfg, mask);
+  p.cache[0] = K;
+  p.cache[1] = V;
+  p.out[0] = K_out;
+  p.out[1] = V_out;
+  const uint64_t blocks_k = (uint64_t)cfg->L * cfg->B * cfg->H * (uint64_t)p.tiles;
+  if (2 * blocks_k > 0x7FFFFFFFull)
+    return fail(HG_ERR_SHAPE, "grid of %llu workgroups too large", (unsigned long long)(2 * blocks_k));
+  p.blocks_k = (uint32_t)blocks_k;
+  hipError_t e = hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream);
+  if (e != hipSuccess) return fail(HG_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 int hg_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, const uint8_t* mask,
                 const hg_packed* out, hipStream_t stream) {
   if (!K || !V) {

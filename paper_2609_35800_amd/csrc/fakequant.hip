@@ -1,0 +1,246 @@
+// Fused simulated quantization for gfx950: the image rows of every
+// unprotected head are quantized by the base and reconstructed to BF16 in
+// registers, in one pass over the cache (HeadGuard §4, Quantization setup:
+// entries assigned low precision are rounded to the base quantizer's levels and
+// reconstructed as floating-point values).  The result is bit-identical to
+// hg_quantize followed by hg_dequantize, without the packed buffers: 4 bytes
+// of traffic per element instead of about 4.6.  Protected rows are copied
+// (or left alone when the output is the input); text rows are not written.
+//
+// Work decomposition as in quantize.hip (a workgroup per slice and 128 image
+// tokens, 32 per wavefront).  Per-token groups are computed with a lane quad
+// per token and the reconstructed rows are transposed through LDS so that
+// every store instruction writes whole consecutive token rows; KIVI keys are
+// computed and stored in the whole-row load layout directly.
+
+#include "hg_device.h"
+#include "hg_kernels.h"
+
+namespace hg {
+
+// LDS slot of (token, chunk) in a 16-token stage of D/8 16-byte chunks per
+// token, XOR-swizzled by token so that the quad-per-token writes spread over
+// the banks.
+template <int D>
+__device__ __forceinline__ constexpr int fq_slot(int t, int c) {
+  return t * (D / 8) + (c ^ (D == 128 ? (t & 3) : ((t >> 1) & 1)));
+}
+
+template <int D, int BITS, bool ROTATE>
+__device__ __forceinline__ void fake_tokens(const uint16_t* __restrict__ rows, uint16_t* __restrict__ out,
+                                            int t_first, int n, int lane, u32x4* __restrict__ stage) {
+  constexpr int E = D / 4;             // elements per lane (quad per token)
+  constexpr int NV = E / 8;            // 16-byte chunks per lane
+  constexpr int CPT = D / 8;           // chunks per token row
+  constexpr int RPL = 64 / CPT;        // token rows per store instruction
+  constexpr int NSP = 16 / RPL;        // store instructions per 16-token pass
+  constexpr int LEVELS = (1 << BITS) - 1;
+  const int j = lane & 3;
+  const int q = lane >> 2;
+
+  // Tokens past the span's end load the last token (never stored).
+  u32x4 raw[2][NV];
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int t = min(t_first + pass * 16 + q, n - 1);
+    const u32x4* src = (const u32x4*)(rows + (size_t)t * D + j * E);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) raw[pass][k] = src[k];
+  }
+
+#pragma unroll 1
+  for (int pass = 0; pass < 2; ++pass) {
+    float x[E];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      x[8 * k + 0] = bf16_lo(raw[pass][k].x);
+      x[8 * k + 1] = bf16_hi(raw[pass][k].x);
+      x[8 * k + 2] = bf16_lo(raw[pass][k].y);
+      x[8 * k + 3] = bf16_hi(raw[pass][k].y);
+      x[8 * k + 4] = bf16_lo(raw[pass][k].z);
+      x[8 * k + 5] = bf16_hi(raw[pass][k].z);
+      x[8 * k + 6] = bf16_lo(raw[pass][k].w);
+      x[8 * k + 7] = bf16_hi(raw[pass][k].w);
+    }
+    if constexpr (ROTATE) fwht_quad<E>(x, j, fwht_scale<D>());
+
+    float mn = x[0], mx = x[0];
+#pragma unroll
+    for (int e = 1; e < E; ++e) {
+      mn = fminf(mn, x[e]);
+      mx = fmaxf(mx, x[e]);
+    }
+    mn = quad_min(mn);
+    mx = quad_max(mx);
+    const GroupScale g = group_scale<LEVELS>(mn, mx);
+    const float S = bf16_as_float(g.meta & 0xFFFFu);
+
+    // Level of each code, q*S + m (q*S exact, one rounding), then the inverse
+    // rotation for AKVQ keys, then BF16.
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const uint32_t code = code_bits(x[e], g) - kMagicBits;
+      x[e] = __builtin_fmaf((float)code, S, g.m);
+    }
+    if constexpr (ROTATE) fwht_quad<E>(x, j, fwht_scale<D>());
+
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const u32x4 v = {pack_bf16x2_hw(x[8 * k + 0], x[8 * k + 1]), pack_bf16x2_hw(x[8 * k + 2], x[8 * k + 3]),
+                       pack_bf16x2_hw(x[8 * k + 4], x[8 * k + 5]), pack_bf16x2_hw(x[8 * k + 6], x[8 * k + 7])};
+      stage[fq_slot<D>(q, j * NV + k)] = v;
+    }
+    // LDS operations of one wavefront execute in order; the fences keep the
+    // compiler from moving the accesses across each other.
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const int c = lane % CPT;
+    const int r = lane / CPT;
+#pragma unroll
+    for (int k = 0; k < NSP; ++k) {
+      const int tl = r + RPL * k;
+      const int t = t_first + pass * 16 + tl;
+      const u32x4 v = stage[fq_slot<D>(tl, c)];
+      if (t < n) store_nt((u32x4*)(out + (size_t)t * D + 8 * c), v);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  }
+}
+
+template <int D, int BITS>
+__device__ __forceinline__ void fake_kivi_keys(const uint16_t* __restrict__ rows, uint16_t* __restrict__ out,
+                                               int g_first, int n, int lane) {
+  constexpr int LPR = D / 8;             // lanes per token row (8 channels each)
+  constexpr int RPL = 64 / LPR;          // token rows per load
+  constexpr int NL = kWaveTokens / RPL;  // loads per lane
+  constexpr int LEVELS = (1 << BITS) - 1;
+  const int c8 = lane % LPR;
+  const int r = lane / LPR;
+
+  u32x4 raw[NL];
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    const int t = min(g_first + r + RPL * k, n - 1);  // past-the-end rows: excluded below
+    raw[k] = *(const u32x4*)(rows + (size_t)t * D + 8 * c8);
+  }
+  float x[NL][8];
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    x[k][0] = bf16_lo(raw[k].x); x[k][1] = bf16_hi(raw[k].x);
+    x[k][2] = bf16_lo(raw[k].y); x[k][3] = bf16_hi(raw[k].y);
+    x[k][4] = bf16_lo(raw[k].z); x[k][5] = bf16_hi(raw[k].z);
+    x[k][6] = bf16_lo(raw[k].w); x[k][7] = bf16_hi(raw[k].w);
+  }
+  GroupScale g[8];
+  float S[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    float mn = __builtin_inff(), mx = -__builtin_inff();
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      const bool ok = g_first + r + RPL * k < n;
+      mn = fminf(mn, ok ? x[k][e] : __builtin_inff());
+      mx = fmaxf(mx, ok ? x[k][e] : -__builtin_inff());
+    }
+#pragma unroll
+    for (int off = LPR; off < 64; off *= 2) {
+      mn = fminf(mn, __shfl_xor(mn, off));
+      mx = fmaxf(mx, __shfl_xor(mx, off));
+    }
+    g[e] = group_scale<LEVELS>(mn, mx);
+    S[e] = bf16_as_float(g[e].meta & 0xFFFFu);
+  }
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    const int t = g_first + r + RPL * k;
+    float y[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      y[e] = __builtin_fmaf((float)(code_bits(x[k][e], g[e]) - kMagicBits), S[e], g[e].m);
+    const u32x4 v = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
+                     pack_bf16x2_hw(y[6], y[7])};
+    if (t < n) store_nt((u32x4*)(out + (size_t)t * D + 8 * c8), v);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void fake_copy(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
+                                          int t_first, int n, int lane) {
+  constexpr int VPT = D / 8;
+  const int nvec = min(kWaveTokens, n - t_first) * VPT;
+  const u32x4* s = (const u32x4*)(src + (size_t)t_first * D);
+  u32x4* d = (u32x4*)(dst + (size_t)t_first * D);
+  constexpr int kMax = kWaveTokens * VPT / 64;
+  u32x4 v[kMax];
+#pragma unroll
+  for (int k = 0; k < kMax; ++k) v[k] = s[min(lane + 64 * k, nvec - 1)];
+#pragma unroll
+  for (int k = 0; k < kMax; ++k) {
+    const int i = lane + 64 * k;
+    if (i < nvec) store_nt(d + i, v[k]);
+  }
+}
+
+template <int BASE, int D, int BITS>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWaves)))
+void fake_quantize_kernel(const Params p) {
+  const Slice sl = decode_block(p, blockIdx.x);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int t_first = sl.tile * kBlockTokens + wave * kWaveTokens;
+  if (t_first >= p.n) return;
+
+  const size_t base = ((size_t)sl.s * p.T + p.s0) * D;
+  const uint16_t* rows = p.cache[sl.X] + base;
+  uint16_t* out = p.out[sl.X] + base;
+  if (sl.kept) {
+    if (out != rows) fake_copy<D>(rows, out, t_first, p.n, lane);
+    return;
+  }
+  if (BASE == HG_BASE_KIVI && sl.X == 0) {
+    fake_kivi_keys<D, BITS>(rows, out, t_first, p.n, lane);
+  } else {
+    __shared__ u32x4 stage_all[kThreads / 64][16 * (D / 8)];
+    if (BASE == HG_BASE_AKVQ && sl.X == 0)
+      fake_tokens<D, BITS, true>(rows, out, t_first, p.n, lane, stage_all[wave]);
+    else
+      fake_tokens<D, BITS, false>(rows, out, t_first, p.n, lane, stage_all[wave]);
+  }
+}
+
+template <int BASE, int D, int BITS>
+static hipError_t launch_f(const Params& p, uint32_t blocks, hipStream_t stream) {
+  hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS>), dim3(blocks), dim3(kThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+template <int BASE, int D>
+static hipError_t launch_f_bits(const Params& p, int bits, uint32_t blocks, hipStream_t stream) {
+  switch (bits) {
+    case 2: return launch_f<BASE, D, 2>(p, blocks, stream);
+    case 3: return launch_f<BASE, D, 3>(p, blocks, stream);
+    case 4: return launch_f<BASE, D, 4>(p, blocks, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int BASE>
+static hipError_t launch_f_dim(const Params& p, int D, int bits, uint32_t blocks, hipStream_t stream) {
+  switch (D) {
+    case 64: return launch_f_bits<BASE, 64>(p, bits, blocks, stream);
+    case 128: return launch_f_bits<BASE, 128>(p, bits, blocks, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
+                                hipStream_t stream) {
+  switch (base) {
+    case HG_BASE_MINMAX: return launch_f_dim<HG_BASE_MINMAX>(p, D, bits, blocks, stream);
+    case HG_BASE_KIVI: return launch_f_dim<HG_BASE_KIVI>(p, D, bits, blocks, stream);
+    case HG_BASE_AKVQ: return launch_f_dim<HG_BASE_AKVQ>(p, D, bits, blocks, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace hg

@@ -30,7 +30,8 @@ struct Route {
 // K tiles, the rest V tiles.  Each block takes one (tensor, l, b, h) slice and
 // kBlockTokens consecutive image tokens of it.
 struct Params {
-  const uint16_t* cache[2];  // quantize: K, V input; dequantize: K_out, V_out
+  const uint16_t* cache[2];  // quantize, fake quantize: K, V input; dequantize: K_out, V_out
+  uint16_t* out[2];          // fake quantize: K_out, V_out (may equal the input)
   uint8_t* codes[2];
   uint32_t* meta[2];
   uint16_t* side[2];
@@ -48,6 +49,8 @@ hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t 
                            hipStream_t stream);
 hipError_t launch_dequantize(const Params& p, int base, int D, int bits, uint32_t blocks,
                              hipStream_t stream);
+hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
+                                hipStream_t stream);
 
 // Routing of one (tensor, slice): whether it is kept in BF16 and its slot in
 // the packed buffers (rank among kept heads if kept, else among quantized

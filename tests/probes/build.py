@@ -8,9 +8,12 @@ LIB = os.path.join(HERE, "libhg_probes.so")
 
 
 def build() -> str:
-    import sys
-    sys.path.insert(0, ROOT)
-    from paper_2609_35800_amd.build import FLAGS
+    import importlib.util
+    spec = importlib.util.spec_from_file_location(
+        "hg_build", os.path.join(ROOT, "paper_2609_35800_amd", "build.py"))
+    hg_build = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(hg_build)  # not the package: its __init__ loads the library
+    FLAGS = hg_build.FLAGS
     tmp = LIB + ".tmp"
     subprocess.check_call([os.environ.get("HIPCC", "/opt/rocm/bin/hipcc"), *FLAGS, "-o", tmp,
                            os.path.join(HERE, "hg_probes.hip")])

@@ -1,0 +1,109 @@
+"""GPU parity of the one-pass simulated quantization (hg_fake_quantize, §4
+Quantization setup) against its definition, the oracle's dequantize of its
+quantize: image rows bit-exact, protected rows bit-identical, text rows
+untouched, in place and out of place; at full size, equality with the
+library's own quantize then dequantize over the whole cache plus sampled
+slices against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synthkv
+from hgtest import bf16_ulp_diff
+from test_gpu_parity import _special_values, small
+
+pytestmark = pytest.mark.gpu
+SENTINEL = 0x7FBF
+
+
+def oracle_roundtrip(w, Kb, Vb, mask, init_K, init_V):
+    cfg = oracle.make_config(**w.config_fields())
+    packed = oracle.quantize(cfg, Kb, Vb, mask, threads=8)
+    Ko, Vo = init_K.copy(), init_V.copy()
+    oracle.dequantize(cfg, mask, packed, Ko, Vo, threads=8)
+    return Ko, Vo
+
+
+def run_fake(w, K, V, mask, inplace):
+    import paper_2609_35800_amd as hg
+    cfg = hg.make_config(**w.config_fields())
+    Kg, Vg = K.cuda().contiguous(), V.cuda().contiguous()
+    if inplace:
+        hg.hg_fake_quantize(cfg, Kg, Vg, mask, Kg, Vg)
+        Ko, Vo = Kg, Vg
+    else:
+        Ko = torch.full(Kg.shape, SENTINEL, dtype=torch.int16, device="cuda").view(torch.bfloat16)
+        Vo = torch.full(Vg.shape, SENTINEL, dtype=torch.int16, device="cuda").view(torch.bfloat16)
+        hg.hg_fake_quantize(cfg, Kg, Vg, mask, Ko, Vo)
+    torch.cuda.synchronize()
+    return synthkv.bf16_bits(Ko), synthkv.bf16_bits(Vo)
+
+
+def check(w, K, V, mask, inplace):
+    Kb, Vb = synthkv.bf16_bits(K), synthkv.bf16_bits(V)
+    gK, gV = run_fake(w, K, V, mask, inplace)
+    initK = Kb if inplace else np.full_like(Kb, SENTINEL)
+    initV = Vb if inplace else np.full_like(Vb, SENTINEL)
+    oK, oV = oracle_roundtrip(w, Kb, Vb, mask, initK, initV)
+    assert bf16_ulp_diff(gK, oK) <= 1 and bf16_ulp_diff(gV, oV) <= 1
+    assert np.array_equal(gK, oK), (w.name, int(np.count_nonzero(gK != oK)))
+    assert np.array_equal(gV, oV), (w.name, int(np.count_nonzero(gV != oV)))
+
+
+CASES = [small(b, D, bits, ko) for b in ("minmax", "kivi", "akvq") for D in (64, 128)
+         for bits in (2, 3, 4) for ko in (0, 1)]
+
+
+@pytest.mark.parametrize("inplace", [False, True])
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def test_small(w, inplace):
+    K, V = synthkv.gen_kv(w)
+    check(w, K, V, synthkv.protect_mask(w), inplace)
+
+
+@pytest.mark.parametrize("base", ["minmax", "kivi", "akvq"])
+@pytest.mark.parametrize("img_len", [1, 31, 33, 129, 257])
+def test_ragged(base, img_len):
+    w = small(base, img_len=img_len, img_start=3, text=2, L=1, B=2, H=2, n_protected=1)
+    K, V = synthkv.gen_kv(w)
+    check(w, K, V, synthkv.protect_mask(w), inplace=False)
+
+
+@pytest.mark.parametrize("base", ["minmax", "kivi", "akvq"])
+def test_special_values(base):
+    w = small(base, bits=2, img_len=96, n_protected=0)
+    K, V = synthkv.gen_kv(w)
+    K, V = _special_values(w, K, V)
+    check(w, K, V, np.zeros(w.L * w.H, np.uint8), inplace=True)
+
+
+@pytest.mark.parametrize("name", ["qwen2.5-vl-7b", "llava-next-7b", "internvl-8b"])
+def test_full_size_equals_quantize_then_dequantize(name):
+    import paper_2609_35800_amd as hg
+    w = synthkv.WORKLOADS[name]
+    mask = synthkv.protect_mask(w)
+    cfg = hg.make_config(**w.config_fields())
+    K, V = synthkv.gen_kv(w, device="cuda")
+    packed = hg.alloc_packed(cfg, mask)
+    Kr, Vr = K.clone(), V.clone()
+    hg.hg_quantize(cfg, K, V, mask, packed)
+    hg.hg_dequantize(cfg, mask, packed, Kr, Vr)
+    del packed
+    hg.hg_fake_quantize(cfg, K, V, mask, K, V)  # in place
+    torch.cuda.synchronize()
+    assert torch.equal(K.view(torch.int16), Kr.view(torch.int16))
+    assert torch.equal(V.view(torch.int16), Vr.view(torch.int16))
+    # sampled slices against the oracle (the inputs are regenerated)
+    K0, V0 = synthkv.gen_kv(w, device="cuda")
+    ocfg = oracle.make_config(**w.config_fields())
+    rng = np.random.default_rng(5)
+    s0, n = w.img_start, w.img_len
+    for _ in range(8):
+        l, b, h = int(rng.integers(w.L)), int(rng.integers(w.B)), int(rng.integers(w.H))
+        for X, (src, got) in enumerate(((K0, K), (V0, V))):
+            rows = synthkv.bf16_bits(src[l, b, h, s0:s0 + n])
+            prot, _ = oracle.route(ocfg, mask, X, l, h)
+            want = rows if prot else oracle.dequantize_slice(ocfg, X, *oracle.quantize_slice(ocfg, X, rows))
+            assert np.array_equal(synthkv.bf16_bits(got[l, b, h, s0:s0 + n]), want)
+    torch.cuda.empty_cache()
