@@ -69,11 +69,13 @@ def lib():
                                 C.POINTER(C.c_int), C.POINTER(C.c_int)]
         L.hgo_sizes.argtypes = [C.POINTER(Config), P, C.POINTER(Sizes)]
         L.hgo_quantize_slice.argtypes = [C.POINTER(Config), C.c_int, P, P, P]
+        L.hgo_quantize_slice_seq.argtypes = [C.POINTER(Config), C.c_int, P, P, P]
         L.hgo_dequantize_slice.argtypes = [C.POINTER(Config), C.c_int, P, P, P]
         L.hgo_quantize.argtypes = [C.POINTER(Config), P, P, P, P, P, P, P, P, P, C.c_int]
         L.hgo_dequantize.argtypes = [C.POINTER(Config), P, P, P, P, P, P, P, P, P, C.c_int]
         L.hgo_select_heads.argtypes = [P, P, C.c_int, C.c_int, C.c_int, C.c_int, P]
-        for f in ("hgo_route", "hgo_sizes", "hgo_quantize_slice", "hgo_dequantize_slice",
+        for f in ("hgo_route", "hgo_sizes", "hgo_quantize_slice", "hgo_quantize_slice_seq",
+                  "hgo_dequantize_slice",
                   "hgo_quantize", "hgo_dequantize", "hgo_select_heads"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -157,17 +159,33 @@ def sizes(cfg: Config, mask: np.ndarray) -> Dict[str, int]:
     return {n: getattr(out, n) for n, _ in Sizes._fields_}
 
 
-def quantize_slice(cfg: Config, X: int, rows: np.ndarray):
-    """Codes (uint8 [n, D*bits/8]) and meta (uint32) of one unprotected slice."""
-    rows = np.ascontiguousarray(rows, dtype=np.uint16)
+def _slice_outputs(cfg: Config, X: int):
     n, D = cfg.img_len, cfg.D
     codes = np.zeros((n, D * cfg.bits // 8), dtype=np.uint8)
     if cfg.base == 1 and X == 0:
-        meta = np.zeros((-(-n // cfg.kivi_group), D), dtype=np.uint32)
+        ng = (1 if n > 0 else 0) if cfg.kivi_group == 0 else -(-n // cfg.kivi_group)
+        meta = np.zeros((ng, D), dtype=np.uint32)
     else:
         meta = np.zeros(n, dtype=np.uint32)
+    return codes, meta
+
+
+def quantize_slice(cfg: Config, X: int, rows: np.ndarray):
+    """Codes (uint8 [n, D*bits/8]) and meta (uint32) of one unprotected slice,
+    from its n image rows."""
+    rows = np.ascontiguousarray(rows, dtype=np.uint16)
+    codes, meta = _slice_outputs(cfg, X)
     if lib().hgo_quantize_slice(C.byref(cfg), X, _ptr(rows), _ptr(codes), _ptr(meta)):
         raise ValueError("hgo_quantize_slice failed")
+    return codes, meta
+
+
+def quantize_slice_seq(cfg: Config, X: int, slice_rows: np.ndarray):
+    """The same from the whole slice [T, D] (text rows included)."""
+    slice_rows = np.ascontiguousarray(slice_rows, dtype=np.uint16)
+    codes, meta = _slice_outputs(cfg, X)
+    if lib().hgo_quantize_slice_seq(C.byref(cfg), X, _ptr(slice_rows), _ptr(codes), _ptr(meta)):
+        raise ValueError("hgo_quantize_slice_seq failed")
     return codes, meta
 
 

@@ -145,7 +145,7 @@ static int cfg_ok(const hgo_config* c) {
   if (c->bits < 1 || c->bits > 8) return 0;
   if ((c->D * c->bits) % 8 != 0) return 0;
   if (c->base < HGO_MINMAX || c->base > HGO_AKVQ) return 0;
-  if (c->base == HGO_KIVI && c->kivi_group <= 0) return 0;
+  if (c->base == HGO_KIVI && c->kivi_group < 0) return 0;
   if (c->base == HGO_AKVQ && (c->D & (c->D - 1)) != 0) return 0;
   return 1;
 }
@@ -173,9 +173,15 @@ int hgo_route(const hgo_config* c, const uint8_t* mask, int X, int l, int h,
 
 static int kivi_keys(const hgo_config* c, int X) { return c->base == HGO_KIVI && X == 0; }
 
+/* KIVI-style keys: kivi_group > 0 tiles the image span into groups of that
+ * many tokens; kivi_group == 0 is one group per slice whose range covers the
+ * whole supplied sequence, text included (§4 Quantization setup). */
+static int kivi_whole(const hgo_config* c) { return c->kivi_group == 0; }
+
 static uint64_t meta_words_per_slice(const hgo_config* c, int X) {
   if (kivi_keys(c, X)) {
-    uint64_t ng = ((uint64_t)c->img_len + c->kivi_group - 1) / c->kivi_group;
+    uint64_t ng = kivi_whole(c) ? (c->img_len > 0 ? 1 : 0)
+                                : ((uint64_t)c->img_len + c->kivi_group - 1) / c->kivi_group;
     return ng * (uint64_t)c->D;
   }
   return (uint64_t)c->img_len;
@@ -225,6 +231,7 @@ static unsigned get_code(const uint8_t* row, int bits, int i) {
 int hgo_quantize_slice(const hgo_config* c, int X, const uint16_t* rows,
                        uint8_t* codes, uint32_t* meta) {
   if (!cfg_ok(c) || X < 0 || X > 1) return -1;
+  if (kivi_keys(c, X) && kivi_whole(c)) return -1; /* needs the whole slice */
   int n = c->img_len, D = c->D, b = c->bits;
   size_t row_bytes = (size_t)D * b / 8;
   memset(codes, 0, (size_t)n * row_bytes);
@@ -259,6 +266,30 @@ int hgo_quantize_slice(const hgo_config* c, int X, const uint16_t* rows,
   return 0;
 }
 
+int hgo_quantize_slice_seq(const hgo_config* c, int X, const uint16_t* slice,
+                           uint8_t* codes, uint32_t* meta) {
+  if (!cfg_ok(c) || X < 0 || X > 1) return -1;
+  if (!(kivi_keys(c, X) && kivi_whole(c)))
+    return hgo_quantize_slice(c, X, slice + (size_t)c->img_start * c->D, codes, meta);
+  /* Keys per channel, one range over all T tokens of the slice (text
+   * included); only the image tokens' codes are kept. */
+  int T = c->T, n = c->img_len, D = c->D, b = c->bits, s0 = c->img_start;
+  size_t row_bytes = (size_t)D * b / 8;
+  memset(codes, 0, (size_t)n * row_bytes);
+  if (n == 0) return 0;
+  float* v = (float*)malloc(sizeof(float) * (size_t)T);
+  uint8_t* q = (uint8_t*)malloc((size_t)T);
+  if (!v || !q) { free(v); free(q); return -1; }
+  for (int d = 0; d < D; ++d) {
+    for (int t = 0; t < T; ++t) v[t] = hgo_bf16_to_f32(slice[(size_t)t * D + d]);
+    meta[d] = hgo_quantize_group(v, T, 1, b, q, 1);
+    for (int t = 0; t < n; ++t) put_code(codes + (size_t)t * row_bytes, b, d, q[s0 + t]);
+  }
+  free(v);
+  free(q);
+  return 0;
+}
+
 int hgo_dequantize_slice(const hgo_config* c, int X, const uint8_t* codes,
                          const uint32_t* meta, uint16_t* rows_out) {
   if (!cfg_ok(c) || X < 0 || X > 1) return -1;
@@ -269,7 +300,8 @@ int hgo_dequantize_slice(const hgo_config* c, int X, const uint8_t* codes,
   for (int t = 0; t < n; ++t) {
     const uint8_t* row = codes + (size_t)t * row_bytes;
     for (int d = 0; d < D; ++d) {
-      uint32_t w = kivi_keys(c, X) ? meta[(size_t)(t / c->kivi_group) * D + d] : meta[t];
+      uint32_t w = !kivi_keys(c, X) ? meta[t]
+                   : meta[(size_t)(kivi_whole(c) ? 0 : t / c->kivi_group) * D + d];
       y[d] = hgo_level(w, get_code(row, b, d));
     }
     /* AKVQ-style keys come back to the original basis: H is symmetric and
@@ -310,15 +342,16 @@ static void* run_slices(void* arg) {
     int h = (int)(r % c->H);
     int prot, slot;
     if (hgo_route(c, j->mask, X, l, h, &prot, &slot) != 0) { j->status = -1; return NULL; }
-    size_t cache_off = ((((size_t)l * c->B + b) * c->H + h) * c->T + c->img_start) * D;
+    size_t slice_off = (((size_t)l * c->B + b) * c->H + h) * c->T * D;
+    size_t cache_off = slice_off + (size_t)c->img_start * D;
     size_t slab = (size_t)slot * c->B + b; /* [slot][B] */
     uint16_t* side = j->side[X] ? j->side[X] + slab * n * D : NULL;
     if (!j->dequant) {
       const uint16_t* rows = j->in[X] + cache_off;
       if (prot) {
         memcpy(side, rows, (size_t)n * D * 2);
-      } else if (hgo_quantize_slice(c, X, rows, j->codes[X] + slab * n * row_bytes,
-                                    j->meta[X] + slab * meta_words_per_slice(c, X)) != 0) {
+      } else if (hgo_quantize_slice_seq(c, X, j->in[X] + slice_off, j->codes[X] + slab * n * row_bytes,
+                                        j->meta[X] + slab * meta_words_per_slice(c, X)) != 0) {
         j->status = -1;
         return NULL;
       }

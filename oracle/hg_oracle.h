@@ -18,6 +18,8 @@
  *   codes_X       [slot][B][n][D*bits/8]   LSB-first bitstream per token row
  *   meta_X        u32 [slot][B][n]           per-token groups
  *                 u32 [slot][B][ceil(n/G)][D] KIVI-style keys, G = kivi_group
+ *                 u32 [slot][B][1][D]         KIVI-style keys, kivi_group = 0
+ *                                             (range over the whole sequence)
  *                 each word = bf16(scale) | bf16(min) << 16
  *   side_X        BF16 bits [p][B][n][D]     protected heads' image rows
  * where n = img_len, slot = rank of (l,h) among the heads whose tensor X is
@@ -79,6 +81,11 @@ int hgo_sizes(const hgo_config* c, const uint8_t* mask, hgo_sizes_t* out);
  * KIVI-style keys). */
 int hgo_quantize_slice(const hgo_config* c, int X, const uint16_t* rows,
                        uint8_t* codes, uint32_t* meta);
+/* The same from the whole slice (T*D BF16, text rows included), as needed by
+ * KIVI-style keys with kivi_group == 0: one range per channel over all T
+ * tokens, meta D words, codes for the n image tokens only. */
+int hgo_quantize_slice_seq(const hgo_config* c, int X, const uint16_t* slice,
+                           uint8_t* codes, uint32_t* meta);
 int hgo_dequantize_slice(const hgo_config* c, int X, const uint8_t* codes,
                          const uint32_t* meta, uint16_t* rows_out);
 

@@ -214,3 +214,53 @@ def test_empty_span():
     cfg, mask, Kb, Vb, packed, Ko, Vo = run_oracle(w)
     assert all(v.size == 0 for v in packed.values())
     assert np.all(Ko == 0x7FBF)
+
+
+# ------------------------------------------------- KIVI-style keys, whole sequence
+
+def test_kivi_whole_sequence_keys():
+    """kivi_group = 0 (§4: KIVI-style key ranges recomputed over the supplied
+    sequence, text included; text KV stays BF16): per channel, the metadata is
+    the per-token routine over the channel's T values; image codes are that
+    group's codes at the image positions."""
+    w = small_workload("kivi", kivi_group=0, bits=2, img_start=5, img_len=37, T=50)
+    cfg = oracle.make_config(**w.config_fields())
+    K, _ = synthkv.gen_kv(w)
+    sl = _bits(K)[1, 0, 2]  # whole slice [T, D]
+    codes, meta = oracle.quantize_slice_seq(cfg, 0, sl)
+    assert meta.shape == (1, w.D)
+    x = _f32(sl)
+    for d in range(w.D):
+        q, mw = oracle.quantize_group(x[:, d].copy(), w.bits)
+        assert meta[0, d] == mw
+        for t in range(w.img_len):
+            assert _unpack(codes[t], w.bits, w.D)[d] == q[w.img_start + t]
+    # a text outlier widens the range and so changes the image tokens' metadata
+    sl2 = sl.copy()
+    sl2[0, 3] = 0x4700  # 32768.0 in a text row
+    _, meta2 = oracle.quantize_slice_seq(cfg, 0, sl2)
+    assert meta2[0, 3] != meta[0, 3] and np.array_equal(np.delete(meta2, 3), np.delete(meta, 3))
+    # the image-rows entry point cannot see the text and refuses this mode
+    with pytest.raises(ValueError):
+        oracle.quantize_slice(cfg, 0, sl[w.img_start:w.img_start + w.img_len])
+
+
+def test_kivi_whole_sequence_cache_round_trip():
+    w = small_workload("kivi", kivi_group=0, bits=3)
+    cfg, mask, Kb, Vb, packed, Ko, Vo = run_oracle(w)
+    sizes = oracle.sizes(cfg, mask)
+    assert sizes["meta_k"] == sizes["n_unprot_k"] * w.B * w.D * 4
+    assert np.all(Ko[:, :, :, :w.img_start] == 0x7FBF)  # text untouched
+    meta = packed["meta_k"].reshape(-1, w.B, 1, w.D)
+    x, xh = _f32(img(Kb, w)), _f32(img(Ko, w))
+    m2 = mask.reshape(w.L, w.H).astype(bool)
+    u = 0
+    for l in range(w.L):
+        for h in range(w.H):
+            if m2[l, h]:
+                continue
+            for b in range(w.B):
+                S = _f32((meta[u, b, 0] & 0xFFFF).astype(np.uint16))
+                err = np.abs(x[l, b, h] - xh[l, b, h])
+                assert np.all(err <= S / 2 + np.abs(xh[l, b, h]) * 2.0 ** -8 + 1e-30)
+            u += 1

@@ -46,7 +46,11 @@ MUTANTS = [
      "v[t] = hgo_bf16_to_f32(rows[(size_t)t * D + d]);"),
     ("pack_msb_first", "if ((q >> k) & 1u) row[pos / 8] |= (uint8_t)(1u << (pos % 8));",
      "if ((q >> k) & 1u) row[pos / 8] |= (uint8_t)(1u << (7 - pos % 8));"),
-    ("span_offset_dropped", "c->T + c->img_start) * D;", "c->T) * D;"),
+    ("span_offset_dropped", "size_t cache_off = slice_off + (size_t)c->img_start * D;",
+     "size_t cache_off = slice_off;"),
+    ("span_offset_dropped_in_quantize",
+     "return hgo_quantize_slice(c, X, slice + (size_t)c->img_start * c->D, codes, meta);",
+     "return hgo_quantize_slice(c, X, slice, codes, meta);"),
     ("akvq_no_inverse_rotation", "if (c->base == HGO_AKVQ && X == 0) hgo_fwht_norm(y, D);", "(void)0;"),
     ("akvq_rotates_values", "if (c->base == HGO_AKVQ && X == 0) hgo_fwht_norm(v, D);",
      "if (c->base == HGO_AKVQ) hgo_fwht_norm(v, D);"),
@@ -55,6 +59,10 @@ MUTANTS = [
     ("negative_zero_min_kept", "if (m16 == 0x8000u) m16 = 0;", ""),
     ("no_scale_floor", "if (s16 != 0 && hgo_bf16_to_f32(s16) < 0x1p-126f) s16 = 0x0080u; /* 2^-126 */", ""),
     ("zero_range_not_special", "if (s16 == 0) {", "if (s16 == 0 && 0) {"),
+    ("kivi_whole_image_only", "for (int t = 0; t < T; ++t) v[t] = hgo_bf16_to_f32(slice[(size_t)t * D + d]);",
+     "for (int t = 0; t < n; ++t) v[t] = hgo_bf16_to_f32(slice[(size_t)(s0 + t) * D + d]);"),
+    ("kivi_whole_codes_unshifted", "put_code(codes + (size_t)t * row_bytes, b, d, q[s0 + t]);",
+     "put_code(codes + (size_t)t * row_bytes, b, d, q[t]);"),
     ("select_difference", "sc[i] = gb[i] + ob[i];", "sc[i] = gb[i] - ob[i];"),
     ("select_interleaved_groups", "int i = l * Hkv + hq / rep;", "int i = l * Hkv + hq % Hkv;"),
     ("select_g_not_standardized", "zscore(gb, n);", ""),
