@@ -36,6 +36,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen2.5-vl-7b")
     ap.add_argument("--bits", type=int, default=None, help="override the workload's bit width")
+    ap.add_argument("--kivi-group", type=int, default=None,
+                    help="override the KIVI key group (0: one range over the whole sequence)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time budget of the oracle sample")
@@ -145,7 +147,8 @@ def bench_fakequant(args, hg, w, cfg, mask, K, V):
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded N(0,1) BF16 KV with outlier key channels; no model weights)",
-        "config": {"workload": w.name, "bits": w.bits, "base": w.base, "keys_only": w.keys_only},
+        "config": {"workload": w.name, "bits": w.bits, "base": w.base, "keys_only": w.keys_only,
+                   **({"kivi_group": w.kivi_group} if w.base == "kivi" else {})},
         "image_tokens_per_s": round(w.B * w.img_len / (ms * 1e-3), 1),
         "roofline": {"bound": "hbm", "kernel": "fake_quantize_kernel", "achieved": round(gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
@@ -168,6 +171,8 @@ def main():
     w = synthkv.WORKLOADS[args.workload]
     if args.bits is not None:
         w = w.with_(bits=args.bits)
+    if args.kivi_group is not None:
+        w = w.with_(kivi_group=args.kivi_group)
     mask = synthkv.protect_mask(w)
     cfg = hg.make_config(**w.config_fields())
     sizes = hg.hg_packed_sizes(cfg, mask)
@@ -238,6 +243,7 @@ def main():
         "config": {"workload": w.name, "L": w.L, "B": w.B, "H_kv": w.H, "T": w.T, "D": w.D,
                    "img_start": w.img_start, "img_len": w.img_len, "bits": w.bits,
                    "base": w.base, "keys_only": w.keys_only, "protected_heads": int(mask.sum()),
+                   **({"kivi_group": w.kivi_group} if w.base == "kivi" else {}),
                    "parallelism": "single GPU"},
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "image_tokens_per_s": round(w.B * w.img_len * args.steps / elapsed, 1),

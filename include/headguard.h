@@ -12,8 +12,11 @@
  *
  * Bases (§2 "KV-cache quantization", §4 "Quantization setup"):
  *   HG_BASE_MINMAX  per-token min-max round-to-nearest for keys and values;
- *   HG_BASE_KIVI    keys per channel over groups of `kivi_group` consecutive
- *                   image tokens, values per token;
+ *   HG_BASE_KIVI    keys per channel over groups of `kivi_group` (32)
+ *                   consecutive image tokens, or with kivi_group = 0 over the
+ *                   whole supplied sequence of T tokens, text included (the
+ *                   paper's KIVI-style harness; text still stays BF16);
+ *                   values per token;
  *   HG_BASE_AKVQ    keys rotated by the normalized Walsh-Hadamard matrix over
  *                   head_dim, then per token; values per token, unrotated.
  *
@@ -35,6 +38,7 @@
  *             [bits*d, bits*d + bits) of the token's row, least significant first
  *   meta_X    u32 [slot][B][n]                 per-token groups
  *             u32 [slot][B][ceil(n/G)][D]      KIVI keys, G = kivi_group
+ *             u32 [slot][B][1][D]              KIVI keys, kivi_group = 0
  *   side_X    BF16 [p][B][n][D]  image rows of protected heads, bit-identical
  * slot = rank of (l, h) in row-major order among the heads whose X is
  * quantized; p = rank among the heads whose X is kept in BF16.  V is kept iff
@@ -72,7 +76,7 @@ enum {
   HG_ERR_SHAPE = 2,     /* L, B, H, T not positive, or L*H > HG_MAX_HEADS      */
   HG_ERR_SPAN = 3,      /* image span outside [0, T]                           */
   HG_ERR_BITS = 4,      /* bits not in {2, 3, 4}                               */
-  HG_ERR_BASE = 5,      /* unknown base, or kivi_group unsupported             */
+  HG_ERR_BASE = 5,      /* unknown base, or kivi_group not 32 or 0             */
   HG_ERR_HEADDIM = 6,   /* D not in {64, 128}                                  */
   HG_ERR_ALIGN = 7,     /* a device pointer is not 16-byte aligned             */
   HG_ERR_MASK = 8,      /* a mask entry is neither 0 nor 1                     */
@@ -92,7 +96,7 @@ typedef struct {
   int32_t bits;                /* 2, 3 or 4                                        */
   int32_t base;                /* hg_base                                          */
   int32_t keys_only;           /* 1: protect K only; 0: protect K and V            */
-  int32_t kivi_group;          /* tokens per KIVI key group (32); ignored otherwise */
+  int32_t kivi_group;          /* KIVI key group: 32 tokens, or 0 = whole sequence */
 } hg_config;
 
 typedef struct {

@@ -46,8 +46,8 @@ int check_config(const hg_config* c, const uint8_t* mask) {
   if (c->bits < 2 || c->bits > 4) return fail(HG_ERR_BITS, "bits %d not in {2, 3, 4}", c->bits);
   if (c->base != HG_BASE_MINMAX && c->base != HG_BASE_KIVI && c->base != HG_BASE_AKVQ)
     return fail(HG_ERR_BASE, "unknown base %d", c->base);
-  if (c->base == HG_BASE_KIVI && c->kivi_group != hg::kWaveTokens)
-    return fail(HG_ERR_BASE, "kivi_group %d unsupported (32)", c->kivi_group);
+  if (c->base == HG_BASE_KIVI && c->kivi_group != hg::kWaveTokens && c->kivi_group != 0)
+    return fail(HG_ERR_BASE, "kivi_group %d unsupported (32, or 0 for the whole sequence)", c->kivi_group);
   if (c->keys_only != 0 && c->keys_only != 1) return fail(HG_ERR_SHAPE, "keys_only must be 0 or 1");
   const int LH = c->L * c->H;
   for (int i = 0; i < LH; ++i)
@@ -70,7 +70,7 @@ Counts counts(const hg_config* c, const uint8_t* mask) {
   k.pv = c->keys_only ? 0 : k.P;
   k.n = (uint64_t)c->img_len;
   k.row = (uint64_t)c->D * c->bits / 8;
-  const uint64_t groups = (k.n + hg::kWaveTokens - 1) / hg::kWaveTokens;
+  const uint64_t groups = c->kivi_group == 0 ? (k.n > 0 ? 1 : 0) : (k.n + hg::kWaveTokens - 1) / hg::kWaveTokens;
   k.meta_k_words = c->base == HG_BASE_KIVI ? groups * c->D : k.n;
   k.meta_v_words = k.n;
   return k;
@@ -135,7 +135,8 @@ void fill_params(hg::Params& p, const hg_config* c, const uint8_t* mask) {
   p.s0 = c->img_start;
   p.n = c->img_len;
   p.keys_only = c->keys_only;
-  p.ngroups = (c->img_len + hg::kWaveTokens - 1) / hg::kWaveTokens;
+  p.kivi_whole = c->base == HG_BASE_KIVI && c->kivi_group == 0;
+  p.ngroups = p.kivi_whole ? 1 : (c->img_len + hg::kWaveTokens - 1) / hg::kWaveTokens;
   p.tiles = (c->img_len + hg::kBlockTokens - 1) / hg::kBlockTokens;
   const int LH = c->L * c->H;
   uint32_t running = 0;
@@ -242,6 +243,7 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
   p.blocks_k = (uint32_t)blocks_k;
   hipError_t e = quantize ? hg::launch_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream)
                           : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream);
+  if (e == hipSuccess && quantize && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, false, stream);
   if (e != hipSuccess) return fail(HG_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }
@@ -276,6 +278,7 @@ int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
     return fail(HG_ERR_SHAPE, "grid of %llu workgroups too large", (unsigned long long)(2 * blocks_k));
   p.blocks_k = (uint32_t)blocks_k;
   hipError_t e = hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream);
+  if (e == hipSuccess && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, true, stream);
   if (e != hipSuccess) return fail(HG_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

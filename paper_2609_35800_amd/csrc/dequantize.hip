@@ -62,7 +62,7 @@ template <int D, int BITS>
 __device__ __forceinline__ void dequantize_kivi_keys(const uint8_t* __restrict__ codes,
                                                      const uint32_t* __restrict__ meta,
                                                      uint16_t* __restrict__ rows,
-                                                     int g_first, int n, int lane) {
+                                                     int g_first, int group, int n, int lane) {
   constexpr int LPR = D / 8;
   constexpr int RPL = 64 / LPR;
   constexpr int NL = kWaveTokens / RPL;
@@ -70,7 +70,7 @@ __device__ __forceinline__ void dequantize_kivi_keys(const uint8_t* __restrict__
   const int c8 = lane % LPR;
   const int r = lane / LPR;
 
-  const u32x4* mp = (const u32x4*)(meta + (size_t)(g_first / kWaveTokens) * D + 8 * c8);
+  const u32x4* mp = (const u32x4*)(meta + (size_t)group * D + 8 * c8);
   const u32x4 m0 = mp[0], m1 = mp[1];
   const uint32_t mw[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
   float S[8], m[8];
@@ -136,7 +136,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
   }
   const uint8_t* codes = p.codes[sl.X] + slab * p.n * (D * BITS / 8);
   if (BASE == HG_BASE_KIVI && sl.X == 0) {
-    dequantize_kivi_keys<D, BITS>(codes, p.meta[0] + slab * p.ngroups * D, rows, t_first, p.n, lane);
+    const int group = p.kivi_whole ? 0 : t_first / kWaveTokens;
+    dequantize_kivi_keys<D, BITS>(codes, p.meta[0] + slab * p.ngroups * D, rows, t_first, group, p.n, lane);
   } else {
     const uint32_t* meta = p.meta[sl.X] + slab * p.n;
     if (BASE == HG_BASE_AKVQ && sl.X == 0)

@@ -27,7 +27,8 @@ __device__ __forceinline__ constexpr int fq_slot(int t, int c) {
 }
 
 template <int D, int BITS, bool ROTATE>
-__device__ __forceinline__ void fake_tokens(const uint16_t* __restrict__ rows, uint16_t* __restrict__ out,
+// rows and out may be the same memory (in place): no restrict qualifiers.
+__device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out,
                                             int t_first, int n, int lane, u32x4* __restrict__ stage) {
   constexpr int E = D / 4;             // elements per lane (quad per token)
   constexpr int NV = E / 8;            // 16-byte chunks per lane
@@ -108,7 +109,7 @@ __device__ __forceinline__ void fake_tokens(const uint16_t* __restrict__ rows, u
 }
 
 template <int D, int BITS>
-__device__ __forceinline__ void fake_kivi_keys(const uint16_t* __restrict__ rows, uint16_t* __restrict__ out,
+__device__ __forceinline__ void fake_kivi_keys(const uint16_t* rows, uint16_t* out,
                                                int g_first, int n, int lane) {
   constexpr int LPR = D / 8;             // lanes per token row (8 channels each)
   constexpr int RPL = 64 / LPR;          // token rows per load
@@ -198,6 +199,7 @@ void fake_quantize_kernel(const Params p) {
     return;
   }
   if (BASE == HG_BASE_KIVI && sl.X == 0) {
+    if (p.kivi_whole) return;  // whole-sequence key ranges: kivi_seq.hip
     fake_kivi_keys<D, BITS>(rows, out, t_first, p.n, lane);
   } else {
     __shared__ u32x4 stage_all[kThreads / 64][16 * (D / 8)];

@@ -38,6 +38,7 @@ struct Params {
   int32_t L, B, H, T;
   int32_t s0, n;             // image span
   int32_t keys_only;
+  int32_t kivi_whole;        // KIVI keys: one range over the whole sequence (kivi_seq.hip)
   int32_t ngroups;           // KIVI key groups per slice
   int32_t tiles;             // kBlockTokens tiles per slice
   uint32_t blocks_k;         // blocks of tensor K
@@ -51,6 +52,8 @@ hipError_t launch_dequantize(const Params& p, int base, int D, int bits, uint32_
                              hipStream_t stream);
 hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
                                 hipStream_t stream);
+// KIVI keys over the whole sequence: one workgroup per key slice.
+hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, hipStream_t stream);
 
 // Routing of one (tensor, slice): whether it is kept in BF16 and its slot in
 // the packed buffers (rank among kept heads if kept, else among quantized

@@ -195,6 +195,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
   }
   uint8_t* codes = p.codes[sl.X] + slab * p.n * (D * BITS / 8);
   if (BASE == HG_BASE_KIVI && sl.X == 0) {
+    if (p.kivi_whole) return;  // whole-sequence key ranges: kivi_seq.hip
     uint32_t* meta = p.meta[0] + slab * p.ngroups * D;
     quantize_kivi_keys<D, BITS>(rows, codes, meta, t_first, p.n, lane);
   } else {

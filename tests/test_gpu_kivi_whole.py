@@ -1,0 +1,67 @@
+"""GPU parity of KIVI-style keys with one range per channel over the whole
+supplied sequence, text included (kivi_group = 0; §4 Quantization setup),
+against the oracle: codes, metadata, side store and reconstruction
+bit-exact for quantize / dequantize and for the one-pass simulated
+quantization; full-size sampled slices on the LLaVA-NeXT-7B-shaped cache."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synthkv
+from hgtest import compare_full
+from test_gpu_fakequant import check as check_fake
+from test_gpu_parity import _assert_exact, small
+
+pytestmark = pytest.mark.gpu
+
+CASES = [small("kivi", D, bits, ko).with_(kivi_group=0, name=f"kiviseq-D{D}-b{bits}-ko{ko}")
+         for D in (64, 128) for bits in (2, 3, 4) for ko in (0, 1)]
+
+
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def test_small(w):
+    K, V = synthkv.gen_kv(w)
+    _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), w.name)
+
+
+@pytest.mark.parametrize("w", CASES[:6], ids=lambda w: w.name)
+@pytest.mark.parametrize("inplace", [False, True])
+def test_fake(w, inplace):
+    K, V = synthkv.gen_kv(w)
+    check_fake(w, K, V, synthkv.protect_mask(w), inplace)
+
+
+@pytest.mark.parametrize("img_len,img_start,text", [(1, 0, 0), (5, 3, 40), (130, 0, 7), (64, 64, 0)])
+def test_spans(img_len, img_start, text):
+    w = small("kivi", img_len=img_len, img_start=img_start, text=text, L=1, B=2, H=2,
+              n_protected=1).with_(kivi_group=0)
+    K, V = synthkv.gen_kv(w)
+    K[0, 0, 0, 0, 3] = 3000.0  # a large value in the first row (text when img_start > 0)
+    _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), f"span{img_len}")
+
+
+def test_full_size_llava():
+    import paper_2609_35800_amd as hg
+    w = synthkv.WORKLOADS["llava-next-7b"].with_(kivi_group=0)
+    mask = synthkv.protect_mask(w)
+    cfg = hg.make_config(**w.config_fields())
+    K, V = synthkv.gen_kv(w, device="cuda")
+    packed = hg.alloc_packed(cfg, mask)
+    hg.hg_quantize(cfg, K, V, mask, packed)
+    torch.cuda.synchronize()
+    ocfg = oracle.make_config(**w.config_fields())
+    row = w.D * w.bits // 8
+    codes = packed["codes_k"].view(-1, w.B, w.img_len, row)
+    meta = packed["meta_k"].view(torch.int32).view(-1, w.B, 1, w.D)
+    rng = np.random.default_rng(3)
+    checked = 0
+    while checked < 10:
+        l, b, h = int(rng.integers(w.L)), int(rng.integers(w.B)), int(rng.integers(w.H))
+        prot, slot = oracle.route(ocfg, mask, 0, l, h)
+        if prot:
+            continue
+        oc, om = oracle.quantize_slice_seq(ocfg, 0, synthkv.bf16_bits(K[l, b, h]))
+        assert np.array_equal(codes[slot, b].cpu().numpy(), oc)
+        assert np.array_equal(meta[slot, b].cpu().numpy().view(np.uint32), om)
+        checked += 1
