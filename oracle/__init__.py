@@ -35,14 +35,16 @@ def build() -> str:
 class Config(C.Structure):
     _fields_ = [(n, C.c_int32) for n in
                 ("L", "B", "H", "T", "D", "img_start", "img_len", "bits", "base",
-                 "keys_only", "kivi_group")]
+                 "keys_only", "kivi_group", "retain_permille")]
 
 
 class Sizes(C.Structure):
     _fields_ = [("codes_k", C.c_uint64), ("meta_k", C.c_uint64), ("side_k", C.c_uint64),
                 ("codes_v", C.c_uint64), ("meta_v", C.c_uint64), ("side_v", C.c_uint64),
+                ("norm_k", C.c_uint64), ("ret_idx", C.c_uint64), ("ret_k", C.c_uint64),
+                ("ret_v", C.c_uint64),
                 ("n_protected", C.c_int32), ("n_unprot_k", C.c_int32),
-                ("n_unprot_v", C.c_int32)]
+                ("n_unprot_v", C.c_int32), ("retain_count", C.c_int32)]
 
 
 _lib = None
@@ -74,9 +76,15 @@ def lib():
         L.hgo_quantize.argtypes = [C.POINTER(Config), P, P, P, P, P, P, P, P, P, C.c_int]
         L.hgo_dequantize.argtypes = [C.POINTER(Config), P, P, P, P, P, P, P, P, P, C.c_int]
         L.hgo_select_heads.argtypes = [P, P, C.c_int, C.c_int, C.c_int, C.c_int, P]
+        L.hgo_retain_count.argtypes = [C.POINTER(Config)]
+        L.hgo_key_sqnorm.argtypes = [P, C.c_int]; L.hgo_key_sqnorm.restype = C.c_float
+        L.hgo_retain_select.argtypes = [P, C.c_int, C.c_int, P]
+        L.hgo_retain.argtypes = [C.POINTER(Config), P, P, P, P, P, P, P, C.c_int]
+        L.hgo_restore_retained.argtypes = [C.POINTER(Config), P, P, P, P, P, P]
         for f in ("hgo_route", "hgo_sizes", "hgo_quantize_slice", "hgo_quantize_slice_seq",
                   "hgo_dequantize_slice",
-                  "hgo_quantize", "hgo_dequantize", "hgo_select_heads"):
+                  "hgo_quantize", "hgo_dequantize", "hgo_select_heads", "hgo_retain_count",
+                  "hgo_retain_select", "hgo_retain", "hgo_restore_retained"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -91,6 +99,9 @@ def _ptr(a: np.ndarray):
 
 def make_config(**f) -> Config:
     return Config(**{k: int(v) for k, v in f.items()})
+
+
+RETAIN_BUFFERS = ("norm_k", "ret_idx", "ret_k", "ret_v")
 
 
 # ---------------------------------------------------------------- small pieces
@@ -218,6 +229,16 @@ def quantize(cfg: Config, K: np.ndarray, V: np.ndarray, mask: np.ndarray, thread
                             int(threads))
     if rc:
         raise ValueError("hgo_quantize failed")
+    out["norm_k"] = np.zeros(sz["norm_k"] // 4, dtype=np.float32)
+    out["ret_idx"] = np.zeros(sz["ret_idx"] // 4, dtype=np.int32)
+    out["ret_k"] = np.zeros(sz["ret_k"] // 2, dtype=np.uint16)
+    out["ret_v"] = np.zeros(sz["ret_v"] // 2, dtype=np.uint16)
+    if cfg.retain_permille > 0:
+        rc = lib().hgo_retain(C.byref(cfg), _ptr(K), _ptr(V), _ptr(mask), _ptr(out["norm_k"]),
+                              _ptr(out["ret_idx"]), _ptr(out["ret_k"]), _ptr(out["ret_v"]),
+                              int(threads))
+        if rc:
+            raise ValueError("hgo_retain failed")
     return out
 
 
@@ -233,6 +254,30 @@ def dequantize(cfg: Config, mask: np.ndarray, packed: Dict[str, np.ndarray],
                               _ptr(K_out), _ptr(V_out), int(threads))
     if rc:
         raise ValueError("hgo_dequantize failed")
+    if cfg.retain_permille > 0:
+        rc = lib().hgo_restore_retained(C.byref(cfg), _ptr(mask), _ptr(p["ret_idx"]),
+                                        _ptr(p["ret_k"]), _ptr(p["ret_v"]), _ptr(K_out), _ptr(V_out))
+        if rc:
+            raise ValueError("hgo_restore_retained failed")
+
+
+def retain_count(cfg: Config) -> int:
+    return int(lib().hgo_retain_count(C.byref(cfg)))
+
+
+def key_sqnorm(key) -> float:
+    """fp32 squared norm of one BF16 key (uint16 bit patterns)."""
+    key = np.ascontiguousarray(key, dtype=np.uint16)
+    return float(np.float32(lib().hgo_key_sqnorm(_ptr(key), key.size)))
+
+
+def retain_select(sqnorm, k: int) -> np.ndarray:
+    """Indices (ascending) of the k largest values, lower index first among equals."""
+    sqnorm = np.ascontiguousarray(sqnorm, dtype=np.float32)
+    idx = np.zeros(k, dtype=np.int32)
+    if lib().hgo_retain_select(_ptr(sqnorm), sqnorm.size, int(k), _ptr(idx)):
+        raise ValueError("hgo_retain_select: bad arguments")
+    return idx
 
 
 def select_heads(g: np.ndarray, o: np.ndarray, Hkv: int, K: int) -> np.ndarray:

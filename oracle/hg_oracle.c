@@ -147,6 +147,8 @@ static int cfg_ok(const hgo_config* c) {
   if (c->base < HGO_MINMAX || c->base > HGO_AKVQ) return 0;
   if (c->base == HGO_KIVI && c->kivi_group < 0) return 0;
   if (c->base == HGO_AKVQ && (c->D & (c->D - 1)) != 0) return 0;
+  if (c->retain_permille < 0 || c->retain_permille > 1000) return 0;
+  if (c->retain_permille > 0 && c->base != HGO_AKVQ) return 0;
   return 1;
 }
 
@@ -205,6 +207,12 @@ int hgo_sizes(const hgo_config* c, const uint8_t* mask, hgo_sizes_t* out) {
   out->meta_v = (uint64_t)uv * B * meta_words_per_slice(c, 1) * 4;
   out->side_k = (uint64_t)P * B * n * D * 2;
   out->side_v = (uint64_t)pv * B * n * D * 2;
+  uint64_t k = (uint64_t)hgo_retain_count(c);
+  out->retain_count = (int32_t)k;
+  out->norm_k = c->retain_permille > 0 ? (uint64_t)LH * B * n * 4 : 0;
+  out->ret_idx = (uint64_t)LH * B * k * 4;
+  out->ret_k = (uint64_t)uk * B * k * D * 2;
+  out->ret_v = (uint64_t)uv * B * k * D * 2;
   return 0;
 }
 
@@ -431,6 +439,158 @@ int hgo_dequantize(const hgo_config* c, const uint8_t* mask,
   j.side[0] = (uint16_t*)side_k; j.side[1] = (uint16_t*)side_v;
   j.out[0] = K_out; j.out[1] = V_out;
   return run_all(&j, threads);
+}
+
+/* ---------------------------------------------------- AKVQ-style retention
+ *
+ * §4 Quantization setup: in each KV head the AKVQ-style base also keeps the
+ * keys and values of a nominal 2 % of the image tokens in BF16, the tokens
+ * whose keys have the largest norms, whether or not HeadGuard protects heads.
+ * Readings (the paper fixes none of these):
+ *  - the fraction is retain_permille / 1000 of the n image tokens of the head
+ *    (20 for the paper's 2 %), k = round(n * fraction) with halves rounded up;
+ *  - the norm is that of the key as stored (before the rotation, which keeps
+ *    norms), computed as its square in fp32: each entry squared, then summed
+ *    pairwise (adjacent entries, then adjacent pairs, ...), and tokens are
+ *    ranked by that fp32 value, equal values to the lower token index;
+ *  - a retained token is still quantized like every other (per-token groups do
+ *    not interact); its BF16 row replaces the reconstruction;
+ *  - per batch row and head the retained tokens are the same for K and V, and
+ *    a row is stored only where that tensor is quantized (a protected head's
+ *    BF16 rows already hold it).
+ */
+int hgo_retain_count(const hgo_config* c) {
+  if (c->retain_permille <= 0) return 0;
+  int64_t num = (int64_t)c->img_len * c->retain_permille;
+  return (int)((num + 500) / 1000);
+}
+
+float hgo_key_sqnorm(const uint16_t* key, int D) {
+  float a[D];
+  for (int d = 0; d < D; ++d) {
+    float x = hgo_bf16_to_f32(key[d]);
+    a[d] = x * x;
+  }
+  for (int w = D / 2; w >= 1; w /= 2)
+    for (int i = 0; i < w; ++i) a[i] = a[2 * i] + a[2 * i + 1];
+  return a[0];
+}
+
+int hgo_retain_select(const float* sqnorm, int n, int k, int32_t* idx) {
+  if (n < 0 || k < 0 || k > n) return -1;
+  uint8_t* taken = (uint8_t*)calloc((size_t)n + 1, 1);
+  if (!taken) return -1;
+  /* k times: the largest remaining value, the lowest index among equals */
+  for (int r = 0; r < k; ++r) {
+    int best = -1;
+    for (int i = 0; i < n; ++i)
+      if (!taken[i] && (best < 0 || sqnorm[i] > sqnorm[best])) best = i;
+    taken[best] = 1;
+  }
+  int m = 0;
+  for (int i = 0; i < n; ++i)
+    if (taken[i]) idx[m++] = i;
+  free(taken);
+  return 0;
+}
+
+typedef struct {
+  const hgo_config* c;
+  const uint8_t* mask;
+  const uint16_t* in[2];
+  float* norm_k;
+  int32_t* ret_idx;
+  uint16_t* ret[2];
+  int tid, nthreads, status;
+} retain_job_t;
+
+static void* retain_heads(void* arg) {
+  retain_job_t* j = (retain_job_t*)arg;
+  const hgo_config* c = j->c;
+  int n = c->img_len, D = c->D, k = hgo_retain_count(c);
+  long nslices = (long)c->L * c->B * c->H;
+  for (long s = j->tid; s < nslices; s += j->nthreads) {
+    int l = (int)(s / ((long)c->B * c->H));
+    int b = (int)((s / c->H) % c->B);
+    int h = (int)(s % c->H);
+    const uint16_t* keys = j->in[0] + ((size_t)s * c->T + c->img_start) * D;
+    float* nrm = j->norm_k + (size_t)s * n;
+    for (int t = 0; t < n; ++t) nrm[t] = hgo_key_sqnorm(keys + (size_t)t * D, D);
+    int32_t* idx = j->ret_idx + (size_t)s * k;
+    if (k == 0) continue;
+    if (hgo_retain_select(nrm, n, k, idx) != 0) { j->status = -1; return NULL; }
+    for (int X = 0; X < 2; ++X) {
+      int prot, slot;
+      if (hgo_route(c, j->mask, X, l, h, &prot, &slot) != 0) { j->status = -1; return NULL; }
+      if (prot) continue;
+      const uint16_t* rows = j->in[X] + ((size_t)s * c->T + c->img_start) * D;
+      uint16_t* dst = j->ret[X] + ((size_t)slot * c->B + b) * k * D;
+      for (int r = 0; r < k; ++r) memcpy(dst + (size_t)r * D, rows + (size_t)idx[r] * D, (size_t)D * 2);
+    }
+  }
+  return NULL;
+}
+
+int hgo_retain(const hgo_config* c, const uint16_t* K, const uint16_t* V,
+               const uint8_t* mask, float* norm_k, int32_t* ret_idx,
+               uint16_t* ret_k, uint16_t* ret_v, int threads) {
+  if (!cfg_ok(c) || c->retain_permille <= 0 || !K || !V || !mask) return -1;
+  if (c->img_len == 0) return 0; /* no image tokens: nothing to rank or keep */
+  if (!norm_k || (hgo_retain_count(c) > 0 && !ret_idx)) return -1;
+  if (threads < 1) threads = 1;
+  retain_job_t* jobs = (retain_job_t*)calloc((size_t)threads, sizeof(retain_job_t));
+  pthread_t* th = (pthread_t*)calloc((size_t)threads, sizeof(pthread_t));
+  if (!jobs || !th) { free(jobs); free(th); return -1; }
+  for (int t = 0; t < threads; ++t) {
+    retain_job_t* j = &jobs[t];
+    j->c = c; j->mask = mask;
+    j->in[0] = K; j->in[1] = V;
+    j->norm_k = norm_k; j->ret_idx = ret_idx;
+    j->ret[0] = ret_k; j->ret[1] = ret_v;
+    j->tid = t; j->nthreads = threads;
+  }
+  int started = 0;
+  for (int t = 1; t < threads; ++t)
+    if (pthread_create(&th[t], NULL, retain_heads, &jobs[t]) == 0) started = t; else break;
+  if (started != threads - 1) {
+    for (int t = 1; t <= started; ++t) pthread_join(th[t], NULL);
+    for (int t = 0; t < threads; ++t) jobs[t].status = 0;
+    jobs[0].nthreads = 1;
+    retain_heads(&jobs[0]);
+  } else {
+    retain_heads(&jobs[0]);
+    for (int t = 1; t < threads; ++t) pthread_join(th[t], NULL);
+  }
+  int status = 0;
+  for (int t = 0; t < threads; ++t) if (jobs[t].status) status = -1;
+  free(jobs);
+  free(th);
+  return status;
+}
+
+int hgo_restore_retained(const hgo_config* c, const uint8_t* mask,
+                         const int32_t* ret_idx, const uint16_t* ret_k,
+                         const uint16_t* ret_v, uint16_t* K_out, uint16_t* V_out) {
+  if (!cfg_ok(c) || c->retain_permille <= 0 || !mask || !K_out || !V_out) return -1;
+  int D = c->D, k = hgo_retain_count(c);
+  if (k == 0) return 0;
+  const uint16_t* ret[2] = {ret_k, ret_v};
+  uint16_t* out[2] = {K_out, V_out};
+  for (long s = 0; s < (long)c->L * c->B * c->H; ++s) {
+    int l = (int)(s / ((long)c->B * c->H));
+    int b = (int)((s / c->H) % c->B);
+    int h = (int)(s % c->H);
+    const int32_t* idx = ret_idx + (size_t)s * k;
+    for (int X = 0; X < 2; ++X) {
+      int prot, slot;
+      if (hgo_route(c, mask, X, l, h, &prot, &slot) != 0) return -1;
+      if (prot) continue;
+      uint16_t* rows = out[X] + ((size_t)s * c->T + c->img_start) * D;
+      const uint16_t* src = ret[X] + ((size_t)slot * c->B + b) * k * D;
+      for (int r = 0; r < k; ++r) memcpy(rows + (size_t)idx[r] * D, src + (size_t)r * D, (size_t)D * 2);
+    }
+  }
+  return 0;
 }
 
 /* ------------------------------------------------------------ head selection

@@ -22,8 +22,13 @@
  *                                             (range over the whole sequence)
  *                 each word = bf16(scale) | bf16(min) << 16
  *   side_X        BF16 bits [p][B][n][D]     protected heads' image rows
+ * AKVQ-style token retention (retain_permille > 0, §4):
+ *   norm_k        fp32 [L][B][H][n]          squared norm of every image key
+ *   ret_idx       int32 [L][B][H][k]         retained image tokens, ascending
+ *   ret_X         BF16 bits [slot][B][k][D]  their rows, for quantized slots
  * where n = img_len, slot = rank of (l,h) among the heads whose tensor X is
- * quantized, p = rank of (l,h) among protected heads (row-major (l,h) order).
+ * quantized, p = rank of (l,h) among protected heads (row-major (l,h) order),
+ * k = the retained count per head.
  */
 #ifndef HG_ORACLE_H
 #define HG_ORACLE_H
@@ -43,11 +48,14 @@ typedef struct {
   int32_t base;
   int32_t keys_only;
   int32_t kivi_group;
+  int32_t retain_permille; /* AKVQ-style retention, per mille of image tokens; 0 = off */
 } hgo_config;
 
 typedef struct {
   uint64_t codes_k, meta_k, side_k, codes_v, meta_v, side_v; /* bytes */
+  uint64_t norm_k, ret_idx, ret_k, ret_v;                    /* bytes */
   int32_t n_protected, n_unprot_k, n_unprot_v;
+  int32_t retain_count;
 } hgo_sizes_t;
 
 /* BF16 <-> fp32 helpers (exposed so the tests can pin them). */
@@ -103,6 +111,28 @@ int hgo_dequantize(const hgo_config* c, const uint8_t* mask,
                    const uint8_t* codes_v, const uint32_t* meta_v,
                    const uint16_t* side_v,
                    uint16_t* K_out, uint16_t* V_out, int threads);
+
+/* AKVQ-style token retention (§4 Quantization setup): in every KV head the
+ * keys and values of the k image tokens whose keys have the largest norms stay
+ * in BF16, with or without head protection. */
+/* k = round(n * retain_permille / 1000), halves rounded up. */
+int hgo_retain_count(const hgo_config* c);
+/* Squared L2 norm of one BF16 key of D (a power of two) entries in fp32:
+ * squares, then pairwise sums over adjacent blocks of 1, 2, 4, ... entries. */
+float hgo_key_sqnorm(const uint16_t* key, int D);
+/* The k largest of n values (lower index first among equals), written to
+ * idx[k] in ascending index order. */
+int hgo_retain_select(const float* sqnorm, int n, int k, int32_t* idx);
+/* Whole cache: norm_k, ret_idx and the retained rows of the quantized slots
+ * (layouts above).  ret_k / ret_v may be NULL when they hold no slot. */
+int hgo_retain(const hgo_config* c, const uint16_t* K, const uint16_t* V,
+               const uint8_t* mask, float* norm_k, int32_t* ret_idx,
+               uint16_t* ret_k, uint16_t* ret_v, int threads);
+/* After hgo_dequantize: the retained rows of the quantized slots are written
+ * back bit-identical into K_out / V_out. */
+int hgo_restore_retained(const hgo_config* c, const uint8_t* mask,
+                         const int32_t* ret_idx, const uint16_t* ret_k,
+                         const uint16_t* ret_v, uint16_t* K_out, uint16_t* V_out);
 
 /* Head selection (§3 Eq. 2): g, o are per-query-head scores [L][Hq] (fp64);
  * query head hq belongs to KV head hq / (Hq/Hkv).  Writes mask[L*Hkv] with

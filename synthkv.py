@@ -52,6 +52,7 @@ class Workload:
     k_outlier_scale: float
     kivi_group: int = 32
     seed: int = 0
+    retain_permille: int = 0  # AKVQ-style token retention; 20 = the paper's 2 %
 
     def with_(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
@@ -66,7 +67,8 @@ class Workload:
         return dict(L=self.L, B=self.B, H=self.H, T=self.T, D=self.D,
                     img_start=self.img_start, img_len=self.img_len,
                     bits=self.bits, base=BASES[self.base],
-                    keys_only=self.keys_only, kivi_group=self.kivi_group)
+                    keys_only=self.keys_only, kivi_group=self.kivi_group,
+                    retain_permille=self.retain_permille)
 
 
 # The five workloads: a tiny case, then caches shaped like the paper's 7B-72B

@@ -5,7 +5,8 @@ The planted mistakes cover each step of the method: rounding directions and
 tie rules, the range, the scale and its levels, reconstruction, the
 Walsh-Hadamard butterflies and scale, routing ranks and K-only protection,
 KIVI-style group indexing, bit packing, the image-span offset, the buffer
-sizes, and the head selection's sum, grouping, standardization and ties."""
+sizes, the head selection's sum, grouping, standardization and ties, and the
+token retention's count, norm, ranking, ties and row routing."""
 import concurrent.futures as cf
 import os
 import shutil
@@ -69,6 +70,26 @@ MUTANTS = [
     ("select_ties_to_upper", "if (!mask[i] && (best < 0 || sc[i] > sc[best])) best = i;",
      "if (!mask[i] && (best < 0 || sc[i] >= sc[best])) best = i;"),
     ("select_mean_off_by_one", "  mean /= n;", "  mean /= n + 1;"),
+    ("retain_count_floor", "return (int)((num + 500) / 1000);", "return (int)(num / 1000);"),
+    ("retain_smallest", "if (!taken[i] && (best < 0 || sqnorm[i] > sqnorm[best])) best = i;",
+     "if (!taken[i] && (best < 0 || sqnorm[i] < sqnorm[best])) best = i;"),
+    ("retain_ties_upper", "if (!taken[i] && (best < 0 || sqnorm[i] > sqnorm[best])) best = i;",
+     "if (!taken[i] && (best < 0 || sqnorm[i] >= sqnorm[best])) best = i;"),
+    ("sqnorm_running_sum", "for (int i = 0; i < w; ++i) a[i] = a[2 * i] + a[2 * i + 1];",
+     "if (w == 1) for (int d = 1; d < D; ++d) a[0] = a[0] + a[d];"),
+    ("sqnorm_l1", "    a[d] = x * x;", "    a[d] = fabsf(x);"),
+    ("sqnorm_of_rotated_key", "    a[d] = x * x;\n  }",
+     "    a[d] = x;\n  }\n  hgo_fwht_norm(a, D);\n  for (int d = 0; d < D; ++d) a[d] = a[d] * a[d];"),
+    ("retain_norm_span_offset_dropped",
+     "const uint16_t* keys = j->in[0] + ((size_t)s * c->T + c->img_start) * D;",
+     "const uint16_t* keys = j->in[0] + (size_t)s * c->T * D;"),
+    ("retain_values_from_keys",
+     "const uint16_t* rows = j->in[X] + ((size_t)s * c->T + c->img_start) * D;",
+     "const uint16_t* rows = j->in[0] + ((size_t)s * c->T + c->img_start) * D;"),
+    ("restore_skips_values", "      uint16_t* rows = out[X] + ((size_t)s * c->T + c->img_start) * D;",
+     "      if (X == 1) continue;\n      uint16_t* rows = out[X] + ((size_t)s * c->T + c->img_start) * D;"),
+    ("retain_ret_sized_for_all_heads", "out->ret_k = (uint64_t)uk * B * k * D * 2;",
+     "out->ret_k = (uint64_t)LH * B * k * D * 2;"),
 ]
 
 
@@ -88,7 +109,8 @@ def _run_mutant(name, old, new, tmp):
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(ROOT, "tests", "test_oracle_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_cache.py"),
-                        os.path.join(ROOT, "tests", "test_select_pins.py")],
+                        os.path.join(ROOT, "tests", "test_select_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_retain.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     return name, r.returncode
 
