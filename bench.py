@@ -38,6 +38,8 @@ def parse():
     ap.add_argument("--bits", type=int, default=None, help="override the workload's bit width")
     ap.add_argument("--kivi-group", type=int, default=None,
                     help="override the KIVI key group (0: one range over the whole sequence)")
+    ap.add_argument("--retain-permille", type=int, default=None,
+                    help="AKVQ-style token retention per mille (20 = the paper's 2 %%)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time budget of the oracle sample")
@@ -73,10 +75,20 @@ def traffic_from_profile(workload: str, bits: int):
 
 
 def algorithmic_bytes(w, sizes) -> dict:
+    """Bytes each call must move at least.  Quantize: the image rows of K and V
+    read once, every packed buffer written once; with token retention also the
+    key norms read back by the selection and the retained rows read again
+    (the selection needs every norm first).  Dequantize: the packed buffers
+    read, the image rows written; with retention the retained rows are
+    written over the reconstruction."""
     img_elems = w.L * w.B * w.H * w.img_len * w.D
     read = 2 * img_elems * 2  # K and V image rows, BF16
     write = sum(sizes[n] for n in ("codes_k", "meta_k", "side_k", "codes_v", "meta_v", "side_v"))
-    return {"quant": read + write, "dequant": read + write, "read": read, "write": write}
+    rows = sizes.get("ret_k", 0) + sizes.get("ret_v", 0)
+    quant_extra = 2 * sizes.get("norm_k", 0) + sizes.get("ret_idx", 0) + 2 * rows
+    dequant_extra = sizes.get("ret_idx", 0) + 2 * rows
+    return {"quant": read + write + quant_extra, "dequant": read + write + dequant_extra,
+            "read": read, "write": write}
 
 
 def cpu_baseline(w, K, V, mask, budget_s: float):
@@ -148,7 +160,8 @@ def bench_fakequant(args, hg, w, cfg, mask, K, V):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded N(0,1) BF16 KV with outlier key channels; no model weights)",
         "config": {"workload": w.name, "bits": w.bits, "base": w.base, "keys_only": w.keys_only,
-                   **({"kivi_group": w.kivi_group} if w.base == "kivi" else {})},
+                   **({"kivi_group": w.kivi_group} if w.base == "kivi" else {}),
+                   **({"retain_permille": w.retain_permille} if w.retain_permille else {})},
         "image_tokens_per_s": round(w.B * w.img_len / (ms * 1e-3), 1),
         "roofline": {"bound": "hbm", "kernel": "fake_quantize_kernel", "achieved": round(gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
@@ -173,6 +186,8 @@ def main():
         w = w.with_(bits=args.bits)
     if args.kivi_group is not None:
         w = w.with_(kivi_group=args.kivi_group)
+    if args.retain_permille is not None:
+        w = w.with_(retain_permille=args.retain_permille)
     mask = synthkv.protect_mask(w)
     cfg = hg.make_config(**w.config_fields())
     sizes = hg.hg_packed_sizes(cfg, mask)
@@ -244,6 +259,7 @@ def main():
                    "img_start": w.img_start, "img_len": w.img_len, "bits": w.bits,
                    "base": w.base, "keys_only": w.keys_only, "protected_heads": int(mask.sum()),
                    **({"kivi_group": w.kivi_group} if w.base == "kivi" else {}),
+                   **({"retain_permille": w.retain_permille} if w.retain_permille else {}),
                    "parallelism": "single GPU"},
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "image_tokens_per_s": round(w.B * w.img_len * args.steps / elapsed, 1),

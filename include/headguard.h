@@ -18,7 +18,10 @@
  *                   paper's KIVI-style harness; text still stays BF16);
  *                   values per token;
  *   HG_BASE_AKVQ    keys rotated by the normalized Walsh-Hadamard matrix over
- *                   head_dim, then per token; values per token, unrotated.
+ *                   head_dim, then per token; values per token, unrotated;
+ *                   optionally (retain_permille > 0) the keys and values of
+ *                   the image tokens with the largest key norms stay in BF16
+ *                   in every head (§4: a nominal 2 %, retain_permille = 20).
  *
  * Quantizer of one group of values v (a token vector, or one channel of a
  * KIVI key group), all in IEEE fp32 with round-to-nearest-even:
@@ -44,9 +47,21 @@
  * quantized; p = rank among the heads whose X is kept in BF16.  V is kept iff
  * the head is protected and keys_only == 0.
  *
+ * Token retention (AKVQ, retain_permille > 0; §4 Quantization setup).  Per
+ * (l, b, h), k = round(n * retain_permille / 1000) (halves up) image tokens
+ * are retained: those whose keys, as stored (before the rotation), have the
+ * largest squared norm, computed in fp32 as the squares summed pairwise over
+ * adjacent blocks of 1, 2, 4, ... channels; equal norms go to the lower
+ * token.  Every token is still quantized; a retained token's BF16 row
+ * replaces its reconstruction, for each tensor the head does not keep:
+ *   norm_k    fp32 [L][B][H][n]      squared key norm of every image token
+ *   ret_idx   int32 [L][B][H][k]     retained tokens (0-based in the span), ascending
+ *   ret_X     BF16 [slot][B][k][D]   their rows, for the quantized slots of X
+ *
  * Ownership and synchronisation: the caller allocates every buffer.  Device
  * buffers are device memory of the current HIP device; the mask is host
- * memory read during the call only.  The library allocates nothing, keeps no
+ * memory read during the call only.  The library allocates nothing (except
+ * hg_fake_quantize's stream-ordered workspace with token retention), keeps no
  * state between calls and never synchronises: HG_OK means the work is
  * enqueued on `stream`; device faults surface at the caller's next
  * synchronisation.  Every argument check runs before any launch, so on error
@@ -76,7 +91,8 @@ enum {
   HG_ERR_SHAPE = 2,     /* L, B, H, T not positive, or L*H > HG_MAX_HEADS      */
   HG_ERR_SPAN = 3,      /* image span outside [0, T]                           */
   HG_ERR_BITS = 4,      /* bits not in {2, 3, 4}                               */
-  HG_ERR_BASE = 5,      /* unknown base, or kivi_group not 32 or 0             */
+  HG_ERR_BASE = 5,      /* unknown base, kivi_group not 32 or 0, retain_permille
+                           outside [0, 1000] or set with a base other than AKVQ */
   HG_ERR_HEADDIM = 6,   /* D not in {64, 128}                                  */
   HG_ERR_ALIGN = 7,     /* a device pointer is not 16-byte aligned             */
   HG_ERR_MASK = 8,      /* a mask entry is neither 0 nor 1                     */
@@ -97,19 +113,23 @@ typedef struct {
   int32_t base;                /* hg_base                                          */
   int32_t keys_only;           /* 1: protect K only; 0: protect K and V            */
   int32_t kivi_group;          /* KIVI key group: 32 tokens, or 0 = whole sequence */
+  int32_t retain_permille;     /* AKVQ token retention per mille (20 = 2 %), 0 = off */
 } hg_config;
 
 typedef struct {
   uint64_t codes_k, meta_k, side_k, codes_v, meta_v, side_v; /* bytes          */
+  uint64_t norm_k, ret_idx, ret_k, ret_v;  /* bytes; 0 without token retention    */
   int32_t n_protected;         /* heads with mask = 1                             */
   int32_t n_unprot_k, n_unprot_v; /* heads whose K / V are quantized              */
+  int32_t retain_count;        /* k, retained tokens per (l, b, h)                */
 } hg_sizes;
 
 typedef struct {
   void *codes_k, *meta_k, *side_k, *codes_v, *meta_v, *side_v; /* device */
+  void *norm_k, *ret_idx, *ret_k, *ret_v;                      /* device */
 } hg_packed;
 
-/* Byte sizes of the six packed buffers (the storage model of §5.4).  Pure
+/* Byte sizes of the packed buffers (the storage model of §5.4).  Pure
  * host computation; needs no device.  `protect_mask` is host uint8 [L*H],
  * row-major (l, h), entries 0 or 1. */
 int hg_packed_sizes(const hg_config* cfg, const uint8_t* protect_mask, hg_sizes* out);
@@ -123,8 +143,9 @@ int hg_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
 
 /* Reconstruct the image rows of K_out, V_out (device BF16, same layout and
  * shape as K, V) from the packed buffers (simulated quantization's
- * reconstruction, §4).  Protected rows are copied back from the side store;
- * text rows of K_out, V_out are not written. */
+ * reconstruction, §4).  Protected rows are copied back from the side store,
+ * retained rows from ret_k / ret_v; text rows of K_out, V_out are not
+ * written.  norm_k is not read. */
 int hg_dequantize(const hg_config* cfg, const uint8_t* protect_mask, const hg_packed* in,
                   uint16_t* K_out, uint16_t* V_out, hipStream_t stream);
 
@@ -146,7 +167,10 @@ int hg_select_heads(const double* g, const double* o, int32_t L, int32_t Hq, int
  * followed by hg_dequantize would, without packed buffers.  K_out may be K
  * (in place) and V_out may be V; otherwise they must not overlap them.  Kept
  * rows are copied (left alone in place); text rows are not written.  Device
- * pointers 16-byte aligned. */
+ * pointers 16-byte aligned.  With token retention the call allocates a
+ * stream-ordered workspace (hipMallocAsync / hipFreeAsync on `stream`) for
+ * the key norms and the retained rows, about (4n + k(4 + 4D)) bytes per
+ * (l, b, h); HG_ERR_HIP if it cannot. */
 int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
                      const uint8_t* protect_mask, uint16_t* K_out, uint16_t* V_out,
                      hipStream_t stream);

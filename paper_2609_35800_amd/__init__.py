@@ -26,18 +26,20 @@ STATUS = ("HG_OK", "HG_ERR_NULL", "HG_ERR_SHAPE", "HG_ERR_SPAN", "HG_ERR_BITS", 
           "HG_ERR_POINTER", "HG_ERR_VALUE")
 for _i, _n in enumerate(STATUS):
     globals()[_n] = _i
-BUFFERS = ("codes_k", "meta_k", "side_k", "codes_v", "meta_v", "side_v")
+BUFFERS = ("codes_k", "meta_k", "side_k", "codes_v", "meta_v", "side_v",
+           "norm_k", "ret_idx", "ret_k", "ret_v")
 
 
 class hg_config(C.Structure):
     _fields_ = [(n, C.c_int32) for n in
                 ("L", "B", "H", "T", "D", "img_start", "img_len", "bits", "base",
-                 "keys_only", "kivi_group")]
+                 "keys_only", "kivi_group", "retain_permille")]
 
 
 class hg_sizes(C.Structure):
     _fields_ = [(n, C.c_uint64) for n in BUFFERS] + [
-        ("n_protected", C.c_int32), ("n_unprot_k", C.c_int32), ("n_unprot_v", C.c_int32)]
+        ("n_protected", C.c_int32), ("n_unprot_k", C.c_int32), ("n_unprot_v", C.c_int32),
+        ("retain_count", C.c_int32)]
 
 
 class hg_packed(C.Structure):
@@ -116,11 +118,13 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream
 
 
-def make_config(L, B, H, T, D, img_start, img_len, bits, base, keys_only, kivi_group=32) -> hg_config:
+def make_config(L, B, H, T, D, img_start, img_len, bits, base, keys_only, kivi_group=32,
+                retain_permille=0) -> hg_config:
     if isinstance(base, str):
         base = BASES[base]
     return hg_config(L=L, B=B, H=H, T=T, D=D, img_start=img_start, img_len=img_len, bits=bits,
-                     base=base, keys_only=keys_only, kivi_group=kivi_group)
+                     base=base, keys_only=keys_only, kivi_group=kivi_group,
+                     retain_permille=retain_permille)
 
 
 def hg_packed_sizes(cfg: hg_config, protect_mask) -> Dict[str, int]:

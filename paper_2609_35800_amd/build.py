@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libheadguard.so")
-SOURCES = ["api.hip", "quantize.hip", "dequantize.hip", "fakequant.hip", "kivi_seq.hip",
+SOURCES = ["api.hip", "quantize.hip", "dequantize.hip", "fakequant.hip", "kivi_seq.hip", "retain.hip",
            "select.cpp"]
 ARCH = os.environ.get("HG_OFFLOAD_ARCH", "gfx950")
 

@@ -49,6 +49,10 @@ int check_config(const hg_config* c, const uint8_t* mask) {
   if (c->base == HG_BASE_KIVI && c->kivi_group != hg::kWaveTokens && c->kivi_group != 0)
     return fail(HG_ERR_BASE, "kivi_group %d unsupported (32, or 0 for the whole sequence)", c->kivi_group);
   if (c->keys_only != 0 && c->keys_only != 1) return fail(HG_ERR_SHAPE, "keys_only must be 0 or 1");
+  if (c->retain_permille < 0 || c->retain_permille > 1000)
+    return fail(HG_ERR_BASE, "retain_permille %d outside [0, 1000]", c->retain_permille);
+  if (c->retain_permille > 0 && c->base != HG_BASE_AKVQ)
+    return fail(HG_ERR_BASE, "token retention belongs to the AKVQ base (base %d)", c->base);
   const int LH = c->L * c->H;
   for (int i = 0; i < LH; ++i)
     if (mask[i] > 1) return fail(HG_ERR_MASK, "protect_mask[%d] = %u is neither 0 nor 1", i, mask[i]);
@@ -58,6 +62,7 @@ int check_config(const hg_config* c, const uint8_t* mask) {
 struct Counts {
   int P, uk, uv, pv;
   uint64_t n, row, meta_k_words, meta_v_words;
+  uint64_t k;  // retained tokens per (l, b, h)
 };
 
 Counts counts(const hg_config* c, const uint8_t* mask) {
@@ -73,6 +78,8 @@ Counts counts(const hg_config* c, const uint8_t* mask) {
   const uint64_t groups = c->kivi_group == 0 ? (k.n > 0 ? 1 : 0) : (k.n + hg::kWaveTokens - 1) / hg::kWaveTokens;
   k.meta_k_words = c->base == HG_BASE_KIVI ? groups * c->D : k.n;
   k.meta_v_words = k.n;
+  // round(n * permille / 1000), halves up
+  k.k = c->retain_permille > 0 ? (k.n * (uint64_t)c->retain_permille + 500) / 1000 : 0;
   return k;
 }
 
@@ -198,6 +205,12 @@ int hg_packed_sizes(const hg_config* cfg, const uint8_t* mask, hg_sizes* out) {
   out->meta_v = (uint64_t)k.uv * B * k.meta_v_words * 4;
   out->side_k = (uint64_t)k.P * B * k.n * D * 2;
   out->side_v = (uint64_t)k.pv * B * k.n * D * 2;
+  const uint64_t LHB = (uint64_t)cfg->L * cfg->H * B;
+  out->retain_count = (int32_t)k.k;
+  out->norm_k = cfg->retain_permille > 0 ? LHB * k.n * 4 : 0;
+  out->ret_idx = LHB * k.k * 4;
+  out->ret_k = (uint64_t)k.uk * B * k.k * D * 2;
+  out->ret_v = (uint64_t)k.uv * B * k.k * D * 2;
   return ok();
 }
 
@@ -219,6 +232,10 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
       {pk->codes_v, z.codes_v, 16, "codes_v"},
       {pk->meta_v, z.meta_v, 16, "meta_v"},
       {pk->side_v, z.side_v, 16, "side_v"},
+      {pk->norm_k, quantize ? z.norm_k : 0, 16, "norm_k"},  // dequantize does not read it
+      {pk->ret_idx, z.ret_idx, 16, "ret_idx"},
+      {pk->ret_k, z.ret_k, 16, "ret_k"},
+      {pk->ret_v, z.ret_v, 16, "ret_v"},
   };
   s = check_device();
   if (s) return s;
@@ -236,14 +253,24 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
   p.meta[1] = (uint32_t*)pk->meta_v;
   p.side[0] = (uint16_t*)pk->side_k;
   p.side[1] = (uint16_t*)pk->side_v;
+  const bool retain = cfg->retain_permille > 0;
+  p.norm = retain && quantize ? (float*)pk->norm_k : nullptr;
+  p.ret_idx = (int32_t*)pk->ret_idx;
+  p.ret[0] = (uint16_t*)pk->ret_k;
+  p.ret[1] = (uint16_t*)pk->ret_v;
+  p.k = z.retain_count;
+  p.out[0] = quantize ? nullptr : (uint16_t*)K;
+  p.out[1] = quantize ? nullptr : (uint16_t*)V;
   const uint64_t slices = (uint64_t)cfg->L * cfg->B * cfg->H;
   const uint64_t blocks_k = slices * (uint64_t)p.tiles;
   if (2 * blocks_k > 0x7FFFFFFFull)
     return fail(HG_ERR_SHAPE, "grid of %llu workgroups too large", (unsigned long long)(2 * blocks_k));
   p.blocks_k = (uint32_t)blocks_k;
-  hipError_t e = quantize ? hg::launch_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream)
+  hipError_t e = quantize ? hg::launch_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), retain, stream)
                           : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream);
   if (e == hipSuccess && quantize && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, false, stream);
+  if (e == hipSuccess && p.k > 0)
+    e = quantize ? hg::launch_retain_select(p, cfg->D, stream) : hg::launch_retain_scatter(p, cfg->D, stream);
   if (e != hipSuccess) return fail(HG_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }
@@ -277,8 +304,39 @@ int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
   if (2 * blocks_k > 0x7FFFFFFFull)
     return fail(HG_ERR_SHAPE, "grid of %llu workgroups too large", (unsigned long long)(2 * blocks_k));
   p.blocks_k = (uint32_t)blocks_k;
-  hipError_t e = hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream);
+
+  // Token retention: the norms, the selection and a copy of the retained rows
+  // go to a stream-ordered workspace before the outputs (possibly the inputs)
+  // are overwritten; the rows are written back last.
+  hg_sizes z;
+  hg_packed_sizes(cfg, mask, &z);
+  void* ws = nullptr;
+  hipError_t e = hipSuccess;
+  if (z.retain_count > 0) {
+    auto up = [](uint64_t b) { return (b + 255) & ~(uint64_t)255; };
+    const uint64_t o_idx = up(z.norm_k), o_k = o_idx + up(z.ret_idx), o_v = o_k + up(z.ret_k);
+    e = hipMallocAsync(&ws, o_v + up(z.ret_v), stream);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(HG_ERR_HIP, "workspace of %llu bytes: %s", (unsigned long long)(o_v + up(z.ret_v)),
+                  hipGetErrorString(e));
+    }
+    char* w = (char*)ws;
+    p.norm = (float*)w;
+    p.ret_idx = (int32_t*)(w + o_idx);
+    p.ret[0] = (uint16_t*)(w + o_k);
+    p.ret[1] = (uint16_t*)(w + o_v);
+    p.k = z.retain_count;
+    e = hg::launch_key_norms(p, cfg->D, stream);
+    if (e == hipSuccess) e = hg::launch_retain_select(p, cfg->D, stream);
+  }
+  if (e == hipSuccess) e = hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream);
   if (e == hipSuccess && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, true, stream);
+  if (e == hipSuccess && p.k > 0) e = hg::launch_retain_scatter(p, cfg->D, stream);
+  if (ws) {
+    const hipError_t f = hipFreeAsync(ws, stream);
+    if (e == hipSuccess) e = f;
+  }
   if (e != hipSuccess) return fail(HG_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

@@ -247,6 +247,49 @@ __device__ __forceinline__ void fwht_row(float (&x)[8], int c) {
   for (int e = 0; e < 8; ++e) x[e] = __builtin_fmaf(x[e], cs, 0.0f);
 }
 
+// ------------------------------------------------------ squared key norms
+
+// Squared L2 norm in fp32 as a balanced tree over channel index: the squares,
+// then sums of adjacent pairs, of adjacent pairs of those, and so on.  A lane
+// reduces its own aligned block of N channels in registers; lanes holding
+// adjacent blocks then combine through exchanges with lane ^ 1, lane ^ 2, ...,
+// so every node is the sum of the same two halves as in the plain tree.  IEEE
+// addition commutes, so both partners of an exchange hold the same sum.
+template <int N>
+__device__ __forceinline__ float tree_sqnorm(const float (&x)[N]) {
+  float a[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) a[e] = x[e] * x[e];
+#pragma unroll
+  for (int w = N / 2; w >= 1; w /= 2) {
+#pragma unroll
+    for (int i = 0; i < w; ++i) a[i] = a[2 * i] + a[2 * i + 1];
+  }
+  return a[0];
+}
+
+// A token held by a quad, lane j holding channels [j*E, (j+1)*E).
+template <int E>
+__device__ __forceinline__ float quad_sqnorm(const float (&x)[E]) {
+  float s = tree_sqnorm<E>(x);
+  s = s + quad_swap<kQuadXor1>(s);
+  return s + quad_swap<kQuadXor2>(s);
+}
+
+// A token held by a row of D/8 lanes, lane c holding channels [8c, 8c + 8)
+// as one 16-byte vector of BF16.
+template <int D>
+__device__ __forceinline__ float row_sqnorm(u32x4 v) {
+  const float x[8] = {bf16_lo(v.x), bf16_hi(v.x), bf16_lo(v.y), bf16_hi(v.y),
+                      bf16_lo(v.z), bf16_hi(v.z), bf16_lo(v.w), bf16_hi(v.w)};
+  float s = tree_sqnorm<8>(x);
+  s = s + row_xor<1>(s);
+  s = s + row_xor<2>(s);
+  s = s + row_xor<4>(s);
+  if constexpr (D == 128) s = s + row_xor<8>(s);
+  return s;
+}
+
 // BF16 round-to-nearest-even of two fp32 values, packed low/high, by the
 // hardware conversion (v_cvt_pk_bf16_f32).
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));

@@ -42,18 +42,30 @@ struct Params {
   int32_t ngroups;           // KIVI key groups per slice
   int32_t tiles;             // kBlockTokens tiles per slice
   uint32_t blocks_k;         // blocks of tensor K
+  // AKVQ-style token retention
+  float* norm;               // [L][B][H][n] squared key norms
+  int32_t* ret_idx;          // [L][B][H][k] retained tokens, ascending
+  uint16_t* ret[2];          // [slot][B][k][D] retained rows of K, V
+  int32_t k;                 // retained tokens per (l, b, h)
   Route route;
 };
 
 // Dispatch over (base, D, bits); return hipSuccess or the launch error.
+// With `norms`, the quantize kernel also writes the squared key norms (AKVQ).
 hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
-                           hipStream_t stream);
+                           bool norms, hipStream_t stream);
 hipError_t launch_dequantize(const Params& p, int base, int D, int bits, uint32_t blocks,
                              hipStream_t stream);
 hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
                                 hipStream_t stream);
 // KIVI keys over the whole sequence: one workgroup per key slice.
 hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, hipStream_t stream);
+// Token retention: squared key norms of every image token (p.norm); the k
+// largest per (l, b, h) into p.ret_idx with their rows gathered from
+// p.cache into p.ret; the retained rows written back from p.ret into p.out.
+hipError_t launch_key_norms(const Params& p, int D, hipStream_t stream);
+hipError_t launch_retain_select(const Params& p, int D, hipStream_t stream);
+hipError_t launch_retain_scatter(const Params& p, int D, hipStream_t stream);
 
 // Routing of one (tensor, slice): whether it is kept in BF16 and its slot in
 // the packed buffers (rank among kept heads if kept, else among quantized

@@ -18,6 +18,8 @@
 //  - AKVQ keys: the normalized Walsh-Hadamard rotation runs on the quad before
 //    the range reduction: spans 1..D/8 in registers, D/4 and D/2 by DPP.
 //  - Protected slices: 16-byte copies of the image rows to the side store.
+//  - AKVQ-style token retention: the same pass also writes the squared norm of
+//    every image key (quad or row tree, see tree_sqnorm), before any rotation.
 // All per-group arithmetic is IEEE fp32 (no contraction), the same operations
 // in the same order as the reference definition.
 
@@ -28,10 +30,11 @@ namespace hg {
 
 // ---------------------------------------------------------- per-token path
 
-template <int D, int BITS, bool ROTATE>
+template <int D, int BITS, bool ROTATE, bool NORM>
 __device__ __forceinline__ void quantize_tokens(const uint16_t* __restrict__ rows,
                                                 uint8_t* __restrict__ codes,
                                                 uint32_t* __restrict__ meta,
+                                                float* __restrict__ norm,
                                                 int t_first, int n, int lane) {
   constexpr int E = D / 4;             // elements per lane
   constexpr int NV = E / 8;            // 16-byte loads per lane per token
@@ -66,6 +69,10 @@ __device__ __forceinline__ void quantize_tokens(const uint16_t* __restrict__ row
       x[8 * k + 5] = bf16_hi(raw[pass][k].z);
       x[8 * k + 6] = bf16_lo(raw[pass][k].w);
       x[8 * k + 7] = bf16_hi(raw[pass][k].w);
+    }
+    if constexpr (NORM) {
+      const float sq = quad_sqnorm<E>(x);
+      if (t < n && j == 0) __builtin_nontemporal_store(sq, norm + t);
     }
     if constexpr (ROTATE) fwht_quad<E>(x, j, fwht_scale<D>());
 
@@ -157,9 +164,9 @@ __device__ __forceinline__ void quantize_kivi_keys(const uint16_t* __restrict__ 
 
 // ---------------------------------------------------------- protected copy
 
-template <int D>
+template <int D, bool NORM>
 __device__ __forceinline__ void copy_rows(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
-                                          int t_first, int n, int lane) {
+                                          float* __restrict__ norm, int t_first, int n, int lane) {
   constexpr int VPT = D / 8;  // 16-byte vectors per token
   const int ntok = min(kWaveTokens, n - t_first);
   const int nvec = ntok * VPT;
@@ -174,11 +181,20 @@ __device__ __forceinline__ void copy_rows(const uint16_t* __restrict__ src, uint
     const int i = lane + 64 * k;
     if (i < nvec) store_nt(d + i, v[k]);
   }
+  if constexpr (NORM) {
+    // vector i holds channels [8c, 8c + 8) of token i / VPT, c = i % VPT
+#pragma unroll
+    for (int k = 0; k < kMax; ++k) {
+      const float sq = row_sqnorm<D>(v[k]);
+      const int i = lane + 64 * k;
+      if (i < nvec && i % VPT == 0) __builtin_nontemporal_store(sq, norm + t_first + i / VPT);
+    }
+  }
 }
 
 // ---------------------------------------------------------------- kernel
 
-template <int BASE, int D, int BITS>
+template <int BASE, int D, int BITS, bool NORM>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWaves))) void quantize_kernel(const Params p) {
   const Slice sl = decode_block(p, blockIdx.x);
   const int lane = threadIdx.x & 63;
@@ -189,8 +205,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
   const uint16_t* rows = p.cache[sl.X] + ((size_t)sl.s * p.T + p.s0) * D;
   const size_t slab = (size_t)sl.slot * p.B + sl.b;  // [slot][B]
 
+  float* norm = NORM ? p.norm + (size_t)sl.s * p.n : nullptr;  // used for K only
   if (sl.kept) {
-    copy_rows<D>(rows, p.side[sl.X] + slab * p.n * D, t_first, p.n, lane);
+    if (NORM && sl.X == 0)
+      copy_rows<D, NORM>(rows, p.side[0] + slab * p.n * D, norm, t_first, p.n, lane);
+    else
+      copy_rows<D, false>(rows, p.side[sl.X] + slab * p.n * D, nullptr, t_first, p.n, lane);
     return;
   }
   uint8_t* codes = p.codes[sl.X] + slab * p.n * (D * BITS / 8);
@@ -201,43 +221,51 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
   } else {
     uint32_t* meta = p.meta[sl.X] + slab * p.n;
     if (BASE == HG_BASE_AKVQ && sl.X == 0)
-      quantize_tokens<D, BITS, true>(rows, codes, meta, t_first, p.n, lane);
+      quantize_tokens<D, BITS, true, NORM>(rows, codes, meta, norm, t_first, p.n, lane);
     else
-      quantize_tokens<D, BITS, false>(rows, codes, meta, t_first, p.n, lane);
+      quantize_tokens<D, BITS, false, false>(rows, codes, meta, nullptr, t_first, p.n, lane);
   }
 }
 
 template <int BASE, int D, int BITS>
-static hipError_t launch_q(const Params& p, uint32_t blocks, hipStream_t stream) {
-  hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS>), dim3(blocks), dim3(kThreads), 0, stream, p);
+static hipError_t launch_q(const Params& p, uint32_t blocks, bool norms, hipStream_t stream) {
+  if constexpr (BASE == HG_BASE_AKVQ) {
+    if (norms) {
+      hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, true>), dim3(blocks), dim3(kThreads), 0, stream, p);
+      return hipGetLastError();
+    }
+  }
+  if (norms) return hipErrorInvalidValue;  // key norms belong to the AKVQ base
+  hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, false>), dim3(blocks), dim3(kThreads), 0, stream, p);
   return hipGetLastError();
 }
 
 template <int BASE, int D>
-static hipError_t launch_q_bits(const Params& p, int bits, uint32_t blocks, hipStream_t stream) {
+static hipError_t launch_q_bits(const Params& p, int bits, uint32_t blocks, bool norms, hipStream_t stream) {
   switch (bits) {
-    case 2: return launch_q<BASE, D, 2>(p, blocks, stream);
-    case 3: return launch_q<BASE, D, 3>(p, blocks, stream);
-    case 4: return launch_q<BASE, D, 4>(p, blocks, stream);
+    case 2: return launch_q<BASE, D, 2>(p, blocks, norms, stream);
+    case 3: return launch_q<BASE, D, 3>(p, blocks, norms, stream);
+    case 4: return launch_q<BASE, D, 4>(p, blocks, norms, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int BASE>
-static hipError_t launch_q_dim(const Params& p, int D, int bits, uint32_t blocks, hipStream_t stream) {
+static hipError_t launch_q_dim(const Params& p, int D, int bits, uint32_t blocks, bool norms,
+                               hipStream_t stream) {
   switch (D) {
-    case 64: return launch_q_bits<BASE, 64>(p, bits, blocks, stream);
-    case 128: return launch_q_bits<BASE, 128>(p, bits, blocks, stream);
+    case 64: return launch_q_bits<BASE, 64>(p, bits, blocks, norms, stream);
+    case 128: return launch_q_bits<BASE, 128>(p, bits, blocks, norms, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
+hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t blocks, bool norms,
                            hipStream_t stream) {
   switch (base) {
-    case HG_BASE_MINMAX: return launch_q_dim<HG_BASE_MINMAX>(p, D, bits, blocks, stream);
-    case HG_BASE_KIVI: return launch_q_dim<HG_BASE_KIVI>(p, D, bits, blocks, stream);
-    case HG_BASE_AKVQ: return launch_q_dim<HG_BASE_AKVQ>(p, D, bits, blocks, stream);
+    case HG_BASE_MINMAX: return launch_q_dim<HG_BASE_MINMAX>(p, D, bits, blocks, norms, stream);
+    case HG_BASE_KIVI: return launch_q_dim<HG_BASE_KIVI>(p, D, bits, blocks, norms, stream);
+    case HG_BASE_AKVQ: return launch_q_dim<HG_BASE_AKVQ>(p, D, bits, blocks, norms, stream);
     default: return hipErrorInvalidValue;
   }
 }

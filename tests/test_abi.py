@@ -60,6 +60,8 @@ def test_sizes_match_oracle(seed):
     f = _cfg(L=L, B=int(rng.integers(1, 5)), H=H, T=T, D=int(rng.choice([64, 128])),
              img_start=s0, img_len=int(rng.integers(0, T - s0 + 1)), bits=int(rng.integers(2, 5)),
              base=int(rng.integers(0, 3)), keys_only=int(rng.integers(0, 2)))
+    if f["base"] == 2:
+        f["retain_permille"] = int(rng.choice([0, 20, 100, 1000]))
     mask = (rng.random(L * H) < 0.2).astype(np.uint8)
     got = hg.hg_packed_sizes(hg.make_config(**f), mask)
     want = oracle.sizes(oracle.make_config(**f), mask)
@@ -85,6 +87,8 @@ BAD = [
     (dict(img_len=-3), hg.HG_ERR_SPAN),
     (dict(bits=1), hg.HG_ERR_BITS), (dict(bits=5), hg.HG_ERR_BITS),
     (dict(base=3), hg.HG_ERR_BASE), (dict(base=1, kivi_group=16), hg.HG_ERR_BASE),
+    (dict(retain_permille=20), hg.HG_ERR_BASE), (dict(base=1, retain_permille=20), hg.HG_ERR_BASE),
+    (dict(base=2, retain_permille=1001), hg.HG_ERR_BASE), (dict(base=2, retain_permille=-1), hg.HG_ERR_BASE),
 ]
 
 
