@@ -6,12 +6,12 @@
 // same pass that reads the keys (key_norm_kernel does it on its own for the
 // one-pass simulated quantization, whose in-place outputs would otherwise
 // overwrite the rows to keep).  Then, per (l, b, h):
-//  - retain_select_kernel finds the k-th largest norm by a most-significant-
-//    digit-first radix select over the fp32 bit patterns (non-negative, so they
-//    order as unsigned integers), lists the retained tokens in ascending order
-//    (all larger norms, then the lowest-index ties), and gathers their K and V
-//    rows for each tensor the head does not keep in BF16;
-//  - retain_scatter_kernel writes those rows back over the reconstruction.
+//  - retain_select_kernel (norms staged in LDS) finds the k-th largest norm by
+//    a most-significant-digit-first radix select over the fp32 bit patterns
+//    (non-negative, so they order as unsigned integers) and lists the retained
+//    tokens in ascending order (all larger norms, then the lowest-index ties);
+//  - retain_rows_kernel gathers their K and V rows for each tensor the head
+//    does not keep in BF16, or writes them back over the reconstruction.
 
 #include "hg_device.h"
 #include "hg_kernels.h"
@@ -51,32 +51,35 @@ __global__ __launch_bounds__(kThreads) void key_norm_kernel(const Params p) {
 
 // ------------------------------------------------------------ selection
 
-// Copies rows sel[0..m) of one tensor's image span to rows base.. of dst.
-template <int D>
-__device__ __forceinline__ void gather_rows(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
-                                            const int32_t* sel, uint32_t m, uint32_t base) {
-  constexpr int VPT = D / 8;
-  for (uint32_t i = threadIdx.x; i < m * VPT; i += kThreads) {
-    const uint32_t row = i / VPT, c = i % VPT;
-    const u32x4 v = *(const u32x4*)(src + (size_t)sel[row] * D + 8 * c);
-    store_nt((u32x4*)(dst + (size_t)(base + row) * D + 8 * c), v);
-  }
-}
+// Keys held in LDS by the selection when the span fits this many tokens;
+// longer spans read them from global memory (L2) in every pass.
+constexpr int kResidentKeys = 12288;
 
-// One workgroup per (l, b, h); requires 1 <= k <= n.
-template <int D>
+// One workgroup per (l, b, h); requires 1 <= k <= n.  Writes ret_idx only.
+template <bool RESIDENT>
 __global__ __launch_bounds__(kThreads) void retain_select_kernel(const Params p) {
   constexpr int WAVES = kThreads / 64;
+  extern __shared__ uint32_t lds_keys[];  // n keys when RESIDENT
   __shared__ uint32_t hist[256];
   __shared__ uint32_t pick[2];
-  __shared__ uint32_t wcount[WAVES][2];
-  __shared__ int32_t sel[kThreads];
+  __shared__ uint32_t wsum[WAVES][2];
 
   const uint32_t s = blockIdx.x;  // (l*B + b)*H + h
   const int n = p.n;
   const uint32_t k = (uint32_t)p.k;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const uint32_t* key = (const uint32_t*)(p.norm + (size_t)s * n);
+  const uint32_t* gkeys = (const uint32_t*)(p.norm + (size_t)s * n);
+  if constexpr (RESIDENT) {
+    for (int t0 = tid; t0 < n; t0 += 4 * kThreads) {
+      uint32_t u[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) u[i] = gkeys[min(t0 + i * kThreads, n - 1)];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (t0 + i * kThreads < n) lds_keys[t0 + i * kThreads] = u[i];
+    }
+  }
+  const uint32_t* key = RESIDENT ? lds_keys : gkeys;
 
   // 1. The k-th largest key: one 8-bit digit per pass from the top.  `want` is
   //    how many of the candidates sharing `prefix` are still to be taken.
@@ -121,78 +124,90 @@ __global__ __launch_bounds__(kThreads) void retain_select_kernel(const Params p)
   const uint32_t thr = prefix;  // the k-th largest key
   const uint32_t need = want;   // keys equal to thr that are retained (lowest indices)
 
-  // 2. Retained tokens in ascending order: position of a retained token =
-  //    (larger keys before it) + min(equal keys before it, need).
-  const SliceRoute rk = route_slice(p, 0, s), rv = route_slice(p, 1, s);
-  const uint16_t* src_k = p.cache[0] + ((size_t)s * p.T + p.s0) * D;
-  const uint16_t* src_v = p.cache[1] + ((size_t)s * p.T + p.s0) * D;
-  uint16_t* dst_k = rk.kept ? nullptr : p.ret[0] + ((size_t)rk.slot * p.B + rk.b) * k * D;
-  uint16_t* dst_v = rv.kept ? nullptr : p.ret[1] + ((size_t)rv.slot * p.B + rv.b) * k * D;
-  int32_t* idx = p.ret_idx + (size_t)s * k;
-  const uint64_t below = (1ull << lane) - 1ull;
-  uint32_t carry_gt = 0, carry_eq = 0;
-  for (int c0 = 0; c0 < n; c0 += kThreads) {
-    const int t = c0 + tid;
-    const uint32_t u = t < n ? key[t] : 0u;
-    const bool gt = t < n && u > thr;
-    const bool eq = t < n && u == thr;
-    const uint64_t bg = __ballot(gt), be = __ballot(eq);
-    if (lane == 0) {
-      wcount[wave][0] = (uint32_t)__popcll(bg);
-      wcount[wave][1] = (uint32_t)__popcll(be);
-    }
-    __syncthreads();
-    uint32_t pg = carry_gt + (uint32_t)__popcll(bg & below);
-    uint32_t pe = carry_eq + (uint32_t)__popcll(be & below);
-    uint32_t tg = 0, te = 0;
+  // 2. Retained tokens in ascending order.  Each thread owns a contiguous run
+  //    of tokens; a block-wide exclusive scan of the per-run counts of larger
+  //    and equal keys gives every run its starting counts, and the position of
+  //    a retained token is (larger keys before it) + min(equal keys before it,
+  //    need).
+  const int run = (n + kThreads - 1) / kThreads;
+  const int t_lo = min(tid * run, n), t_hi = min(t_lo + run, n);
+  uint32_t cg = 0, ce = 0;
+  for (int t = t_lo; t < t_hi; ++t) {
+    const uint32_t u = key[t];
+    cg += u > thr;
+    ce += u == thr;
+  }
+  uint32_t ig = cg, ie = ce;  // inclusive scans within the wavefront
 #pragma unroll
-    for (int w = 0; w < WAVES; ++w) {
-      if (w < wave) {
-        pg += wcount[w][0];
-        pe += wcount[w][1];
-      }
-      tg += wcount[w][0];
-      te += wcount[w][1];
+  for (int off = 1; off < 64; off *= 2) {
+    const uint32_t yg = __shfl_up(ig, off), ye = __shfl_up(ie, off);
+    if (lane >= off) {
+      ig += yg;
+      ie += ye;
     }
-    const uint32_t base = carry_gt + min(carry_eq, need);
+  }
+  if (lane == 63) {
+    wsum[wave][0] = ig;
+    wsum[wave][1] = ie;
+  }
+  __syncthreads();
+  uint32_t pg = ig - cg, pe = ie - ce;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    if (w < wave) {
+      pg += wsum[w][0];
+      pe += wsum[w][1];
+    }
+  }
+  int32_t* idx = p.ret_idx + (size_t)s * k;
+  for (int t = t_lo; t < t_hi; ++t) {
+    const uint32_t u = key[t];
+    const bool gt = u > thr, eq = u == thr;
     const uint32_t pos = pg + min(pe, need);
-    if ((gt || (eq && pe < need)) && pos < k) {  // exactly k positions are taken
-      idx[pos] = t;
-      sel[pos - base] = t;
-    }
-    carry_gt += tg;
-    carry_eq += te;
-    // retained in this chunk (the bound only guards the buffers)
-    const uint32_t m = min(carry_gt + min(carry_eq, need), k) - min(base, k);
-    __syncthreads();
-    if (m > 0) {
-      if (dst_k) gather_rows<D>(src_k, dst_k, sel, m, base);
-      if (dst_v) gather_rows<D>(src_v, dst_v, sel, m, base);
-    }
+    if ((gt || (eq && pe < need)) && pos < k) idx[pos] = t;  // exactly k positions are taken
+    pg += gt;
+    pe += eq;
   }
 }
 
-// ------------------------------------------------------------ write-back
+// ------------------------------------------------------------ retained rows
 
-// One workgroup per (l, b, h): the retained rows over p.out's image span.
-template <int D>
-__global__ __launch_bounds__(kThreads) void retain_scatter_kernel(const Params p) {
-  constexpr int VPT = D / 8;
+// Grid (l*B*H, 2): one workgroup per (l, b, h) and tensor, skipping tensors the
+// head keeps in BF16.  GATHER copies the retained image rows of p.cache into
+// p.ret; otherwise p.ret is written back over p.out's image rows.
+template <int D, bool GATHER>
+__global__ __launch_bounds__(kThreads) void retain_rows_kernel(const Params p) {
+  constexpr int VPT = D / 8;  // 16-byte vectors per row
+  constexpr int U = 4;        // vectors in flight per thread
   const uint32_t s = blockIdx.x;
+  const int X = blockIdx.y;
+  const SliceRoute r = route_slice(p, X, s);
+  if (r.kept) return;
   const uint32_t k = (uint32_t)p.k;
   const int32_t* idx = p.ret_idx + (size_t)s * k;
+  uint16_t* ret = p.ret[X] + ((size_t)r.slot * p.B + r.b) * k * D;
+  const size_t span = ((size_t)s * p.T + p.s0) * D;
+  const uint32_t total = k * VPT;
+  for (uint32_t i0 = threadIdx.x; i0 < total; i0 += U * kThreads) {
+    u32x4 v[U];
+    uint32_t tok[U];
 #pragma unroll
-  for (int X = 0; X < 2; ++X) {
-    const SliceRoute r = route_slice(p, X, s);
-    if (r.kept) continue;
-    const uint16_t* src = p.ret[X] + ((size_t)r.slot * p.B + r.b) * k * D;
-    uint16_t* dst = p.out[X] + ((size_t)s * p.T + p.s0) * D;
-    for (uint32_t i = threadIdx.x; i < k * VPT; i += kThreads) {
+    for (int u = 0; u < U; ++u) {
+      const uint32_t i = min(i0 + u * kThreads, total - 1);
       const uint32_t row = i / VPT, c = i % VPT;
-      const uint32_t t = (uint32_t)idx[row];
-      if (t >= (uint32_t)p.n) continue;  // not a token of the span: never written
-      const u32x4 v = *(const u32x4*)(src + (size_t)row * D + 8 * c);
-      store_nt((u32x4*)(dst + (size_t)t * D + 8 * c), v);
+      tok[u] = (uint32_t)idx[row];
+      const uint32_t t = min(tok[u], (uint32_t)p.n - 1);  // an out-of-span entry is not stored
+      v[u] = GATHER ? *(const u32x4*)(p.cache[X] + span + (size_t)t * D + 8 * c)
+                    : *(const u32x4*)(ret + (size_t)row * D + 8 * c);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t i = i0 + u * kThreads;
+      if (i >= total || tok[u] >= (uint32_t)p.n) continue;
+      const uint32_t row = i / VPT, c = i % VPT;
+      u32x4* dst = GATHER ? (u32x4*)(ret + (size_t)row * D + 8 * c)
+                          : (u32x4*)(p.out[X] + span + (size_t)tok[u] * D + 8 * c);
+      store_nt(dst, v[u]);
     }
   }
 }
@@ -210,26 +225,31 @@ hipError_t launch_key_norms(const Params& p, int D, hipStream_t stream) {
   return hipGetLastError();
 }
 
-hipError_t launch_retain_select(const Params& p, int D, hipStream_t stream) {
-  const uint32_t blocks = (uint32_t)p.L * p.B * p.H;
+template <bool GATHER>
+static hipError_t launch_rows(const Params& p, int D, hipStream_t stream) {
+  const dim3 grid((uint32_t)p.L * p.B * p.H, 2);
   if (D == 64)
-    hipLaunchKernelGGL((retain_select_kernel<64>), dim3(blocks), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL((retain_rows_kernel<64, GATHER>), grid, dim3(kThreads), 0, stream, p);
   else if (D == 128)
-    hipLaunchKernelGGL((retain_select_kernel<128>), dim3(blocks), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL((retain_rows_kernel<128, GATHER>), grid, dim3(kThreads), 0, stream, p);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-hipError_t launch_retain_scatter(const Params& p, int D, hipStream_t stream) {
+hipError_t launch_retain_select(const Params& p, int D, hipStream_t stream) {
   const uint32_t blocks = (uint32_t)p.L * p.B * p.H;
-  if (D == 64)
-    hipLaunchKernelGGL((retain_scatter_kernel<64>), dim3(blocks), dim3(kThreads), 0, stream, p);
-  else if (D == 128)
-    hipLaunchKernelGGL((retain_scatter_kernel<128>), dim3(blocks), dim3(kThreads), 0, stream, p);
+  if (p.n <= kResidentKeys)
+    hipLaunchKernelGGL((retain_select_kernel<true>), dim3(blocks), dim3(kThreads),
+                       (size_t)p.n * sizeof(uint32_t), stream, p);
   else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+    hipLaunchKernelGGL((retain_select_kernel<false>), dim3(blocks), dim3(kThreads), 0, stream, p);
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? launch_rows<true>(p, D, stream) : e;
+}
+
+hipError_t launch_retain_scatter(const Params& p, int D, hipStream_t stream) {
+  return launch_rows<false>(p, D, stream);
 }
 
 }  // namespace hg

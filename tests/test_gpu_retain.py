@@ -48,6 +48,16 @@ def test_ragged_spans_and_fractions(img_len, permille):
     _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), w.name)
 
 
+@pytest.mark.parametrize("img_len", [12288, 12289, 13000])
+def test_long_spans(img_len):
+    """Spans at and past the length whose norms the selection stages in LDS;
+    longer ones are selected from global memory."""
+    w = retain_case(img_len=img_len, img_start=5, text=3, L=1, B=1, H=2, n_protected=0,
+                    permille=20)
+    K, V = synthkv.gen_kv(w)
+    _assert_exact(compare_full(w, K, V, np.zeros(w.L * w.H, np.uint8)), w.name)
+
+
 def _integer_kv(w, lo, hi, seed):
     g = torch.Generator().manual_seed(seed)
     shape = (w.L, w.B, w.H, w.T, w.D)
