@@ -91,14 +91,14 @@ def algorithmic_bytes(w, sizes) -> dict:
             "read": read, "write": write}
 
 
-def cpu_baseline(w, K, V, mask, budget_s: float):
+def cpu_baseline(w, K, V, mask, budget_s: float, threads: int = 0):
     """The CPU oracle on a bounded sample of the same workload, quantize then
     dequantize: whole passes over the cache, repeated to fill about budget_s
     of wall time, or its first layers (all rows, heads, K and V) when one pass
-    would exceed the budget."""
+    would exceed the budget.  threads = 0: one per host core, at most 16."""
     import oracle  # test infrastructure: the CPU baseline leg only
     import synthkv
-    threads = max(1, min(os.cpu_count() or 1, 16))
+    threads = threads or max(1, min(os.cpu_count() or 1, 16))
 
     def prepare(nl):
         sub = w.with_(L=nl)
@@ -263,16 +263,25 @@ def main():
                    "parallelism": "single GPU"},
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "image_tokens_per_s": round(w.B * w.img_len * args.steps / elapsed, 1),
-        "quantize": {"ms": round(q_avg, 4), "GBps": round(q_gbps, 1),
-                     "bytes": ab["quant"], "image_tokens_per_s": round(w.B * w.img_len / (q_avg * 1e-3), 1)},
+        "quantize": {"ms": round(q_avg, 4), "median_ms": round(float(np.median(q_ms)), 4),
+                     "min_ms": round(float(np.min(q_ms)), 4), "GBps": round(q_gbps, 1),
+                     "bytes": ab["quant"], "image_tokens_per_s": round(w.B * w.img_len / (q_avg * 1e-3), 1),
+                     "token_vectors_per_s": round(2 * w.L * w.B * w.H * w.img_len / (q_avg * 1e-3), 1)},
         "dequantize": None if args.quant_only else
-                      {"ms": round(d_avg, 4), "GBps": round(d_gbps, 1), "bytes": ab["dequant"]},
+                      {"ms": round(d_avg, 4), "median_ms": round(float(np.median(d_ms)), 4),
+                       "min_ms": round(float(np.min(d_ms)), 4), "GBps": round(d_gbps, 1),
+                       "bytes": ab["dequant"]},
         "roofline": {"bound": "hbm", "kernel": QUANT_KERNEL, "achieved": round(q_gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(q_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": traffic},
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, K, V, mask, args.cpu_seconds)
+        cb = cpu_baseline(w, K, V, mask, args.cpu_seconds)
+        one = cpu_baseline(w, K, V, mask, args.cpu_seconds / 2, threads=1)
+        cb["single_thread"] = {"value": one["value"], "unit": one["unit"], "sample": one["sample"]}
+        cb["gpu_speedup"] = round(value / cb["value"], 1)
+        cb["gpu_speedup_vs_single_thread"] = round(value / one["value"], 1)
+        out["cpu_baseline"] = cb
     print(json.dumps(out), flush=True)
 
 

@@ -26,6 +26,7 @@ STATUS = ("HG_OK", "HG_ERR_NULL", "HG_ERR_SHAPE", "HG_ERR_SPAN", "HG_ERR_BITS", 
           "HG_ERR_POINTER", "HG_ERR_VALUE")
 for _i, _n in enumerate(STATUS):
     globals()[_n] = _i
+HG_MAX_HEADS = 8192  # largest L*H the routing holds (headguard.h)
 BUFFERS = ("codes_k", "meta_k", "side_k", "codes_v", "meta_v", "side_v",
            "norm_k", "ret_idx", "ret_k", "ret_v")
 

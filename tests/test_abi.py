@@ -38,6 +38,13 @@ def test_every_declared_symbol_is_exported():
     assert set(names) <= exported
 
 
+def test_binding_constants_match_the_header():
+    text = open(HEADER).read()
+    assert int(re.search(r"#define HG_MAX_HEADS (\d+)", text).group(1)) == hg.HG_MAX_HEADS
+    for i, name in enumerate(hg.STATUS[1:], start=1):
+        assert re.search(rf"\b{name} = {i}\b", text), name
+
+
 def test_status_strings():
     for i, name in enumerate(hg.STATUS):
         assert hg.hg_status_string(i) == name

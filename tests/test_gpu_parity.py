@@ -73,6 +73,23 @@ def test_degenerate_masks(base, which, keys_only):
     _assert_exact(rep, f"{base}-{which}")
 
 
+@pytest.mark.parametrize("base,keys_only,retain", [("minmax", 0, 0), ("kivi", 1, 0), ("akvq", 0, 100)])
+def test_maximum_head_count(base, keys_only, retain):
+    """L*H at the routing limit (8192 heads): the mask bitmap and its prefix
+    counts span every word; protected heads sit in the first and last words."""
+    import paper_2609_35800_amd as hg
+    w = synthkv.Workload(f"maxheads-{base}", L=128, B=1, H=64, T=40, D=64, img_start=3,
+                         img_len=33, bits=3, base=base, keys_only=keys_only, n_protected=0,
+                         k_outliers=2, k_outlier_scale=10.0, kivi_group=32, retain_permille=retain)
+    assert w.L * w.H == hg.HG_MAX_HEADS
+    rng = np.random.default_rng(8192)
+    mask = (rng.random(w.L * w.H) < 0.125).astype(np.uint8)
+    mask[[0, 31, 32, 8191]] = 1
+    mask[8190] = 0
+    K, V = synthkv.gen_kv(w)
+    _assert_exact(compare_full(w, K, V, mask), w.name)
+
+
 def _special_values(w, K, V):
     """Plant constant tokens, signed zeros, tiny ranges, ties and large values."""
     s = w.img_start
