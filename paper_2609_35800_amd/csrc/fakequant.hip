@@ -49,7 +49,10 @@ __device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out,
     for (int k = 0; k < NV; ++k) raw[pass][k] = src[k];
   }
 
-#pragma unroll 1
+  // Rotated keys unroll both passes: rolled, their per-pass register arrays
+  // went to scratch memory.  The plain path is faster rolled (measured).
+  constexpr int kUnrolledPasses = ROTATE ? 2 : 1;
+#pragma unroll kUnrolledPasses
   for (int pass = 0; pass < 2; ++pass) {
     float x[E];
 #pragma unroll

@@ -3,7 +3,8 @@
 // base recomputes key ranges over the supplied sequence, including text,
 // while text KV stays BF16).  Selected by kivi_group = 0.
 //
-// One 256-thread workgroup per key slice (l, b, h):
+// A persistent grid of kSeqBlocksPerCU workgroups of kSeqThreads threads per
+// compute unit walks the key slices (l, b, h); for each slice:
 //  1. per-channel min / max over all T rows of the slice (the load layout
 //     holds a token row across D/8 lanes, 8 channels per lane, so each lane
 //     reduces its 8 channels over its rows in registers);
@@ -14,45 +15,53 @@
 //     quantization, reconstructed to BF16.
 // Values, protected slices and the rest of the cache are handled by the
 // regular kernels of the same call.
+//
+// The second read of a slice's image rows is what makes this mode costlier
+// than the grouped one.  The grid is sized so that the slices in flight at
+// once (one per workgroup, ~770 KB each for a 3000-token slice) stay well
+// within the 256 MB Infinity Cache, so that read is served from it rather
+// than from HBM; large workgroups keep enough loads in flight to stream the
+// first pass at full HBM rate.
+
+#include <algorithm>
 
 #include "hg_device.h"
 #include "hg_kernels.h"
 
 namespace hg {
 
-template <int D, int BITS, bool FAKE>
-__global__ __launch_bounds__(kThreads) void kivi_seq_kernel(const Params p) {
-  constexpr int CPT = D / 8;        // lanes per token row
-  constexpr int RPL = 64 / CPT;     // token rows per load per wavefront
-  constexpr int WAVES = kThreads / 64;
-  constexpr int STEP = WAVES * RPL;  // token rows per workgroup load
+constexpr int kSeqThreads = 1024;
+constexpr int kSeqBlocksPerCU = 2;
+constexpr int kSeqUnroll1 = 4;  // rows in flight per lane, range pass
+constexpr int kSeqUnroll2 = 4;  // rows in flight per lane, code pass
+
+template <int D, int BITS, bool FAKE, int WAVES>
+__device__ __forceinline__ void kivi_seq_slice(const Params& p, uint32_t s, const SliceRoute& route,
+                                               float (&part)[2][WAVES][D]) {
+  constexpr int CPT = D / 8;
+  constexpr int RPL = 64 / CPT;
+  constexpr int STEP = WAVES * RPL;
   constexpr int LEVELS = (1 << BITS) - 1;
   constexpr int ROW = D * BITS / 8;
-  __shared__ float part[2][WAVES][D];
-
-  const uint32_t s = blockIdx.x;  // key slice (l*B + b)*H + h
-  const SliceRoute route = route_slice(p, 0, s);
-  if (route.kept) return;  // whole workgroup: protected keys are copied elsewhere
-
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c8 = lane % CPT;
   const int r = lane / CPT;
   const uint16_t* slice = p.cache[0] + (size_t)s * p.T * D;
 
-  // 1. ranges over all T rows, four rows in flight per lane
+  // 1. ranges over all T rows
   float mn[8], mx[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     mn[e] = __builtin_inff();
     mx[e] = -__builtin_inff();
   }
-  for (int t0 = wave * RPL + r; t0 < p.T; t0 += 4 * STEP) {
-    u32x4 v[4];
+  for (int t0 = wave * RPL + r; t0 < p.T; t0 += kSeqUnroll1 * STEP) {
+    u32x4 v[kSeqUnroll1];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = *(const u32x4*)(slice + (size_t)min(t0 + u * STEP, p.T - 1) * D + 8 * c8);
+    for (int u = 0; u < kSeqUnroll1; ++u) v[u] = *(const u32x4*)(slice + (size_t)min(t0 + u * STEP, p.T - 1) * D + 8 * c8);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < kSeqUnroll1; ++u) {
       // rows past the end re-read the last row: the range is unchanged
       const float x[8] = {bf16_lo(v[u].x), bf16_hi(v[u].x), bf16_lo(v[u].y), bf16_hi(v[u].y),
                           bf16_lo(v[u].z), bf16_hi(v[u].z), bf16_lo(v[u].w), bf16_hi(v[u].w)};
@@ -72,7 +81,9 @@ __global__ __launch_bounds__(kThreads) void kivi_seq_kernel(const Params p) {
     }
   }
 
-  // 2. combine the wavefronts and form the scales
+  // 2. combine the wavefronts and form the scales (the barrier first: the
+  //    previous slice's readers of `part` are done)
+  __syncthreads();
   if (r == 0) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -105,12 +116,12 @@ __global__ __launch_bounds__(kThreads) void kivi_seq_kernel(const Params p) {
   const uint16_t* rows = slice + (size_t)p.s0 * D;
   uint8_t* codes = FAKE ? nullptr : p.codes[0] + slab * p.n * ROW;
   uint16_t* out = FAKE ? p.out[0] + (size_t)s * p.T * D + (size_t)p.s0 * D : nullptr;
-  for (int t0 = wave * RPL + r; t0 < p.n; t0 += 4 * STEP) {
-    u32x4 v[4];
+  for (int t0 = wave * RPL + r; t0 < p.n; t0 += kSeqUnroll2 * STEP) {
+    u32x4 v[kSeqUnroll2];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = *(const u32x4*)(rows + (size_t)min(t0 + u * STEP, p.n - 1) * D + 8 * c8);
+    for (int u = 0; u < kSeqUnroll2; ++u) v[u] = *(const u32x4*)(rows + (size_t)min(t0 + u * STEP, p.n - 1) * D + 8 * c8);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < kSeqUnroll2; ++u) {
       const int t = t0 + u * STEP;
       const float x[8] = {bf16_lo(v[u].x), bf16_hi(v[u].x), bf16_lo(v[u].y), bf16_hi(v[u].y),
                           bf16_lo(v[u].z), bf16_hi(v[u].z), bf16_lo(v[u].w), bf16_hi(v[u].w)};
@@ -132,13 +143,29 @@ __global__ __launch_bounds__(kThreads) void kivi_seq_kernel(const Params p) {
   }
 }
 
+template <int D, int BITS, bool FAKE>
+__global__ __launch_bounds__(kSeqThreads) void kivi_seq_kernel(const Params p) {
+  constexpr int WAVES = kSeqThreads / 64;
+  __shared__ float part[2][WAVES][D];
+  const uint32_t slices = (uint32_t)p.L * p.B * p.H;
+  for (uint32_t s = blockIdx.x; s < slices; s += gridDim.x) {  // key slice (l*B + b)*H + h
+    const SliceRoute route = route_slice(p, 0, s);
+    if (!route.kept) kivi_seq_slice<D, BITS, FAKE, WAVES>(p, s, route, part);  // kept: copied elsewhere
+  }
+}
+
 template <int D, int BITS>
 static hipError_t launch_k(const Params& p, bool fake, hipStream_t stream) {
-  const uint32_t blocks = (uint32_t)p.L * p.B * p.H;
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  const uint32_t slices = (uint32_t)p.L * p.B * p.H;
+  const uint32_t blocks = std::min<uint32_t>(slices, (uint32_t)std::max(cus, 1) * kSeqBlocksPerCU);
   if (fake)
-    hipLaunchKernelGGL((kivi_seq_kernel<D, BITS, true>), dim3(blocks), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL((kivi_seq_kernel<D, BITS, true>), dim3(blocks), dim3(kSeqThreads), 0, stream, p);
   else
-    hipLaunchKernelGGL((kivi_seq_kernel<D, BITS, false>), dim3(blocks), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL((kivi_seq_kernel<D, BITS, false>), dim3(blocks), dim3(kSeqThreads), 0, stream, p);
   return hipGetLastError();
 }
 
