@@ -269,8 +269,11 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
   hipError_t e = quantize ? hg::launch_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), retain, stream)
                           : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream);
   if (e == hipSuccess && quantize && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, false, stream);
-  if (e == hipSuccess && p.k > 0)
-    e = quantize ? hg::launch_retain_select(p, cfg->D, stream) : hg::launch_retain_scatter(p, cfg->D, stream);
+  if (e == hipSuccess && p.k > 0 && quantize) {
+    e = hg::launch_retain_select(p, stream);
+    if (e == hipSuccess) e = hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kGather, stream);
+  }
+  if (e == hipSuccess && p.k > 0 && !quantize) e = hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kScatter, stream);
   if (e != hipSuccess) return fail(HG_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }
@@ -305,34 +308,48 @@ int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
     return fail(HG_ERR_SHAPE, "grid of %llu workgroups too large", (unsigned long long)(2 * blocks_k));
   p.blocks_k = (uint32_t)blocks_k;
 
-  // Token retention: the norms, the selection and a copy of the retained rows
-  // go to a stream-ordered workspace before the outputs (possibly the inputs)
-  // are overwritten; the rows are written back last.
+  // Token retention (a stream-ordered workspace holds the norms and the
+  // selection).  Out of place, the one-pass kernel writes the key norms from
+  // the rows it reads, and the retained rows are then copied from the inputs
+  // to the outputs.  In place (either tensor), the outputs would overwrite the
+  // rows to keep: the norms come from a pass of their own, and the retained
+  // rows are saved to the workspace first and written back last.
   hg_sizes z;
   hg_packed_sizes(cfg, mask, &z);
+  const bool retain = z.retain_count > 0;
+  const bool fused = retain && K_out != K && V_out != V;
   void* ws = nullptr;
   hipError_t e = hipSuccess;
-  if (z.retain_count > 0) {
+  if (retain) {
     auto up = [](uint64_t b) { return (b + 255) & ~(uint64_t)255; };
     const uint64_t o_idx = up(z.norm_k), o_k = o_idx + up(z.ret_idx), o_v = o_k + up(z.ret_k);
-    e = hipMallocAsync(&ws, o_v + up(z.ret_v), stream);
+    const uint64_t bytes = fused ? o_k : o_v + up(z.ret_v);
+    e = hipMallocAsync(&ws, bytes, stream);
     if (e != hipSuccess) {
       (void)hipGetLastError();
-      return fail(HG_ERR_HIP, "workspace of %llu bytes: %s", (unsigned long long)(o_v + up(z.ret_v)),
-                  hipGetErrorString(e));
+      return fail(HG_ERR_HIP, "workspace of %llu bytes: %s", (unsigned long long)bytes, hipGetErrorString(e));
     }
     char* w = (char*)ws;
     p.norm = (float*)w;
     p.ret_idx = (int32_t*)(w + o_idx);
-    p.ret[0] = (uint16_t*)(w + o_k);
-    p.ret[1] = (uint16_t*)(w + o_v);
+    p.ret[0] = fused ? nullptr : (uint16_t*)(w + o_k);
+    p.ret[1] = fused ? nullptr : (uint16_t*)(w + o_v);
     p.k = z.retain_count;
-    e = hg::launch_key_norms(p, cfg->D, stream);
-    if (e == hipSuccess) e = hg::launch_retain_select(p, cfg->D, stream);
+    if (!fused) {
+      e = hg::launch_key_norms(p, cfg->D, stream);
+      if (e == hipSuccess) e = hg::launch_retain_select(p, stream);
+      if (e == hipSuccess) e = hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kGather, stream);
+    }
   }
-  if (e == hipSuccess) e = hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream);
+  if (e == hipSuccess)
+    e = hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), fused, stream);
   if (e == hipSuccess && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, true, stream);
-  if (e == hipSuccess && p.k > 0) e = hg::launch_retain_scatter(p, cfg->D, stream);
+  if (e == hipSuccess && fused) {
+    e = hg::launch_retain_select(p, stream);
+    if (e == hipSuccess) e = hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kCacheToOut, stream);
+  } else if (e == hipSuccess && retain) {
+    e = hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kScatter, stream);
+  }
   if (ws) {
     const hipError_t f = hipFreeAsync(ws, stream);
     if (e == hipSuccess) e = f;

@@ -26,9 +26,9 @@ __device__ __forceinline__ constexpr int fq_slot(int t, int c) {
   return t * (D / 8) + (c ^ (D == 128 ? (t & 3) : ((t >> 1) & 1)));
 }
 
-template <int D, int BITS, bool ROTATE>
+template <int D, int BITS, bool ROTATE, bool NORM>
 // rows and out may be the same memory (in place): no restrict qualifiers.
-__device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out,
+__device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out, float* norm,
                                             int t_first, int n, int lane, u32x4* __restrict__ stage) {
   constexpr int E = D / 4;             // elements per lane (quad per token)
   constexpr int NV = E / 8;            // 16-byte chunks per lane
@@ -65,6 +65,11 @@ __device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out,
       x[8 * k + 5] = bf16_hi(raw[pass][k].z);
       x[8 * k + 6] = bf16_lo(raw[pass][k].w);
       x[8 * k + 7] = bf16_hi(raw[pass][k].w);
+    }
+    if constexpr (NORM) {  // squared key norm for token retention, before the rotation
+      const float sq = quad_sqnorm<E>(x);
+      const int t = t_first + pass * 16 + q;
+      if (t < n && j == 0) norm[t] = sq;
     }
     if constexpr (ROTATE) fwht_quad<E>(x, j, fwht_scale<D>());
 
@@ -167,9 +172,9 @@ __device__ __forceinline__ void fake_kivi_keys(const uint16_t* rows, uint16_t* o
   }
 }
 
-template <int D>
+template <int D, bool NORM>
 __device__ __forceinline__ void fake_copy(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
-                                          int t_first, int n, int lane) {
+                                          float* __restrict__ norm, int t_first, int n, int lane) {
   constexpr int VPT = D / 8;
   const int nvec = min(kWaveTokens, n - t_first) * VPT;
   const u32x4* s = (const u32x4*)(src + (size_t)t_first * D);
@@ -183,9 +188,20 @@ __device__ __forceinline__ void fake_copy(const uint16_t* __restrict__ src, uint
     const int i = lane + 64 * k;
     if (i < nvec) store_nt(d + i, v[k]);
   }
+  if constexpr (NORM) {
+    // vector i holds channels [8c, 8c + 8) of token i / VPT, c = i % VPT
+#pragma unroll
+    for (int k = 0; k < kMax; ++k) {
+      const float sq = row_sqnorm<D>(v[k]);
+      const int i = lane + 64 * k;
+      if (i < nvec && i % VPT == 0) norm[t_first + i / VPT] = sq;
+    }
+  }
 }
 
-template <int BASE, int D, int BITS>
+// NORM (AKVQ keys, out of place only): also write every image key's squared
+// norm for token retention, from the rows this pass reads anyway.
+template <int BASE, int D, int BITS, bool NORM>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWaves)))
 void fake_quantize_kernel(const Params p) {
   const Slice sl = decode_block(p, blockIdx.x);
@@ -197,8 +213,12 @@ void fake_quantize_kernel(const Params p) {
   const size_t base = ((size_t)sl.s * p.T + p.s0) * D;
   const uint16_t* rows = p.cache[sl.X] + base;
   uint16_t* out = p.out[sl.X] + base;
+  float* norm = NORM ? p.norm + (size_t)sl.s * p.n : nullptr;  // used for K only
   if (sl.kept) {
-    if (out != rows) fake_copy<D>(rows, out, t_first, p.n, lane);
+    if (NORM && sl.X == 0)
+      fake_copy<D, NORM>(rows, out, norm, t_first, p.n, lane);
+    else if (out != rows)
+      fake_copy<D, false>(rows, out, nullptr, t_first, p.n, lane);
     return;
   }
   if (BASE == HG_BASE_KIVI && sl.X == 0) {
@@ -207,43 +227,51 @@ void fake_quantize_kernel(const Params p) {
   } else {
     __shared__ u32x4 stage_all[kThreads / 64][16 * (D / 8)];
     if (BASE == HG_BASE_AKVQ && sl.X == 0)
-      fake_tokens<D, BITS, true>(rows, out, t_first, p.n, lane, stage_all[wave]);
+      fake_tokens<D, BITS, true, NORM>(rows, out, norm, t_first, p.n, lane, stage_all[wave]);
     else
-      fake_tokens<D, BITS, false>(rows, out, t_first, p.n, lane, stage_all[wave]);
+      fake_tokens<D, BITS, false, false>(rows, out, nullptr, t_first, p.n, lane, stage_all[wave]);
   }
 }
 
 template <int BASE, int D, int BITS>
-static hipError_t launch_f(const Params& p, uint32_t blocks, hipStream_t stream) {
-  hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS>), dim3(blocks), dim3(kThreads), 0, stream, p);
+static hipError_t launch_f(const Params& p, uint32_t blocks, bool norms, hipStream_t stream) {
+  if constexpr (BASE == HG_BASE_AKVQ) {
+    if (norms) {
+      hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS, true>), dim3(blocks), dim3(kThreads), 0, stream, p);
+      return hipGetLastError();
+    }
+  }
+  if (norms) return hipErrorInvalidValue;  // key norms belong to the AKVQ base
+  hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS, false>), dim3(blocks), dim3(kThreads), 0, stream, p);
   return hipGetLastError();
 }
 
 template <int BASE, int D>
-static hipError_t launch_f_bits(const Params& p, int bits, uint32_t blocks, hipStream_t stream) {
+static hipError_t launch_f_bits(const Params& p, int bits, uint32_t blocks, bool norms, hipStream_t stream) {
   switch (bits) {
-    case 2: return launch_f<BASE, D, 2>(p, blocks, stream);
-    case 3: return launch_f<BASE, D, 3>(p, blocks, stream);
-    case 4: return launch_f<BASE, D, 4>(p, blocks, stream);
+    case 2: return launch_f<BASE, D, 2>(p, blocks, norms, stream);
+    case 3: return launch_f<BASE, D, 3>(p, blocks, norms, stream);
+    case 4: return launch_f<BASE, D, 4>(p, blocks, norms, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int BASE>
-static hipError_t launch_f_dim(const Params& p, int D, int bits, uint32_t blocks, hipStream_t stream) {
+static hipError_t launch_f_dim(const Params& p, int D, int bits, uint32_t blocks, bool norms,
+                               hipStream_t stream) {
   switch (D) {
-    case 64: return launch_f_bits<BASE, 64>(p, bits, blocks, stream);
-    case 128: return launch_f_bits<BASE, 128>(p, bits, blocks, stream);
+    case 64: return launch_f_bits<BASE, 64>(p, bits, blocks, norms, stream);
+    case 128: return launch_f_bits<BASE, 128>(p, bits, blocks, norms, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
+hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, uint32_t blocks, bool norms,
                                 hipStream_t stream) {
   switch (base) {
-    case HG_BASE_MINMAX: return launch_f_dim<HG_BASE_MINMAX>(p, D, bits, blocks, stream);
-    case HG_BASE_KIVI: return launch_f_dim<HG_BASE_KIVI>(p, D, bits, blocks, stream);
-    case HG_BASE_AKVQ: return launch_f_dim<HG_BASE_AKVQ>(p, D, bits, blocks, stream);
+    case HG_BASE_MINMAX: return launch_f_dim<HG_BASE_MINMAX>(p, D, bits, blocks, norms, stream);
+    case HG_BASE_KIVI: return launch_f_dim<HG_BASE_KIVI>(p, D, bits, blocks, norms, stream);
+    case HG_BASE_AKVQ: return launch_f_dim<HG_BASE_AKVQ>(p, D, bits, blocks, norms, stream);
     default: return hipErrorInvalidValue;
   }
 }

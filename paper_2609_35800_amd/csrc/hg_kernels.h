@@ -57,15 +57,17 @@ hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t 
 hipError_t launch_dequantize(const Params& p, int base, int D, int bits, uint32_t blocks,
                              hipStream_t stream);
 hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
-                                hipStream_t stream);
+                                bool norms, hipStream_t stream);
 // KIVI keys over the whole sequence: one workgroup per key slice.
 hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, hipStream_t stream);
 // Token retention: squared key norms of every image token (p.norm); the k
-// largest per (l, b, h) into p.ret_idx with their rows gathered from
-// p.cache into p.ret; the retained rows written back from p.ret into p.out.
+// largest per (l, b, h) into p.ret_idx; their rows gathered from p.cache into
+// p.ret, written back from p.ret into p.out, or copied from p.cache straight
+// into p.out.
 hipError_t launch_key_norms(const Params& p, int D, hipStream_t stream);
-hipError_t launch_retain_select(const Params& p, int D, hipStream_t stream);
-hipError_t launch_retain_scatter(const Params& p, int D, hipStream_t stream);
+hipError_t launch_retain_select(const Params& p, hipStream_t stream);
+enum class RowCopy { kGather, kScatter, kCacheToOut };
+hipError_t launch_retain_rows(const Params& p, int D, RowCopy mode, hipStream_t stream);
 
 // Routing of one (tensor, slice): whether it is kept in BF16 and its slot in
 // the packed buffers (rank among kept heads if kept, else among quantized

@@ -11,7 +11,9 @@
 //    (non-negative, so they order as unsigned integers) and lists the retained
 //    tokens in ascending order (all larger norms, then the lowest-index ties);
 //  - retain_rows_kernel gathers their K and V rows for each tensor the head
-//    does not keep in BF16, or writes them back over the reconstruction.
+//    does not keep in BF16, or writes them back over the reconstruction; an
+//    out-of-place one-pass call, which computes the norms in its own pass,
+//    copies them from the input straight to the output.
 
 #include "hg_device.h"
 #include "hg_kernels.h"
@@ -173,9 +175,10 @@ __global__ __launch_bounds__(kThreads) void retain_select_kernel(const Params p)
 // ------------------------------------------------------------ retained rows
 
 // Grid (l*B*H, 2): one workgroup per (l, b, h) and tensor, skipping tensors the
-// head keeps in BF16.  GATHER copies the retained image rows of p.cache into
-// p.ret; otherwise p.ret is written back over p.out's image rows.
-template <int D, bool GATHER>
+// head keeps in BF16.  kGather copies the retained image rows of p.cache into
+// p.ret, kScatter writes p.ret back over p.out's image rows, kCacheToOut copies
+// them from p.cache to p.out directly.
+template <int D, RowCopy MODE>
 __global__ __launch_bounds__(kThreads) void retain_rows_kernel(const Params p) {
   constexpr int VPT = D / 8;  // 16-byte vectors per row
   constexpr int U = 4;        // vectors in flight per thread
@@ -185,7 +188,7 @@ __global__ __launch_bounds__(kThreads) void retain_rows_kernel(const Params p) {
   if (r.kept) return;
   const uint32_t k = (uint32_t)p.k;
   const int32_t* idx = p.ret_idx + (size_t)s * k;
-  uint16_t* ret = p.ret[X] + ((size_t)r.slot * p.B + r.b) * k * D;
+  uint16_t* ret = MODE == RowCopy::kCacheToOut ? nullptr : p.ret[X] + ((size_t)r.slot * p.B + r.b) * k * D;
   const size_t span = ((size_t)s * p.T + p.s0) * D;
   const uint32_t total = k * VPT;
   for (uint32_t i0 = threadIdx.x; i0 < total; i0 += U * kThreads) {
@@ -197,16 +200,16 @@ __global__ __launch_bounds__(kThreads) void retain_rows_kernel(const Params p) {
       const uint32_t row = i / VPT, c = i % VPT;
       tok[u] = (uint32_t)idx[row];
       const uint32_t t = min(tok[u], (uint32_t)p.n - 1);  // an out-of-span entry is not stored
-      v[u] = GATHER ? *(const u32x4*)(p.cache[X] + span + (size_t)t * D + 8 * c)
-                    : *(const u32x4*)(ret + (size_t)row * D + 8 * c);
+      v[u] = MODE == RowCopy::kScatter ? *(const u32x4*)(ret + (size_t)row * D + 8 * c)
+                                       : *(const u32x4*)(p.cache[X] + span + (size_t)t * D + 8 * c);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const uint32_t i = i0 + u * kThreads;
       if (i >= total || tok[u] >= (uint32_t)p.n) continue;
       const uint32_t row = i / VPT, c = i % VPT;
-      u32x4* dst = GATHER ? (u32x4*)(ret + (size_t)row * D + 8 * c)
-                          : (u32x4*)(p.out[X] + span + (size_t)tok[u] * D + 8 * c);
+      u32x4* dst = MODE == RowCopy::kGather ? (u32x4*)(ret + (size_t)row * D + 8 * c)
+                                            : (u32x4*)(p.out[X] + span + (size_t)tok[u] * D + 8 * c);
       store_nt(dst, v[u]);
     }
   }
@@ -225,31 +228,37 @@ hipError_t launch_key_norms(const Params& p, int D, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <bool GATHER>
-static hipError_t launch_rows(const Params& p, int D, hipStream_t stream) {
+template <int D>
+static hipError_t launch_rows_d(const Params& p, RowCopy mode, hipStream_t stream) {
   const dim3 grid((uint32_t)p.L * p.B * p.H, 2);
-  if (D == 64)
-    hipLaunchKernelGGL((retain_rows_kernel<64, GATHER>), grid, dim3(kThreads), 0, stream, p);
-  else if (D == 128)
-    hipLaunchKernelGGL((retain_rows_kernel<128, GATHER>), grid, dim3(kThreads), 0, stream, p);
-  else
-    return hipErrorInvalidValue;
+  switch (mode) {
+    case RowCopy::kGather:
+      hipLaunchKernelGGL((retain_rows_kernel<D, RowCopy::kGather>), grid, dim3(kThreads), 0, stream, p);
+      break;
+    case RowCopy::kScatter:
+      hipLaunchKernelGGL((retain_rows_kernel<D, RowCopy::kScatter>), grid, dim3(kThreads), 0, stream, p);
+      break;
+    default:
+      hipLaunchKernelGGL((retain_rows_kernel<D, RowCopy::kCacheToOut>), grid, dim3(kThreads), 0, stream, p);
+      break;
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_retain_select(const Params& p, int D, hipStream_t stream) {
+hipError_t launch_retain_rows(const Params& p, int D, RowCopy mode, hipStream_t stream) {
+  if (D == 64) return launch_rows_d<64>(p, mode, stream);
+  if (D == 128) return launch_rows_d<128>(p, mode, stream);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_retain_select(const Params& p, hipStream_t stream) {
   const uint32_t blocks = (uint32_t)p.L * p.B * p.H;
   if (p.n <= kResidentKeys)
     hipLaunchKernelGGL((retain_select_kernel<true>), dim3(blocks), dim3(kThreads),
                        (size_t)p.n * sizeof(uint32_t), stream, p);
   else
     hipLaunchKernelGGL((retain_select_kernel<false>), dim3(blocks), dim3(kThreads), 0, stream, p);
-  hipError_t e = hipGetLastError();
-  return e == hipSuccess ? launch_rows<true>(p, D, stream) : e;
-}
-
-hipError_t launch_retain_scatter(const Params& p, int D, hipStream_t stream) {
-  return launch_rows<false>(p, D, stream);
+  return hipGetLastError();
 }
 
 }  // namespace hg

@@ -126,6 +126,29 @@ def test_fake_quantize(w, inplace):
     check_fake(w, K, V, synthkv.protect_mask(w), inplace)
 
 
+@pytest.mark.parametrize("k_in_place", [True, False])
+def test_fake_quantize_one_tensor_in_place(k_in_place):
+    """One output is its input and the other is not: the retained rows of
+    the in-place tensor must be saved before they are overwritten."""
+    import paper_2609_35800_amd as hg
+    from test_gpu_fakequant import SENTINEL, oracle_roundtrip
+    w = retain_case(img_len=300, permille=50)
+    K, V = synthkv.gen_kv(w)
+    mask = synthkv.protect_mask(w)
+    cfg = hg.make_config(**w.config_fields())
+    Kg, Vg = K.cuda().contiguous(), V.cuda().contiguous()
+    fresh = lambda t: torch.full(t.shape, SENTINEL, dtype=torch.int16, device="cuda").view(torch.bfloat16)
+    Ko = Kg if k_in_place else fresh(Kg)
+    Vo = fresh(Vg) if k_in_place else Vg
+    hg.hg_fake_quantize(cfg, Kg, Vg, mask, Ko, Vo)
+    torch.cuda.synchronize()
+    Kb, Vb = synthkv.bf16_bits(K), synthkv.bf16_bits(V)
+    oK, oV = oracle_roundtrip(w, Kb, Vb, mask, Kb if k_in_place else np.full_like(Kb, SENTINEL),
+                              np.full_like(Vb, SENTINEL) if k_in_place else Vb)
+    assert np.array_equal(synthkv.bf16_bits(Ko), oK)
+    assert np.array_equal(synthkv.bf16_bits(Vo), oV)
+
+
 def test_fake_quantize_ties_in_place():
     w = retain_case(img_len=500, permille=60)
     K, V = _integer_kv(w, -2, 3, 5)
@@ -181,11 +204,18 @@ def test_full_size_internvl_two_percent():
                             idx.long().unsqueeze(-1).expand(-1, -1, -1, -1, D))
     source = torch.gather(K[:, :, :, s0:s0 + n], 3, idx.long().unsqueeze(-1).expand(-1, -1, -1, -1, D))
     assert torch.equal(gathered.view(torch.int16), source.view(torch.int16))
-    # the one-pass form writes exactly the same bytes
+    # the one-pass form writes exactly the same bytes, out of place (norms
+    # from its own pass) and in place (norms from a separate pass)
     del packed
+    img = slice(s0, s0 + n)
+    Kf, Vf = torch.empty_like(K), torch.empty_like(V)
+    hg.hg_fake_quantize(cfg, K, V, mask, Kf, Vf)
+    torch.cuda.synchronize()
+    assert torch.equal(Kf[:, :, :, img].view(torch.int16), Ko[:, :, :, img].view(torch.int16))
+    assert torch.equal(Vf[:, :, :, img].view(torch.int16), Vo[:, :, :, img].view(torch.int16))
+    del Kf, Vf
     hg.hg_fake_quantize(cfg, K, V, mask, K, V)
     torch.cuda.synchronize()
-    img = slice(s0, s0 + n)
     assert torch.equal(K[:, :, :, img].view(torch.int16), Ko[:, :, :, img].view(torch.int16))
     assert torch.equal(V[:, :, :, img].view(torch.int16), Vo[:, :, :, img].view(torch.int16))
     torch.cuda.empty_cache()
