@@ -183,18 +183,40 @@ __device__ __forceinline__ float butterfly_fma(float v, float s) {
   return __builtin_fmaf(quad_swap<CTRL>(v), s, v);
 }
 
+// Eight butterflies of one stage, each a single v_fmac_f32 whose first source
+// is read through the DPP swizzle PERM: x = dpp(x) * s + x, one rounding, as
+// butterfly_fma (the compiler keeps a separate DPP move otherwise).  A DPP
+// read of a register needs two wait states after the VALU write of it, so the
+// block starts and ends with s_nop 1; inside, each instruction reads only its
+// own register, written before the block.
+#define HG_BUTTERFLY8(PERM, x, s)                                                              \
+  asm("s_nop 1\n"                                                                              \
+      "v_fmac_f32_dpp %0, %0, %8 " PERM " row_mask:0xf bank_mask:0xf\n"                         \
+      "v_fmac_f32_dpp %1, %1, %8 " PERM " row_mask:0xf bank_mask:0xf\n"                         \
+      "v_fmac_f32_dpp %2, %2, %8 " PERM " row_mask:0xf bank_mask:0xf\n"                         \
+      "v_fmac_f32_dpp %3, %3, %8 " PERM " row_mask:0xf bank_mask:0xf\n"                         \
+      "v_fmac_f32_dpp %4, %4, %8 " PERM " row_mask:0xf bank_mask:0xf\n"                         \
+      "v_fmac_f32_dpp %5, %5, %8 " PERM " row_mask:0xf bank_mask:0xf\n"                         \
+      "v_fmac_f32_dpp %6, %6, %8 " PERM " row_mask:0xf bank_mask:0xf\n"                         \
+      "v_fmac_f32_dpp %7, %7, %8 " PERM " row_mask:0xf bank_mask:0xf\n"                         \
+      "s_nop 1"                                                                                \
+      : "+v"((x)[0]), "+v"((x)[1]), "+v"((x)[2]), "+v"((x)[3]), "+v"((x)[4]), "+v"((x)[5]),    \
+        "+v"((x)[6]), "+v"((x)[7])                                                             \
+      : "v"(s))
+
 // Full transform over D = 4E elements held by a lane quad (lane j holds
 // elements [E*j, E*j + E)): spans 1..E/2 in registers, then E (lane ^ 1) and
 // 2E (lane ^ 2), then the scale c.  Same butterfly order as spans 1..D/2.
 template <int E>
 __device__ __forceinline__ void fwht_quad(float (&x)[E], int j, float c) {
+  static_assert(E % 8 == 0, "whole blocks of eight");
   fwht_lane<E>(x);
   const float s1 = (j & 1) ? -1.0f : 1.0f;
   const float s2 = (j & 2) ? -1.0f : 1.0f;
 #pragma unroll
-  for (int e = 0; e < E; ++e) x[e] = butterfly_fma<kQuadXor1>(x[e], s1);
+  for (int e = 0; e < E; e += 8) HG_BUTTERFLY8("quad_perm:[1,0,3,2]", x + e, s1);
 #pragma unroll
-  for (int e = 0; e < E; ++e) x[e] = butterfly_fma<kQuadXor2>(x[e], s2);
+  for (int e = 0; e < E; e += 8) HG_BUTTERFLY8("quad_perm:[2,3,0,1]", x + e, s2);
   const float cs = c * s1 * s2;  // c with the carried sign, exact
 #pragma unroll
   for (int e = 0; e < E; ++e) x[e] = __builtin_fmaf(x[e], cs, 0.0f);
