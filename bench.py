@@ -92,6 +92,17 @@ def algorithmic_bytes(w, sizes) -> dict:
             "read": read, "write": write}
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, K, V, mask, budget_s: float, threads: int = 0):
     """The CPU oracle on a bounded sample of the same workload, quantize then
     dequantize: whole passes over the cache, repeated to fill about budget_s
@@ -126,7 +137,8 @@ def cpu_baseline(w, K, V, mask, budget_s: float, threads: int = 0):
     ab = algorithmic_bytes(sub, {n: int(v.nbytes) for n, v in pk.items()})
     per_pass = total / passes
     return {"value": round((ab["quant"] + ab["dequant"]) / per_pass / 1e9, 4), "unit": "GB/s",
-            "cores": threads, "kind": "oracle",
+            "cores": threads, "kind": "oracle", "cpu_model": cpu_model(),
+            "host_cores": os.cpu_count(),
             "sample": f"{nl} of {w.L} layers of the same workload (all rows, heads, K and V), "
                       f"quantize+dequantize, {passes} pass(es), {total:.2f} s wall",
             # image tokens of the whole cache, scaled by the fraction of layers in the sample
