@@ -90,6 +90,19 @@ def test_maximum_head_count(base, keys_only, retain):
     _assert_exact(compare_full(w, K, V, mask), w.name)
 
 
+@pytest.mark.parametrize("base,kivi_group,retain", [("minmax", 32, 0), ("kivi", 32, 0), ("kivi", 0, 0),
+                                                     ("akvq", 32, 20)])
+def test_long_span(base, kivi_group, retain):
+    """A 70001-token image span (547 workgroup tiles per slice, ragged tail;
+    the retention selection reads its norms from global memory)."""
+    w = synthkv.Workload(f"long-{base}-{kivi_group}-{retain}", L=1, B=1, H=2, T=70011, D=64, img_start=6,
+                         img_len=70001, bits=2, base=base, keys_only=0, n_protected=0, k_outliers=2,
+                         k_outlier_scale=10.0, kivi_group=kivi_group, retain_permille=retain)
+    K, V = synthkv.gen_kv(w)
+    mask = np.array([0, 1], np.uint8)
+    _assert_exact(compare_full(w, K, V, mask), w.name)
+
+
 def _special_values(w, K, V):
     """Plant constant tokens, signed zeros, tiny ranges, ties and large values."""
     s = w.img_start
