@@ -2,10 +2,11 @@
 // head the keys and values of a nominal 2 % of the image tokens, those whose
 // keys have the largest norms, stay in BF16, with or without head protection.
 //
-// The quantize kernel writes the squared key norm of every image token in the
-// same pass that reads the keys (key_norm_kernel does it on its own for the
-// one-pass simulated quantization, whose in-place outputs would otherwise
-// overwrite the rows to keep).  Then, per (l, b, h):
+// The quantize kernel, and the one-pass simulated quantization out of place,
+// write the squared key norm of every image token in the pass that reads the
+// keys; key_norm_kernel computes them on their own for an in-place one-pass
+// call, whose outputs would otherwise overwrite the rows to keep.  Then, per
+// (l, b, h):
 //  - retain_select_kernel (norms staged in LDS) finds the k-th largest norm by
 //    a most-significant-digit-first radix select over the fp32 bit patterns
 //    (non-negative, so they order as unsigned integers) and lists the retained
