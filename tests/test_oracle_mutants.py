@@ -38,6 +38,7 @@ MUTANTS = [
      "float S = hgo_bf16_to_f32((uint16_t)(meta >> 16));\n  float m = hgo_bf16_to_f32((uint16_t)(meta & 0xFFFFu));"),
     ("fwht_sign", "a[j + h] = p - q;", "a[j + h] = q - p;"),
     ("fwht_missing_stage", "for (int h = 1; h < D; h *= 2)", "for (int h = 1; h < D / 2; h *= 2)"),
+    ("fwht_reversed_stages", "for (int h = 1; h < D; h *= 2)", "for (int h = D / 2; h >= 1; h /= 2)"),
     ("fwht_missing_scale", "for (int j = 0; j < D; ++j) a[j] = a[j] * c;", "(void)c;"),
     ("route_rank_counts_all", "if (is_kept(c, mask, X, j) == kept) rank++;", "rank++;"),
     ("k_only_protects_values", "return X == 0 ? 1 : !c->keys_only;", "return 1;"),
