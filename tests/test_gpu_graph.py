@@ -1,0 +1,61 @@
+"""The entry points inside a captured HIP graph: hg_quantize followed by
+hg_dequantize is captured once (the calls only launch kernels on the given
+stream: no allocation, no synchronisation, no memset) and replayed several
+times, with the outputs cleared by eager work in between; every replay must
+write exactly the bytes of the eager calls.  Covers the per-token, KIVI
+(grouped and whole-sequence) and AKVQ-with-retention paths."""
+import numpy as np
+import pytest
+import torch
+
+import synthkv
+from test_gpu_parity import small
+
+pytestmark = pytest.mark.gpu
+
+CASES = [small("minmax", img_len=300), small("kivi", keys_only=1, img_len=300),
+         small("kivi", img_len=300).with_(kivi_group=0, name="kivi-whole"),
+         small("akvq", img_len=300).with_(retain_permille=50, name="akvq-retain")]
+
+
+def _snapshot(packed, Ko, Vo):
+    return {**{n: t.clone() for n, t in packed.items()}, "K": Ko.clone(), "V": Vo.clone()}
+
+
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def test_capture_and_replay(w):
+    import paper_2609_35800_amd as hg
+    mask = synthkv.protect_mask(w)
+    cfg = hg.make_config(**w.config_fields())
+    K, V = synthkv.gen_kv(w, device="cuda")
+    packed = hg.alloc_packed(cfg, mask)
+    Ko, Vo = torch.zeros_like(K), torch.zeros_like(V)
+
+    def clear():
+        for t in packed.values():
+            t.fill_(0xA5)
+        Ko.fill_(0.0)
+        Vo.fill_(0.0)
+
+    clear()
+    hg.hg_quantize(cfg, K, V, mask, packed)
+    hg.hg_dequantize(cfg, mask, packed, Ko, Vo)
+    torch.cuda.synchronize()
+    want = _snapshot(packed, Ko, Vo)
+
+    clear()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        hg.hg_quantize(cfg, K, V, mask, packed)
+        hg.hg_dequantize(cfg, mask, packed, Ko, Vo)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        clear()  # eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = _snapshot(packed, Ko, Vo)
+        for name in want:
+            assert torch.equal(got[name].view(torch.uint8), want[name].view(torch.uint8)), name
+    del graph
