@@ -32,7 +32,7 @@ KERNEL_SOURCES = ("paper_2609_35800_amd/csrc/quantize.hip", "paper_2609_35800_am
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen2.5-vl-7b")
     ap.add_argument("--bits", type=int, default=None, help="override the workload's bit width")
