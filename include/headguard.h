@@ -165,7 +165,9 @@ int hg_select_heads(const double* g, const double* o, int32_t L, int32_t Hq, int
  * entries are rounded to the base's levels and reconstructed as floating-point
  * values): writes to the image rows of K_out, V_out exactly what hg_quantize
  * followed by hg_dequantize would, without packed buffers.  K_out may be K
- * (in place) and V_out may be V; otherwise they must not overlap them.  Kept
+ * (in place) and V_out may be V; otherwise an output must not overlap its
+ * input, and no output may overlap the other tensor's input or the other
+ * output (HG_ERR_POINTER, checked before any device work).  Kept
  * rows are copied (left alone in place); text rows are not written.  Device
  * pointers 16-byte aligned.  With token retention the call allocates a
  * stream-ordered workspace (hipMallocAsync / hipFreeAsync on `stream`) for

@@ -285,12 +285,23 @@ int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
   const uint64_t cache_bytes = (uint64_t)cfg->L * cfg->B * cfg->H * cfg->T * cfg->D * 2;
   const uint64_t need = cfg->img_len > 0 ? cache_bytes : 0;
   if (need && (!K || !V || !K_out || !V_out)) return fail(HG_ERR_NULL, "K, V, K_out and V_out are required");
+  // Each output is its own input or disjoint from it; no output may overlap
+  // the other tensor's input or the other output.
+  auto overlap = [need](const void* x, const void* y) {
+    const uintptr_t a = (uintptr_t)x, b = (uintptr_t)y;
+    return need && a < b + need && b < a + need;
+  };
   for (int X = 0; X < 2; ++X) {
-    const uintptr_t a = (uintptr_t)(X ? V : K), b = (uintptr_t)(X ? V_out : K_out);
-    if (need && a != b && a < b + need && b < a + need)
-      return fail(HG_ERR_POINTER, "%s_out partially overlaps %s (must be the same buffer or disjoint)",
-                  X ? "V" : "K", X ? "V" : "K");
+    const void* in = X ? (const void*)V : (const void*)K;
+    const void* out = X ? (const void*)V_out : (const void*)K_out;
+    const void* other_in = X ? (const void*)K : (const void*)V;
+    const char* nm = X ? "V" : "K";
+    if (out != in && overlap(in, out))
+      return fail(HG_ERR_POINTER, "%s_out partially overlaps %s (must be the same buffer or disjoint)", nm, nm);
+    if (overlap(out, other_in))
+      return fail(HG_ERR_POINTER, "%s_out overlaps %s", nm, X ? "K" : "V");
   }
+  if (overlap(K_out, V_out)) return fail(HG_ERR_POINTER, "K_out and V_out overlap");
   const Buf bufs[] = {{K, need, 16, "K"}, {V, need, 16, "V"}, {K_out, need, 16, "K_out"}, {V_out, need, 16, "V_out"}};
   s = check_device();
   if (s) return s;

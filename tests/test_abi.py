@@ -136,6 +136,22 @@ def test_mask_values_and_nulls():
     assert lib.hg_dequantize(C.byref(cfg), m, C.byref(pk), None, 16, None) == hg.HG_ERR_NULL
 
 
+def test_fake_quantize_overlaps_are_refused_before_device_work():
+    cfg = hg.make_config(**_cfg())
+    need = 2 * 3 * 4 * 40 * 128 * 2  # cache bytes
+    mask = np.zeros(8, np.uint8).ctypes.data_as(C.c_void_p)
+    lib = hg.library()
+    K, V, Ko, Vo = 1 << 32, 2 << 32, 3 << 32, 4 << 32  # disjoint, 16-byte aligned, never touched
+    cases = [(K, V, K + 256, Vo),        # K_out partially overlaps K
+             (K, V, Ko, V + need - 16),  # V_out partially overlaps V
+             (K, V, V, Vo),              # K_out is V
+             (K, V, Ko, K + 16),         # V_out overlaps K
+             (K, V, Ko, Ko + 16)]        # the outputs overlap
+    for k, v, ko, vo in cases:
+        assert lib.hg_fake_quantize(C.byref(cfg), k, v, mask, ko, vo, None) == hg.HG_ERR_POINTER
+        assert "overlap" in hg.hg_last_error() or "is V" in hg.hg_last_error()
+
+
 def test_no_device_is_reported_not_crashed():
     import torch
     if torch.cuda.is_available():
