@@ -67,10 +67,11 @@
  * synchronisation.  Every argument check runs before any launch, so on error
  * no output is touched.  Calls are thread-safe; the error detail is per thread.
  *
- * Preconditions not checked: inputs finite with |x| < 2^96 (so every range
- * and rotated value, at most sqrt(D) |x|, keeps its scale below 2^101); buffers
- * at least the sizes hg_packed_sizes reports; no overlap between inputs and
- * outputs.
+ * Every buffer a call writes must be disjoint from every other buffer of the
+ * call (HG_ERR_POINTER, checked on the host from the pointers and the sizes
+ * hg_packed_sizes reports).  Preconditions not checked: inputs finite with
+ * |x| < 2^96 (so every range and rotated value, at most sqrt(D) |x|, keeps its
+ * scale below 2^101); buffers at least the sizes hg_packed_sizes reports.
  */
 #ifndef HEADGUARD_H
 #define HEADGUARD_H

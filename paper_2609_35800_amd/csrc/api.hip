@@ -237,9 +237,22 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
       {pk->ret_k, z.ret_k, 16, "ret_k"},
       {pk->ret_v, z.ret_v, 16, "ret_v"},
   };
+  const int nb = (int)(sizeof bufs / sizeof bufs[0]);
+  // Every buffer the call writes (quantize: the packed ones; dequantize: K_out,
+  // V_out) must be disjoint from every other buffer of the call.
+  for (int i = 0; i < nb; ++i) {
+    const bool written = quantize ? i >= 2 : i < 2;
+    if (!written || bufs[i].bytes == 0) continue;
+    for (int j = 0; j < nb; ++j) {
+      if (j == i || bufs[j].bytes == 0) continue;
+      const uintptr_t a = (uintptr_t)bufs[i].p, b = (uintptr_t)bufs[j].p;
+      if (a < b + bufs[j].bytes && b < a + bufs[i].bytes)
+        return fail(HG_ERR_POINTER, "%s overlaps %s", bufs[i].name, bufs[j].name);
+    }
+  }
   s = check_device();
   if (s) return s;
-  s = check_buffers(bufs, (int)(sizeof bufs / sizeof bufs[0]));
+  s = check_buffers(bufs, nb);
   if (s) return s;
   if (cfg->img_len == 0) return ok();
 

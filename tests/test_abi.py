@@ -152,6 +152,36 @@ def test_fake_quantize_overlaps_are_refused_before_device_work():
         assert "overlap" in hg.hg_last_error() or "is V" in hg.hg_last_error()
 
 
+def test_overlapping_outputs_are_refused_before_device_work():
+    f = _cfg()
+    cfg = hg.make_config(**f)
+    mask = np.zeros(8, np.uint8)
+    sz = hg.hg_packed_sizes(cfg, mask)
+    need = 2 * 3 * 4 * 40 * 128 * 2
+    lib = hg.library()
+    base = 1 << 36
+    ptrs = {n: base + (i + 1) * (1 << 30) for i, n in enumerate(hg.BUFFERS)}
+    K, V = base + (20 << 30), base + (22 << 30)
+    m = mask.ctypes.data_as(C.c_void_p)
+
+    def packed(**over):
+        return hg.hg_packed(**{**{n: ptrs[n] for n in hg.BUFFERS}, **over})
+
+    # quantize: a packed output overlapping an input or another output
+    for over in ({"codes_k": K + 16}, {"meta_v": ptrs["codes_k"] + 16}, {"codes_v": V}):
+        pk = packed(**over)
+        assert lib.hg_quantize(C.byref(cfg), K, V, m, C.byref(pk), None) == hg.HG_ERR_POINTER
+        assert "overlaps" in hg.hg_last_error()
+    # dequantize: an output overlapping the other output or a packed input
+    pk = packed()
+    assert lib.hg_dequantize(C.byref(cfg), m, C.byref(pk), K, K + need - 16, None) == hg.HG_ERR_POINTER
+    assert lib.hg_dequantize(C.byref(cfg), m, C.byref(pk), ptrs["codes_v"], V, None) == hg.HG_ERR_POINTER
+    # K and V may be the same input to quantize; that alone is not an overlap error
+    rc = lib.hg_quantize(C.byref(cfg), K, K, m, C.byref(packed()), None)
+    assert rc != hg.HG_ERR_POINTER
+    assert sz["codes_k"] > 0
+
+
 def test_no_device_is_reported_not_crashed():
     import torch
     if torch.cuda.is_available():
@@ -159,7 +189,7 @@ def test_no_device_is_reported_not_crashed():
     cfg = hg.make_config(**_cfg())
     mask = np.zeros(8, np.uint8)
     lib = hg.library()
-    pk = hg.hg_packed()
+    pk = hg.hg_packed(**{n: (1 << 36) + (i + 1) * (1 << 30) for i, n in enumerate(hg.BUFFERS)})
     rc = lib.hg_quantize(C.byref(cfg), 16, 16, mask.ctypes.data_as(C.c_void_p), C.byref(pk), None)
     assert rc == hg.HG_ERR_NO_DEVICE
 
