@@ -173,7 +173,9 @@ int hg_select_heads(const double* g, const double* o, int32_t L, int32_t Hq, int
  * pointers 16-byte aligned.  With token retention the call allocates a
  * stream-ordered workspace (hipMallocAsync / hipFreeAsync on `stream`) for
  * the key norms and the retained rows, about (4n + k(4 + 4D)) bytes per
- * (l, b, h); HG_ERR_HIP if it cannot. */
+ * (l, b, h); HG_ERR_HIP if it cannot.  Without retention the call only
+ * launches kernels on `stream` (as hg_quantize and hg_dequantize do), so it can
+ * be captured in a HIP graph. */
 int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
                      const uint8_t* protect_mask, uint16_t* K_out, uint16_t* V_out,
                      hipStream_t stream);

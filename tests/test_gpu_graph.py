@@ -1,5 +1,6 @@
 """The entry points inside a captured HIP graph: hg_quantize followed by
-hg_dequantize is captured once (the calls only launch kernels on the given
+hg_dequantize (and, separately, the one-pass hg_fake_quantize without token
+retention) is captured once (the calls only launch kernels on the given
 stream: no allocation, no synchronisation, no memset) and replayed several
 times, with the outputs cleared by eager work in between; every replay must
 write exactly the bytes of the eager calls.  Covers the per-token, KIVI
@@ -58,4 +59,29 @@ def test_capture_and_replay(w):
         got = _snapshot(packed, Ko, Vo)
         for name in want:
             assert torch.equal(got[name].view(torch.uint8), want[name].view(torch.uint8)), name
+    del graph
+
+
+@pytest.mark.parametrize("w", CASES[:3], ids=lambda w: w.name)
+def test_capture_one_pass(w):
+    """hg_fake_quantize without token retention only launches kernels too."""
+    import paper_2609_35800_amd as hg
+    mask = synthkv.protect_mask(w)
+    cfg = hg.make_config(**w.config_fields())
+    K, V = synthkv.gen_kv(w, device="cuda")
+    Ko, Vo = torch.zeros_like(K), torch.zeros_like(V)
+    hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo)
+    torch.cuda.synchronize()
+    want_k, want_v = Ko.clone(), Vo.clone()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo)
+    for _ in range(3):
+        Ko.fill_(0.0)
+        Vo.fill_(0.0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(Ko.view(torch.int16), want_k.view(torch.int16))
+        assert torch.equal(Vo.view(torch.int16), want_v.view(torch.int16))
     del graph
