@@ -94,7 +94,7 @@ enum {
   HG_ERR_BITS = 4,      /* bits not in {2, 3, 4}                               */
   HG_ERR_BASE = 5,      /* unknown base, kivi_group not 32 or 0, retain_permille
                            outside [0, 1000] or set with a base other than AKVQ */
-  HG_ERR_HEADDIM = 6,   /* D not in {64, 128}                                  */
+  HG_ERR_HEADDIM = 6,   /* D not in {64, 128, 256}                             */
   HG_ERR_ALIGN = 7,     /* a device pointer is not 16-byte aligned             */
   HG_ERR_MASK = 8,      /* a mask entry is neither 0 nor 1                     */
   HG_ERR_NO_DEVICE = 9, /* no usable HIP device                                */

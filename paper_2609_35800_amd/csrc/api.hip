@@ -39,7 +39,8 @@ int check_config(const hg_config* c, const uint8_t* mask) {
     return fail(HG_ERR_SHAPE, "L, B, H, T must be positive (got %d, %d, %d, %d)", c->L, c->B, c->H, c->T);
   if ((int64_t)c->L * c->H > HG_MAX_HEADS)
     return fail(HG_ERR_SHAPE, "L*H = %lld exceeds %d", (long long)c->L * c->H, HG_MAX_HEADS);
-  if (c->D != 64 && c->D != 128) return fail(HG_ERR_HEADDIM, "head_dim %d not in {64, 128}", c->D);
+  if (c->D != 64 && c->D != 128 && c->D != 256)
+    return fail(HG_ERR_HEADDIM, "head_dim %d not in {64, 128, 256}", c->D);
   if (c->img_start < 0 || c->img_len < 0 || (int64_t)c->img_start + c->img_len > c->T)
     return fail(HG_ERR_SPAN, "image span [%d, %d + %d) outside [0, %d]", c->img_start, c->img_start,
                 c->img_len, c->T);

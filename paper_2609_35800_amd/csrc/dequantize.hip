@@ -63,40 +63,45 @@ __device__ __forceinline__ void dequantize_kivi_keys(const uint8_t* __restrict__
                                                      const uint32_t* __restrict__ meta,
                                                      uint16_t* __restrict__ rows,
                                                      int g_first, int group, int n, int lane) {
-  constexpr int LPR = D / 8;
+  constexpr int DH = D < 128 ? D : 128;  // channels per pass (head_dim 256: two passes)
+  constexpr int LPR = DH / 8;
   constexpr int RPL = 64 / LPR;
   constexpr int NL = kWaveTokens / RPL;
   constexpr int ROW = D * BITS / 8;
-  const int c8 = lane % LPR;
   const int r = lane / LPR;
 
-  const u32x4* mp = (const u32x4*)(meta + (size_t)group * D + 8 * c8);
-  const u32x4 m0 = mp[0], m1 = mp[1];
-  const uint32_t mw[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
-  float S[8], m[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    S[e] = bf16_as_float(mw[e] & 0xFFFFu);
-    m[e] = bf16_as_float(mw[e] >> 16);
-  }
+  for (int h = 0; h < D / DH; ++h) {
+    const int c8 = h * LPR + lane % LPR;
 
-  constexpr uint32_t kMask = (1u << BITS) - 1u;
-  uint32_t pc[NL];
+    const u32x4* mp = (const u32x4*)(meta + (size_t)group * D + 8 * c8);
+    const u32x4 m0 = mp[0], m1 = mp[1];
+    const uint32_t mw[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+    float S[8], m[8];
 #pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    const int t = min(g_first + r + RPL * k, n - 1);
-    pc[k] = load_piece8<BITS, ROW>(codes + (size_t)t * ROW, c8);
-  }
+    for (int e = 0; e < 8; ++e) {
+      S[e] = bf16_as_float(mw[e] & 0xFFFFu);
+      m[e] = bf16_as_float(mw[e] >> 16);
+    }
+
+    constexpr uint32_t kMask = (1u << BITS) - 1u;
+    uint32_t pc[NL];
 #pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    const int t = g_first + r + RPL * k;
-    float y[8];
+    for (int k = 0; k < NL; ++k) {
+      const int t = min(g_first + r + RPL * k, n - 1);
+      pc[k] = load_piece8<BITS, ROW>(codes + (size_t)t * ROW, c8);
+    }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf((float)((pc[k] >> (BITS * e)) & kMask), S[e], m[e]);
-    if (t < n) {
-      u32x4 v = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
-                 pack_bf16x2_hw(y[6], y[7])};
-      store_nt((u32x4*)(rows + (size_t)t * D + 8 * c8), v);
+    for (int k = 0; k < NL; ++k) {
+      const int t = g_first + r + RPL * k;
+      float y[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf((float)((pc[k] >> (BITS * e)) & kMask), S[e], m[e]);
+      if (t < n) {
+        u32x4 v = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
+                   pack_bf16x2_hw(y[6], y[7])};
+        store_nt((u32x4*)(rows + (size_t)t * D + 8 * c8), v);
+      }
     }
   }
 }
@@ -168,6 +173,7 @@ static hipError_t launch_d_dim(const Params& p, int D, int bits, uint32_t blocks
   switch (D) {
     case 64: return launch_d_bits<BASE, 64>(p, bits, blocks, stream);
     case 128: return launch_d_bits<BASE, 128>(p, bits, blocks, stream);
+    case 256: return launch_d_bits<BASE, 256>(p, bits, blocks, stream);
     default: return hipErrorInvalidValue;
   }
 }

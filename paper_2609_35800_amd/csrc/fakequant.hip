@@ -18,157 +18,168 @@
 
 namespace hg {
 
-// LDS slot of (token, chunk) in a 16-token stage of D/8 16-byte chunks per
-// token, XOR-swizzled by token so that the quad-per-token writes spread over
-// the banks.
+// LDS slot of (token, chunk) in a one-pass stage (16 tokens, 8 at head_dim
+// 256) of D/8 16-byte chunks per token, XOR-swizzled by token so that the
+// per-token-group writes spread over the banks.
 template <int D>
 __device__ __forceinline__ constexpr int fq_slot(int t, int c) {
-  return t * (D / 8) + (c ^ (D == 128 ? (t & 3) : ((t >> 1) & 1)));
+  return t * (D / 8) + (c ^ (D == 64 ? ((t >> 1) & 1) : (t & 3)));
 }
 
 template <int D, int BITS, bool ROTATE, bool NORM>
 // rows and out may be the same memory (in place): no restrict qualifiers.
 __device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out, float* norm,
                                             int t_first, int n, int lane, u32x4* __restrict__ stage) {
-  constexpr int E = D / 4;             // elements per lane (quad per token)
+  constexpr int G = kTokenLanes<D>;     // lanes per token
+  constexpr int E = D / G;             // elements per lane
   constexpr int NV = E / 8;            // 16-byte chunks per lane
+  constexpr int TPP = 64 / G;          // tokens per pass
+  constexpr int PASSES = kWaveTokens / TPP;
   constexpr int CPT = D / 8;           // chunks per token row
   constexpr int RPL = 64 / CPT;        // token rows per store instruction
-  constexpr int NSP = 16 / RPL;        // store instructions per 16-token pass
+  constexpr int NSP = TPP / RPL;       // store instructions per pass
   constexpr int LEVELS = (1 << BITS) - 1;
-  const int j = lane & 3;
-  const int q = lane >> 2;
+  const int j = lane % G;
+  const int q = lane / G;
 
-  // Tokens past the span's end load the last token (never stored).
-  u32x4 raw[2][NV];
 #pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-    const int t = min(t_first + pass * 16 + q, n - 1);
-    const u32x4* src = (const u32x4*)(rows + (size_t)t * D + j * E);
+  for (int p0 = 0; p0 < PASSES; p0 += 2) {
+    // Tokens past the span's end load the last token (never stored).
+    u32x4 raw[2][NV];
 #pragma unroll
-    for (int k = 0; k < NV; ++k) raw[pass][k] = src[k];
-  }
+    for (int b = 0; b < 2; ++b) {
+      const int t = min(t_first + (p0 + b) * TPP + q, n - 1);
+      const u32x4* src = (const u32x4*)(rows + (size_t)t * D + j * E);
+#pragma unroll
+      for (int k = 0; k < NV; ++k) raw[b][k] = src[k];
+    }
 
-  // Rotated keys unroll both passes: rolled, their per-pass register arrays
-  // went to scratch memory.  The plain path is faster rolled (measured).
-  constexpr int kUnrolledPasses = ROTATE ? 2 : 1;
+    // Rotated keys unroll both passes: rolled, their per-pass register arrays
+    // went to scratch memory.  The plain path is faster rolled (measured).
+    constexpr int kUnrolledPasses = ROTATE ? 2 : 1;
 #pragma unroll kUnrolledPasses
-  for (int pass = 0; pass < 2; ++pass) {
-    float x[E];
+    for (int pass = 0; pass < 2; ++pass) {
+      float x[E];
 #pragma unroll
-    for (int k = 0; k < NV; ++k) {
-      x[8 * k + 0] = bf16_lo(raw[pass][k].x);
-      x[8 * k + 1] = bf16_hi(raw[pass][k].x);
-      x[8 * k + 2] = bf16_lo(raw[pass][k].y);
-      x[8 * k + 3] = bf16_hi(raw[pass][k].y);
-      x[8 * k + 4] = bf16_lo(raw[pass][k].z);
-      x[8 * k + 5] = bf16_hi(raw[pass][k].z);
-      x[8 * k + 6] = bf16_lo(raw[pass][k].w);
-      x[8 * k + 7] = bf16_hi(raw[pass][k].w);
-    }
-    if constexpr (NORM) {  // squared key norm for token retention, before the rotation
-      const float sq = quad_sqnorm<E>(x);
-      const int t = t_first + pass * 16 + q;
-      if (t < n && j == 0) norm[t] = sq;
-    }
-    if constexpr (ROTATE) fwht_quad<E>(x, j, fwht_scale<D>());
+      for (int k = 0; k < NV; ++k) {
+        x[8 * k + 0] = bf16_lo(raw[pass][k].x);
+        x[8 * k + 1] = bf16_hi(raw[pass][k].x);
+        x[8 * k + 2] = bf16_lo(raw[pass][k].y);
+        x[8 * k + 3] = bf16_hi(raw[pass][k].y);
+        x[8 * k + 4] = bf16_lo(raw[pass][k].z);
+        x[8 * k + 5] = bf16_hi(raw[pass][k].z);
+        x[8 * k + 6] = bf16_lo(raw[pass][k].w);
+        x[8 * k + 7] = bf16_hi(raw[pass][k].w);
+      }
+      if constexpr (NORM) {  // squared key norm for token retention, before the rotation
+        const float sq = quad_sqnorm<E, G>(x);
+        const int t = t_first + (p0 + pass) * TPP + q;
+        if (t < n && j == 0) norm[t] = sq;
+      }
+      if constexpr (ROTATE) fwht_quad<E, G>(x, j, fwht_scale<D>());
 
-    float mn = x[0], mx = x[0];
+      float mn = x[0], mx = x[0];
 #pragma unroll
-    for (int e = 1; e < E; ++e) {
-      mn = fminf(mn, x[e]);
-      mx = fmaxf(mx, x[e]);
-    }
-    mn = quad_min(mn);
-    mx = quad_max(mx);
-    const GroupScale g = group_scale<LEVELS>(mn, mx);
-    const float S = bf16_as_float(g.meta & 0xFFFFu);
+      for (int e = 1; e < E; ++e) {
+        mn = fminf(mn, x[e]);
+        mx = fmaxf(mx, x[e]);
+      }
+      mn = group_min<G>(mn);
+      mx = group_max<G>(mx);
+      const GroupScale g = group_scale<LEVELS>(mn, mx);
+      const float S = bf16_as_float(g.meta & 0xFFFFu);
 
-    // Level of each code, q*S + m (q*S exact, one rounding), then the inverse
-    // rotation for AKVQ keys, then BF16.
+      // Level of each code, q*S + m (q*S exact, one rounding), then the inverse
+      // rotation for AKVQ keys, then BF16.
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const uint32_t code = code_bits(x[e], g) - kMagicBits;
-      x[e] = __builtin_fmaf((float)code, S, g.m);
-    }
-    if constexpr (ROTATE) fwht_quad<E>(x, j, fwht_scale<D>());
+      for (int e = 0; e < E; ++e) {
+        const uint32_t code = code_bits(x[e], g) - kMagicBits;
+        x[e] = __builtin_fmaf((float)code, S, g.m);
+      }
+      if constexpr (ROTATE) fwht_quad<E, G>(x, j, fwht_scale<D>());
 
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
 #pragma unroll
-    for (int k = 0; k < NV; ++k) {
-      const u32x4 v = {pack_bf16x2_hw(x[8 * k + 0], x[8 * k + 1]), pack_bf16x2_hw(x[8 * k + 2], x[8 * k + 3]),
-                       pack_bf16x2_hw(x[8 * k + 4], x[8 * k + 5]), pack_bf16x2_hw(x[8 * k + 6], x[8 * k + 7])};
-      stage[fq_slot<D>(q, j * NV + k)] = v;
-    }
-    // LDS operations of one wavefront execute in order; the fences keep the
-    // compiler from moving the accesses across each other.
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    const int c = lane % CPT;
-    const int r = lane / CPT;
+      for (int k = 0; k < NV; ++k) {
+        const u32x4 v = {pack_bf16x2_hw(x[8 * k + 0], x[8 * k + 1]), pack_bf16x2_hw(x[8 * k + 2], x[8 * k + 3]),
+                         pack_bf16x2_hw(x[8 * k + 4], x[8 * k + 5]), pack_bf16x2_hw(x[8 * k + 6], x[8 * k + 7])};
+        stage[fq_slot<D>(q, j * NV + k)] = v;
+      }
+      // LDS operations of one wavefront execute in order; the fences keep the
+      // compiler from moving the accesses across each other.
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      const int c = lane % CPT;
+      const int r = lane / CPT;
 #pragma unroll
-    for (int k = 0; k < NSP; ++k) {
-      const int tl = r + RPL * k;
-      const int t = t_first + pass * 16 + tl;
-      const u32x4 v = stage[fq_slot<D>(tl, c)];
-      if (t < n) store_nt((u32x4*)(out + (size_t)t * D + 8 * c), v);
+      for (int k = 0; k < NSP; ++k) {
+        const int tl = r + RPL * k;
+        const int t = t_first + (p0 + pass) * TPP + tl;
+        const u32x4 v = stage[fq_slot<D>(tl, c)];
+        if (t < n) store_nt((u32x4*)(out + (size_t)t * D + 8 * c), v);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   }
 }
 
 template <int D, int BITS>
 __device__ __forceinline__ void fake_kivi_keys(const uint16_t* rows, uint16_t* out,
                                                int g_first, int n, int lane) {
-  constexpr int LPR = D / 8;             // lanes per token row (8 channels each)
+  constexpr int DH = D < 128 ? D : 128;  // channels per pass (head_dim 256: two passes)
+  constexpr int LPR = DH / 8;            // lanes per token row (8 channels each)
   constexpr int RPL = 64 / LPR;          // token rows per load
   constexpr int NL = kWaveTokens / RPL;  // loads per lane
   constexpr int LEVELS = (1 << BITS) - 1;
-  const int c8 = lane % LPR;
   const int r = lane / LPR;
 
-  u32x4 raw[NL];
 #pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    const int t = min(g_first + r + RPL * k, n - 1);  // past-the-end rows: excluded below
-    raw[k] = *(const u32x4*)(rows + (size_t)t * D + 8 * c8);
-  }
-  float x[NL][8];
-#pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    x[k][0] = bf16_lo(raw[k].x); x[k][1] = bf16_hi(raw[k].x);
-    x[k][2] = bf16_lo(raw[k].y); x[k][3] = bf16_hi(raw[k].y);
-    x[k][4] = bf16_lo(raw[k].z); x[k][5] = bf16_hi(raw[k].z);
-    x[k][6] = bf16_lo(raw[k].w); x[k][7] = bf16_hi(raw[k].w);
-  }
-  GroupScale g[8];
-  float S[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    float mn = __builtin_inff(), mx = -__builtin_inff();
+  for (int h = 0; h < D / DH; ++h) {
+    const int c8 = h * LPR + lane % LPR;
+
+    u32x4 raw[NL];
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
-      const bool ok = g_first + r + RPL * k < n;
-      mn = fminf(mn, ok ? x[k][e] : __builtin_inff());
-      mx = fmaxf(mx, ok ? x[k][e] : -__builtin_inff());
+      const int t = min(g_first + r + RPL * k, n - 1);  // past-the-end rows: excluded below
+      raw[k] = *(const u32x4*)(rows + (size_t)t * D + 8 * c8);
+    }
+    float x[NL][8];
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      x[k][0] = bf16_lo(raw[k].x); x[k][1] = bf16_hi(raw[k].x);
+      x[k][2] = bf16_lo(raw[k].y); x[k][3] = bf16_hi(raw[k].y);
+      x[k][4] = bf16_lo(raw[k].z); x[k][5] = bf16_hi(raw[k].z);
+      x[k][6] = bf16_lo(raw[k].w); x[k][7] = bf16_hi(raw[k].w);
+    }
+    GroupScale g[8];
+    float S[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float mn = __builtin_inff(), mx = -__builtin_inff();
+#pragma unroll
+      for (int k = 0; k < NL; ++k) {
+        const bool ok = g_first + r + RPL * k < n;
+        mn = fminf(mn, ok ? x[k][e] : __builtin_inff());
+        mx = fmaxf(mx, ok ? x[k][e] : -__builtin_inff());
+      }
+#pragma unroll
+      for (int off = LPR; off < 64; off *= 2) {
+        mn = fminf(mn, __shfl_xor(mn, off));
+        mx = fmaxf(mx, __shfl_xor(mx, off));
+      }
+      g[e] = group_scale<LEVELS>(mn, mx);
+      S[e] = bf16_as_float(g[e].meta & 0xFFFFu);
     }
 #pragma unroll
-    for (int off = LPR; off < 64; off *= 2) {
-      mn = fminf(mn, __shfl_xor(mn, off));
-      mx = fmaxf(mx, __shfl_xor(mx, off));
+    for (int k = 0; k < NL; ++k) {
+      const int t = g_first + r + RPL * k;
+      float y[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        y[e] = __builtin_fmaf((float)(code_bits(x[k][e], g[e]) - kMagicBits), S[e], g[e].m);
+      const u32x4 v = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
+                       pack_bf16x2_hw(y[6], y[7])};
+      if (t < n) store_nt((u32x4*)(out + (size_t)t * D + 8 * c8), v);
     }
-    g[e] = group_scale<LEVELS>(mn, mx);
-    S[e] = bf16_as_float(g[e].meta & 0xFFFFu);
-  }
-#pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    const int t = g_first + r + RPL * k;
-    float y[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      y[e] = __builtin_fmaf((float)(code_bits(x[k][e], g[e]) - kMagicBits), S[e], g[e].m);
-    const u32x4 v = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
-                     pack_bf16x2_hw(y[6], y[7])};
-    if (t < n) store_nt((u32x4*)(out + (size_t)t * D + 8 * c8), v);
   }
 }
 
@@ -225,7 +236,7 @@ void fake_quantize_kernel(const Params p) {
     if (p.kivi_whole) return;  // whole-sequence key ranges: kivi_seq.hip
     fake_kivi_keys<D, BITS>(rows, out, t_first, p.n, lane);
   } else {
-    __shared__ u32x4 stage_all[kThreads / 64][16 * (D / 8)];
+    __shared__ u32x4 stage_all[kThreads / 64][(64 / kTokenLanes<D>) * (D / 8)];
     if (BASE == HG_BASE_AKVQ && sl.X == 0)
       fake_tokens<D, BITS, true, NORM>(rows, out, norm, t_first, p.n, lane, stage_all[wave]);
     else
@@ -262,6 +273,7 @@ static hipError_t launch_f_dim(const Params& p, int D, int bits, uint32_t blocks
   switch (D) {
     case 64: return launch_f_bits<BASE, 64>(p, bits, blocks, norms, stream);
     case 128: return launch_f_bits<BASE, 128>(p, bits, blocks, norms, stream);
+    case 256: return launch_f_bits<BASE, 256>(p, bits, blocks, norms, stream);
     default: return hipErrorInvalidValue;
   }
 }

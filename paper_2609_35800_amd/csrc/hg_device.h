@@ -64,6 +64,47 @@ __device__ __forceinline__ float quad_max(float v) {
   return fmaxf(v, quad_swap<kQuadXor2>(v));
 }
 
+// Row-level exchanges for a token held by a row of R = D/8 lanes (8 channels
+// per lane): partner lane = lane ^ m for m = 1, 2, 4, 8, all within one
+// 16-lane DPP row.  xor 4 composes quad reverse (lane ^ 3) with the
+// half-row mirror (lane ^ 7); xor 8 is a rotation of the row by 8.  xor 16
+// (head_dim 256) crosses DPP rows and goes through the LDS crossbar.
+constexpr int kQuadRev = 0x1B;       // quad_perm [3,2,1,0]
+constexpr int kRowHalfMirror = 0x141;
+constexpr int kRowRor8 = 0x128;
+
+template <int M>
+__device__ __forceinline__ float row_xor(float v) {
+  if constexpr (M == 1) return quad_swap<kQuadXor1>(v);
+  else if constexpr (M == 2) return quad_swap<kQuadXor2>(v);
+  else if constexpr (M == 4) return quad_swap<kRowHalfMirror>(quad_swap<kQuadRev>(v));
+  else if constexpr (M == 8) return quad_swap<kRowRor8>(v);
+  else {
+    static_assert(M == 16, "row exchange");
+    return __shfl_xor(v, 16);
+  }
+}
+
+// Minimum / maximum over the G = 4 or 8 lanes holding one token.
+template <int G>
+__device__ __forceinline__ float group_min(float v) {
+  v = quad_min(v);
+  if constexpr (G == 8) v = fminf(v, row_xor<4>(v));
+  return v;
+}
+template <int G>
+__device__ __forceinline__ float group_max(float v) {
+  v = quad_max(v);
+  if constexpr (G == 8) v = fmaxf(v, row_xor<4>(v));
+  return v;
+}
+
+// Lanes per token in the per-token compute layout: a quad up to head_dim 128
+// (D/4 elements per lane), eight lanes at 256 (32 per lane), so a lane never
+// holds more than 32 elements.
+template <int D>
+constexpr int kTokenLanes = D == 256 ? 8 : 4;
+
 // --------------------------------------------------------- group scale rule
 
 // fp32 RN(1/L) for L = 2^b - 1.
@@ -137,12 +178,12 @@ __device__ __forceinline__ uint32_t code_bits(float v, const GroupScale& g) {
 
 // ------------------------------------------------- Walsh-Hadamard transform
 
-// fp32(1/sqrt(D)) for the supported power-of-two head dims: 1/8 exactly, and
-// 1/sqrt(128) = 0.08838834764... rounded to nearest fp32.
+// fp32(1/sqrt(D)) for the supported power-of-two head dims: 1/8 and 1/16
+// exactly, and 1/sqrt(128) = 0.08838834764... rounded to nearest fp32.
 template <int D>
 __device__ __forceinline__ constexpr float fwht_scale() {
-  static_assert(D == 64 || D == 128, "head_dim");
-  return D == 64 ? 0.125f : 0x1.6a09e6p-4f;
+  static_assert(D == 64 || D == 128 || D == 256, "head_dim");
+  return D == 64 ? 0.125f : D == 128 ? 0x1.6a09e6p-4f : 0.0625f;
 }
 
 // Butterflies of spans 1 .. E/2 inside one lane's E contiguous elements.
@@ -204,12 +245,13 @@ __device__ __forceinline__ float butterfly_fma(float v, float s) {
         "+v"((x)[6]), "+v"((x)[7])                                                             \
       : "v"(s))
 
-// Full transform over D = 4E elements held by a lane quad (lane j holds
-// elements [E*j, E*j + E)): spans 1..E/2 in registers, then E (lane ^ 1) and
-// 2E (lane ^ 2), then the scale c.  Same butterfly order as spans 1..D/2.
-template <int E>
+// Full transform over D = G*E elements held by G = 4 or 8 consecutive lanes
+// (lane j of the group holds elements [E*j, E*j + E)): spans 1..E/2 in
+// registers, then E (lane ^ 1), 2E (lane ^ 2) and, for G = 8, 4E (lane ^ 4),
+// then the scale c.  Same butterfly order as spans 1..D/2.
+template <int E, int G = 4>
 __device__ __forceinline__ void fwht_quad(float (&x)[E], int j, float c) {
-  static_assert(E % 8 == 0, "whole blocks of eight");
+  static_assert(E % 8 == 0 && (G == 4 || G == 8), "whole blocks of eight; quad or octet");
   fwht_lane<E>(x);
   const float s1 = (j & 1) ? -1.0f : 1.0f;
   const float s2 = (j & 2) ? -1.0f : 1.0f;
@@ -217,28 +259,15 @@ __device__ __forceinline__ void fwht_quad(float (&x)[E], int j, float c) {
   for (int e = 0; e < E; e += 8) HG_BUTTERFLY8("quad_perm:[1,0,3,2]", x + e, s1);
 #pragma unroll
   for (int e = 0; e < E; e += 8) HG_BUTTERFLY8("quad_perm:[2,3,0,1]", x + e, s2);
-  const float cs = c * s1 * s2;  // c with the carried sign, exact
+  float cs = c * s1 * s2;  // c with the carried sign, exact
+  if constexpr (G == 8) {
+    const float s4 = (j & 4) ? -1.0f : 1.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) x[e] = __builtin_fmaf(row_xor<4>(x[e]), s4, x[e]);
+    cs = cs * s4;
+  }
 #pragma unroll
   for (int e = 0; e < E; ++e) x[e] = __builtin_fmaf(x[e], cs, 0.0f);
-}
-
-// Row-level exchanges for a token held by a row of R = D/8 lanes (8 channels
-// per lane): partner lane = lane ^ m for m = 1, 2, 4, 8, all within one
-// 16-lane DPP row.  xor 4 composes quad reverse (lane ^ 3) with the
-// half-row mirror (lane ^ 7); xor 8 is a rotation of the row by 8.
-constexpr int kQuadRev = 0x1B;       // quad_perm [3,2,1,0]
-constexpr int kRowHalfMirror = 0x141;
-constexpr int kRowRor8 = 0x128;
-
-template <int M>
-__device__ __forceinline__ float row_xor(float v) {
-  if constexpr (M == 1) return quad_swap<kQuadXor1>(v);
-  else if constexpr (M == 2) return quad_swap<kQuadXor2>(v);
-  else if constexpr (M == 4) return quad_swap<kRowHalfMirror>(quad_swap<kQuadRev>(v));
-  else {
-    static_assert(M == 8, "row exchange");
-    return quad_swap<kRowRor8>(v);
-  }
 }
 
 // Full transform over D = 8R elements held by a row of R lanes (lane c holds
@@ -253,17 +282,23 @@ __device__ __forceinline__ void fwht_row_stage(float (&x)[8], float s) {
 
 template <int D>
 __device__ __forceinline__ void fwht_row(float (&x)[8], int c) {
-  static_assert(D == 64 || D == 128, "head_dim");
+  static_assert(D == 64 || D == 128 || D == 256, "head_dim");
   fwht_lane<8>(x);
   const float s1 = (c & 1) ? -1.0f : 1.0f, s2 = (c & 2) ? -1.0f : 1.0f;
-  const float s4 = (c & 4) ? -1.0f : 1.0f, s8 = (c & 8) ? -1.0f : 1.0f;
+  const float s4 = (c & 4) ? -1.0f : 1.0f;
   fwht_row_stage<1>(x, s1);
   fwht_row_stage<2>(x, s2);
   fwht_row_stage<4>(x, s4);
   float cs = fwht_scale<D>() * s1 * s2 * s4;
-  if constexpr (D == 128) {
+  if constexpr (D >= 128) {
+    const float s8 = (c & 8) ? -1.0f : 1.0f;
     fwht_row_stage<8>(x, s8);
     cs = cs * s8;
+  }
+  if constexpr (D == 256) {
+    const float s16 = (c & 16) ? -1.0f : 1.0f;
+    fwht_row_stage<16>(x, s16);
+    cs = cs * s16;
   }
 #pragma unroll
   for (int e = 0; e < 8; ++e) x[e] = __builtin_fmaf(x[e], cs, 0.0f);
@@ -290,12 +325,14 @@ __device__ __forceinline__ float tree_sqnorm(const float (&x)[N]) {
   return a[0];
 }
 
-// A token held by a quad, lane j holding channels [j*E, (j+1)*E).
-template <int E>
+// A token held by G = 4 or 8 lanes, lane j holding channels [j*E, (j+1)*E).
+template <int E, int G = 4>
 __device__ __forceinline__ float quad_sqnorm(const float (&x)[E]) {
   float s = tree_sqnorm<E>(x);
   s = s + quad_swap<kQuadXor1>(s);
-  return s + quad_swap<kQuadXor2>(s);
+  s = s + quad_swap<kQuadXor2>(s);
+  if constexpr (G == 8) s = s + row_xor<4>(s);
+  return s;
 }
 
 // A token held by a row of D/8 lanes, lane c holding channels [8c, 8c + 8)
@@ -308,7 +345,8 @@ __device__ __forceinline__ float row_sqnorm(u32x4 v) {
   s = s + row_xor<1>(s);
   s = s + row_xor<2>(s);
   s = s + row_xor<4>(s);
-  if constexpr (D == 128) s = s + row_xor<8>(s);
+  if constexpr (D >= 128) s = s + row_xor<8>(s);
+  if constexpr (D == 256) s = s + row_xor<16>(s);
   return s;
 }
 

@@ -183,6 +183,7 @@ hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, hipStrea
   switch (D) {
     case 64: return launch_k_bits<64>(p, bits, fake, stream);
     case 128: return launch_k_bits<128>(p, bits, fake, stream);
+    case 256: return launch_k_bits<256>(p, bits, fake, stream);
     default: return hipErrorInvalidValue;
   }
 }

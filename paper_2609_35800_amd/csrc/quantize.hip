@@ -7,16 +7,18 @@
 // Work decomposition: a 256-thread workgroup owns one (tensor, l, b, h) slice
 // and 128 consecutive image tokens of it; each wavefront owns 32 tokens.
 //  - Per-token groups (min-max K and V, KIVI V, AKVQ K and V): a lane quad
-//    holds one token vector, lane j the D/4 contiguous elements
-//    [j*D/4, (j+1)*D/4) loaded with 16-byte loads; the range is reduced with
-//    two quad DPP exchanges; a lane's codes form one contiguous piece of the
-//    packed row.  A wavefront covers 16 tokens per pass, two passes.
+//    (eight lanes at head_dim 256) holds one token vector, lane j the E
+//    contiguous elements [j*E, (j+1)*E) loaded with 16-byte loads; the range
+//    is reduced with two (three) DPP exchanges; a lane's codes form one
+//    contiguous piece of the packed row.  A wavefront covers 16 (8) tokens per
+//    pass, two (four) passes.
 //  - KIVI keys: the wavefront holds one 32-token group; lanes cover D/8
-//    channel octets per token row and 64/(D/8) token rows per load, so the
-//    per-channel range over tokens is an in-register reduction plus
-//    cross-row shuffles.
-//  - AKVQ keys: the normalized Walsh-Hadamard rotation runs on the quad before
-//    the range reduction: spans 1..D/8 in registers, D/4 and D/2 by DPP.
+//    channel octets per token row (head_dim 256: one half of the channels at
+//    a time) and 64/(D/8) token rows per load, so the per-channel range over
+//    tokens is an in-register reduction plus cross-row shuffles.
+//  - AKVQ keys: the normalized Walsh-Hadamard rotation runs on the token's
+//    lanes before the range reduction: spans 1..E/2 in registers, the rest
+//    by DPP exchanges.
 //  - Protected slices: 16-byte copies of the image rows to the side store.
 //  - AKVQ-style token retention: the same pass also writes the squared norm of
 //    every image key (quad or row tree, see tree_sqnorm), before any rotation.
@@ -36,63 +38,70 @@ __device__ __forceinline__ void quantize_tokens(const uint16_t* __restrict__ row
                                                 uint32_t* __restrict__ meta,
                                                 float* __restrict__ norm,
                                                 int t_first, int n, int lane) {
-  constexpr int E = D / 4;             // elements per lane
+  constexpr int G = kTokenLanes<D>;     // lanes per token
+  constexpr int E = D / G;             // elements per lane
   constexpr int NV = E / 8;            // 16-byte loads per lane per token
+  constexpr int TPP = 64 / G;          // tokens per pass of the wavefront
+  constexpr int PASSES = kWaveTokens / TPP;
   constexpr int LEVELS = (1 << BITS) - 1;
   constexpr int ROW = D * BITS / 8;    // packed bytes per token
   constexpr int PIECE = E * BITS / 8;  // packed bytes per lane
-  const int j = lane & 3;
-  const int q = lane >> 2;
-
-  // Tokens past the span's end load the last token instead (their results are
-  // not stored), so every load is unconditional.
-  u32x4 raw[2][NV];
-#pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-    const int t = min(t_first + pass * 16 + q, n - 1);
-    const u32x4* src = (const u32x4*)(rows + (size_t)t * D + j * E);
-#pragma unroll
-    for (int k = 0; k < NV; ++k) raw[pass][k] = src[k];
-  }
+  const int j = lane % G;
+  const int q = lane / G;
 
 #pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-    const int t = t_first + pass * 16 + q;
-    float x[E];
+  for (int p0 = 0; p0 < PASSES; p0 += 2) {
+    // Two passes' loads are issued together.  Tokens past the span's end load
+    // the last token instead (their results are not stored), so every load is
+    // unconditional.
+    u32x4 raw[2][NV];
 #pragma unroll
-    for (int k = 0; k < NV; ++k) {
-      x[8 * k + 0] = bf16_lo(raw[pass][k].x);
-      x[8 * k + 1] = bf16_hi(raw[pass][k].x);
-      x[8 * k + 2] = bf16_lo(raw[pass][k].y);
-      x[8 * k + 3] = bf16_hi(raw[pass][k].y);
-      x[8 * k + 4] = bf16_lo(raw[pass][k].z);
-      x[8 * k + 5] = bf16_hi(raw[pass][k].z);
-      x[8 * k + 6] = bf16_lo(raw[pass][k].w);
-      x[8 * k + 7] = bf16_hi(raw[pass][k].w);
+    for (int b = 0; b < 2; ++b) {
+      const int t = min(t_first + (p0 + b) * TPP + q, n - 1);
+      const u32x4* src = (const u32x4*)(rows + (size_t)t * D + j * E);
+#pragma unroll
+      for (int k = 0; k < NV; ++k) raw[b][k] = src[k];
     }
-    if constexpr (NORM) {
-      const float sq = quad_sqnorm<E>(x);
-      if (t < n && j == 0) __builtin_nontemporal_store(sq, norm + t);
-    }
-    if constexpr (ROTATE) fwht_quad<E>(x, j, fwht_scale<D>());
 
-    float mn = x[0], mx = x[0];
 #pragma unroll
-    for (int e = 1; e < E; ++e) {
-      mn = fminf(mn, x[e]);
-      mx = fmaxf(mx, x[e]);
-    }
-    mn = quad_min(mn);
-    mx = quad_max(mx);
-    const GroupScale g = group_scale<LEVELS>(mn, mx);
+    for (int pass = 0; pass < 2; ++pass) {
+      const int t = t_first + (p0 + pass) * TPP + q;
+      float x[E];
+#pragma unroll
+      for (int k = 0; k < NV; ++k) {
+        x[8 * k + 0] = bf16_lo(raw[pass][k].x);
+        x[8 * k + 1] = bf16_hi(raw[pass][k].x);
+        x[8 * k + 2] = bf16_lo(raw[pass][k].y);
+        x[8 * k + 3] = bf16_hi(raw[pass][k].y);
+        x[8 * k + 4] = bf16_lo(raw[pass][k].z);
+        x[8 * k + 5] = bf16_hi(raw[pass][k].z);
+        x[8 * k + 6] = bf16_lo(raw[pass][k].w);
+        x[8 * k + 7] = bf16_hi(raw[pass][k].w);
+      }
+      if constexpr (NORM) {
+        const float sq = quad_sqnorm<E, G>(x);
+        if (t < n && j == 0) __builtin_nontemporal_store(sq, norm + t);
+      }
+      if constexpr (ROTATE) fwht_quad<E, G>(x, j, fwht_scale<D>());
 
-    uint32_t c[E];
+      float mn = x[0], mx = x[0];
 #pragma unroll
-    for (int e = 0; e < E; ++e) c[e] = code_bits(x[e], g);
-    const Packed<E, BITS> pk = pack_code_bits<E, BITS>(c);
-    if (t < n) {
-      store_packed<E, BITS>(codes + (size_t)t * ROW + j * PIECE, pk);
-      if (j == 0) __builtin_nontemporal_store(g.meta, meta + t);
+      for (int e = 1; e < E; ++e) {
+        mn = fminf(mn, x[e]);
+        mx = fmaxf(mx, x[e]);
+      }
+      mn = group_min<G>(mn);
+      mx = group_max<G>(mx);
+      const GroupScale g = group_scale<LEVELS>(mn, mx);
+
+      uint32_t c[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) c[e] = code_bits(x[e], g);
+      const Packed<E, BITS> pk = pack_code_bits<E, BITS>(c);
+      if (t < n) {
+        store_packed<E, BITS>(codes + (size_t)t * ROW + j * PIECE, pk);
+        if (j == 0) __builtin_nontemporal_store(g.meta, meta + t);
+      }
     }
   }
 }
@@ -104,61 +113,66 @@ __device__ __forceinline__ void quantize_kivi_keys(const uint16_t* __restrict__ 
                                                    uint8_t* __restrict__ codes,
                                                    uint32_t* __restrict__ meta,
                                                    int g_first, int n, int lane) {
-  constexpr int LPR = D / 8;                 // lanes per token row (8 channels each)
+  constexpr int DH = D < 128 ? D : 128;      // channels per pass (head_dim 256: two passes)
+  constexpr int LPR = DH / 8;                // lanes per token row (8 channels each)
   constexpr int RPL = 64 / LPR;              // token rows per load
   constexpr int NL = kWaveTokens / RPL;      // loads per lane
   constexpr int LEVELS = (1 << BITS) - 1;
   constexpr int ROW = D * BITS / 8;
-  const int c8 = lane % LPR;                 // channel octet
   const int r = lane / LPR;                  // token row within a load
 
-  u32x4 raw[NL];
 #pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    const int t = min(g_first + r + RPL * k, n - 1);  // past-the-end rows: excluded below
-    raw[k] = *(const u32x4*)(rows + (size_t)t * D + 8 * c8);
-  }
+  for (int h = 0; h < D / DH; ++h) {
+    const int c8 = h * LPR + lane % LPR;       // channel octet
 
-  float x[NL][8];
-#pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    x[k][0] = bf16_lo(raw[k].x); x[k][1] = bf16_hi(raw[k].x);
-    x[k][2] = bf16_lo(raw[k].y); x[k][3] = bf16_hi(raw[k].y);
-    x[k][4] = bf16_lo(raw[k].z); x[k][5] = bf16_hi(raw[k].z);
-    x[k][6] = bf16_lo(raw[k].w); x[k][7] = bf16_hi(raw[k].w);
-  }
-
-  GroupScale g[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    float mn = __builtin_inff(), mx = -__builtin_inff();
+    u32x4 raw[NL];
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
-      const bool ok = g_first + r + RPL * k < n;
-      mn = fminf(mn, ok ? x[k][e] : __builtin_inff());
-      mx = fmaxf(mx, ok ? x[k][e] : -__builtin_inff());
+      const int t = min(g_first + r + RPL * k, n - 1);  // past-the-end rows: excluded below
+      raw[k] = *(const u32x4*)(rows + (size_t)t * D + 8 * c8);
     }
+
+    float x[NL][8];
 #pragma unroll
-    for (int off = LPR; off < 64; off *= 2) {
-      mn = fminf(mn, __shfl_xor(mn, off));
-      mx = fmaxf(mx, __shfl_xor(mx, off));
+    for (int k = 0; k < NL; ++k) {
+      x[k][0] = bf16_lo(raw[k].x); x[k][1] = bf16_hi(raw[k].x);
+      x[k][2] = bf16_lo(raw[k].y); x[k][3] = bf16_hi(raw[k].y);
+      x[k][4] = bf16_lo(raw[k].z); x[k][5] = bf16_hi(raw[k].z);
+      x[k][6] = bf16_lo(raw[k].w); x[k][7] = bf16_hi(raw[k].w);
     }
-    g[e] = group_scale<LEVELS>(mn, mx);
-  }
+
+    GroupScale g[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float mn = __builtin_inff(), mx = -__builtin_inff();
+#pragma unroll
+      for (int k = 0; k < NL; ++k) {
+        const bool ok = g_first + r + RPL * k < n;
+        mn = fminf(mn, ok ? x[k][e] : __builtin_inff());
+        mx = fmaxf(mx, ok ? x[k][e] : -__builtin_inff());
+      }
+#pragma unroll
+      for (int off = LPR; off < 64; off *= 2) {
+        mn = fminf(mn, __shfl_xor(mn, off));
+        mx = fmaxf(mx, __shfl_xor(mx, off));
+      }
+      g[e] = group_scale<LEVELS>(mn, mx);
+    }
 
 #pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    const int t = g_first + r + RPL * k;
-    uint32_t cq[8];
+    for (int k = 0; k < NL; ++k) {
+      const int t = g_first + r + RPL * k;
+      uint32_t cq[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) cq[e] = code_bits(x[k][e], g[e]);
-    const Packed<8, BITS> pk = pack_code_bits<8, BITS>(cq);
-    if (t < n) store_packed<8, BITS>(codes + (size_t)t * ROW + c8 * BITS, pk);
-  }
-  if (r == 0) {
-    uint32_t* m = meta + (size_t)(g_first / kWaveTokens) * D + 8 * c8;
-    __builtin_nontemporal_store(u32x4{g[0].meta, g[1].meta, g[2].meta, g[3].meta}, (u32x4*)m);
-    __builtin_nontemporal_store(u32x4{g[4].meta, g[5].meta, g[6].meta, g[7].meta}, (u32x4*)m + 1);
+      for (int e = 0; e < 8; ++e) cq[e] = code_bits(x[k][e], g[e]);
+      const Packed<8, BITS> pk = pack_code_bits<8, BITS>(cq);
+      if (t < n) store_packed<8, BITS>(codes + (size_t)t * ROW + c8 * BITS, pk);
+    }
+    if (r == 0) {
+      uint32_t* m = meta + (size_t)(g_first / kWaveTokens) * D + 8 * c8;
+      __builtin_nontemporal_store(u32x4{g[0].meta, g[1].meta, g[2].meta, g[3].meta}, (u32x4*)m);
+      __builtin_nontemporal_store(u32x4{g[4].meta, g[5].meta, g[6].meta, g[7].meta}, (u32x4*)m + 1);
+    }
   }
 }
 
@@ -256,6 +270,7 @@ static hipError_t launch_q_dim(const Params& p, int D, int bits, uint32_t blocks
   switch (D) {
     case 64: return launch_q_bits<BASE, 64>(p, bits, blocks, norms, stream);
     case 128: return launch_q_bits<BASE, 128>(p, bits, blocks, norms, stream);
+    case 256: return launch_q_bits<BASE, 256>(p, bits, blocks, norms, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -224,6 +224,8 @@ hipError_t launch_key_norms(const Params& p, int D, hipStream_t stream) {
     hipLaunchKernelGGL((key_norm_kernel<64>), dim3(blocks), dim3(kThreads), 0, stream, p);
   else if (D == 128)
     hipLaunchKernelGGL((key_norm_kernel<128>), dim3(blocks), dim3(kThreads), 0, stream, p);
+  else if (D == 256)
+    hipLaunchKernelGGL((key_norm_kernel<256>), dim3(blocks), dim3(kThreads), 0, stream, p);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -249,6 +251,7 @@ static hipError_t launch_rows_d(const Params& p, RowCopy mode, hipStream_t strea
 hipError_t launch_retain_rows(const Params& p, int D, RowCopy mode, hipStream_t stream) {
   if (D == 64) return launch_rows_d<64>(p, mode, stream);
   if (D == 128) return launch_rows_d<128>(p, mode, stream);
+  if (D == 256) return launch_rows_d<256>(p, mode, stream);
   return hipErrorInvalidValue;
 }
 

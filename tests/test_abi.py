@@ -64,7 +64,7 @@ def test_sizes_match_oracle(seed):
     L, H = int(rng.integers(1, 9)), int(rng.integers(1, 9))
     T = int(rng.integers(1, 300))
     s0 = int(rng.integers(0, T))
-    f = _cfg(L=L, B=int(rng.integers(1, 5)), H=H, T=T, D=int(rng.choice([64, 128])),
+    f = _cfg(L=L, B=int(rng.integers(1, 5)), H=H, T=T, D=int(rng.choice([64, 128, 256])),
              img_start=s0, img_len=int(rng.integers(0, T - s0 + 1)), bits=int(rng.integers(2, 5)),
              base=int(rng.integers(0, 3)), keys_only=int(rng.integers(0, 2)))
     if f["base"] == 2:
@@ -89,7 +89,7 @@ def test_storage_model_bits_per_element():
 BAD = [
     (dict(L=0), hg.HG_ERR_SHAPE), (dict(B=-1), hg.HG_ERR_SHAPE), (dict(T=0), hg.HG_ERR_SHAPE),
     (dict(L=128, H=65), hg.HG_ERR_SHAPE), (dict(keys_only=2), hg.HG_ERR_SHAPE),
-    (dict(D=96), hg.HG_ERR_HEADDIM), (dict(D=256), hg.HG_ERR_HEADDIM),
+    (dict(D=96), hg.HG_ERR_HEADDIM), (dict(D=512), hg.HG_ERR_HEADDIM), (dict(D=32), hg.HG_ERR_HEADDIM),
     (dict(img_start=-1), hg.HG_ERR_SPAN), (dict(img_start=20, img_len=21), hg.HG_ERR_SPAN),
     (dict(img_len=-3), hg.HG_ERR_SPAN),
     (dict(bits=1), hg.HG_ERR_BITS), (dict(bits=5), hg.HG_ERR_BITS),

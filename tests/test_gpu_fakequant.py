@@ -51,7 +51,7 @@ def check(w, K, V, mask, inplace):
     assert np.array_equal(gV, oV), (w.name, int(np.count_nonzero(gV != oV)))
 
 
-CASES = [small(b, D, bits, ko) for b in ("minmax", "kivi", "akvq") for D in (64, 128)
+CASES = [small(b, D, bits, ko) for b in ("minmax", "kivi", "akvq") for D in (64, 128, 256)
          for bits in (2, 3, 4) for ko in (0, 1)]
 
 

@@ -16,7 +16,7 @@ from test_gpu_parity import _assert_exact, small
 pytestmark = pytest.mark.gpu
 
 CASES = [small("kivi", D, bits, ko).with_(kivi_group=0, name=f"kiviseq-D{D}-b{bits}-ko{ko}")
-         for D in (64, 128) for bits in (2, 3, 4) for ko in (0, 1)]
+         for D in (64, 128, 256) for bits in (2, 3, 4) for ko in (0, 1)]
 
 
 @pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)

@@ -37,7 +37,7 @@ def small(base, D=128, bits=2, keys_only=0, img_len=300, img_start=7, text=13, L
 
 
 CASES = [small(b, D, bits, ko)
-         for b in ("minmax", "kivi", "akvq") for D in (64, 128) for bits in (2, 3, 4)
+         for b in ("minmax", "kivi", "akvq") for D in (64, 128, 256) for bits in (2, 3, 4)
          for ko in (0, 1)]
 
 

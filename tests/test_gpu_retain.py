@@ -29,7 +29,7 @@ def retain_case(D=128, bits=2, keys_only=0, permille=20, img_len=600, **kw):
     return w.with_(retain_permille=permille, name=w.name + f"-r{permille}")
 
 
-CASES = [retain_case(D, bits, ko, pm) for D in (64, 128) for bits in (2, 3, 4) for ko in (0, 1)
+CASES = [retain_case(D, bits, ko, pm) for D in (64, 128, 256) for bits in (2, 3, 4) for ko in (0, 1)
          for pm in (20, 100)]
 
 
@@ -66,7 +66,7 @@ def _integer_kv(w, lo, hi, seed):
     return K, V
 
 
-@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("D", [64, 128, 256])
 @pytest.mark.parametrize("spread", [1, 3])
 def test_ties_go_to_the_lower_token(D, spread):
     """Entries in {-spread..spread}: key norms are small integers, so most
@@ -115,7 +115,7 @@ def test_empty_span():
 
 # ---------------------------------------------------------------- one pass
 
-FAKE_CASES = [retain_case(D, bits, ko, pm, img_len=400) for D in (64, 128) for bits in (2, 4)
+FAKE_CASES = [retain_case(D, bits, ko, pm, img_len=400) for D in (64, 128, 256) for bits in (2, 4)
               for ko in (0, 1) for pm in (20, 250)]
 
 

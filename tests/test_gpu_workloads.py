@@ -96,7 +96,8 @@ def _check_workload(w):
             assert np.array_equal(grec, orec), (X, l, b, h)
 
 
-@pytest.mark.parametrize("name", ["tiny", "qwen2.5-vl-7b", "llava-next-7b", "internvl-8b"])
+@pytest.mark.parametrize("name", ["tiny", "qwen2.5-vl-7b", "llava-next-7b", "internvl-8b", "gemma-3-12b",
+                                  "72b-long-tp8"])
 def test_workload(name):
     _check_workload(synthkv.WORKLOADS[name])
     torch.cuda.empty_cache()

@@ -199,7 +199,7 @@ def test_fwht_matches_explicit_matrix(D):
         assert np.all(np.abs(got - exact) <= bound)
 
 
-@pytest.mark.parametrize("D", [4, 16, 64, 128])
+@pytest.mark.parametrize("D", [4, 16, 64, 128, 256])
 def test_fwht_integer_identities(D):
     rng = np.random.default_rng(3 * D)
     x = rng.integers(-1000, 1000, D).astype(np.float32)
@@ -211,7 +211,7 @@ def test_fwht_integer_identities(D):
     assert np.all(ones[1:] == 0)
 
 
-@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("D", [64, 128, 256])
 def test_fwht_orthonormal_round_trip(D):
     rng = np.random.default_rng(5)
     for _ in range(50):

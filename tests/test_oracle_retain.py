@@ -81,7 +81,7 @@ def test_retention_needs_the_akvq_base():
 
 # ---------------------------------------------------------------- the norm
 
-@pytest.mark.parametrize("D,want", [(64, 2.0 ** 24 + 62), (128, 2.0 ** 24 + 126)])
+@pytest.mark.parametrize("D,want", [(64, 2.0 ** 24 + 62), (128, 2.0 ** 24 + 126), (256, 2.0 ** 24 + 254)])
 @pytest.mark.parametrize("where", [0, -1, 17])
 def test_sqnorm_pairwise_order(D, want, where):
     """One entry 2^12 (square 2^24) among ones.  Worked by hand: the first pair
@@ -95,7 +95,7 @@ def test_sqnorm_pairwise_order(D, want, where):
     assert got == want
 
 
-@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("D", [64, 128, 256])
 def test_sqnorm_exact_for_small_integers(D):
     """Integer entries |x| <= 15: every square and partial sum is an integer
     below 2^24, so the fp32 result is the exact sum."""
@@ -105,7 +105,7 @@ def test_sqnorm_exact_for_small_integers(D):
         assert oracle.key_sqnorm(_bf16_of(x)) == float(np.sum(x.astype(np.int64) ** 2))
 
 
-@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("D", [64, 128, 256])
 def test_sqnorm_within_pairwise_error_bound(D):
     """BF16 squares are exact in fp32 (8-bit significands); pairwise summation
     over log2(D) levels errs by at most gamma_{log2 D} times the exact sum."""
