@@ -19,7 +19,8 @@ namespace hg {
 // Per-token groups.  A token row is held by D/8 lanes, lane c holding
 // channels [8c, 8c + 8), so each 16-byte store instruction of the wavefront
 // writes 64/(D/8) whole consecutive token rows (one contiguous 1 KiB run for
-// D = 128).  AKVQ keys are rotated back across the row's lanes first.
+// D = 128; two 512-byte rows at 256).  AKVQ keys are rotated back across the
+// row's lanes first.
 template <int D, int BITS, bool ROTATE>
 __device__ __forceinline__ void dequantize_tokens(const uint8_t* __restrict__ codes,
                                                   const uint32_t* __restrict__ meta,
