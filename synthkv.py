@@ -73,7 +73,8 @@ class Workload:
 
 # The five workloads: a tiny case, then caches shaped like the paper's 7B-72B
 # VLMs (Qwen2.5-VL-7B, LLaVA-NeXT-7B, InternVL3-8B, a 72B model) with image
-# spans of 1296-6400 tokens; a Gemma-3-12B-shaped cache (head_dim 256); and
+# spans of 1296-6400 tokens; LLaVA-1.5-7B- and Gemma-3-12B-shaped caches
+# (576-token spans; head_dim 256); and
 # one GPU's share of the 72B cache under an eight-way split by KV head.
 WORKLOADS: Dict[str, Workload] = {
     "tiny": Workload("tiny", L=2, B=1, H=4, T=288, D=64, img_start=16, img_len=256,
@@ -94,6 +95,10 @@ WORKLOADS: Dict[str, Workload] = {
     "72b-long": Workload("72b-long", L=80, B=2, H=8, T=6656, D=128, img_start=128,
                          img_len=6400, bits=2, base="minmax", keys_only=0,
                          n_protected=80, k_outliers=8, k_outlier_scale=20.0),
+    # LLaVA-1.5-7B-shaped: 32 KV heads (no grouping), one 576-token image
+    "llava-1.5-7b": Workload("llava-1.5-7b", L=32, B=16, H=32, T=640, D=128, img_start=32,
+                             img_len=576, bits=2, base="minmax", keys_only=0, n_protected=128,
+                             k_outliers=4, k_outlier_scale=10.0),
     # Gemma-3-12B-shaped: head_dim 256, one 256-token image per prompt
     "gemma-3-12b": Workload("gemma-3-12b", L=48, B=32, H=8, T=320, D=256, img_start=32,
                             img_len=256, bits=2, base="minmax", keys_only=0, n_protected=48,

@@ -97,7 +97,7 @@ def _check_workload(w):
 
 
 @pytest.mark.parametrize("name", ["tiny", "qwen2.5-vl-7b", "llava-next-7b", "internvl-8b", "gemma-3-12b",
-                                  "72b-long-tp8"])
+                                  "llava-1.5-7b", "72b-long-tp8"])
 def test_workload(name):
     _check_workload(synthkv.WORKLOADS[name])
     torch.cuda.empty_cache()
