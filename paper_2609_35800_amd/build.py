@@ -26,17 +26,31 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
+# AddressSanitizer on the host side only (argument checks, sizes, routing,
+# head selection); the device code is built as usual.
+HOST_ASAN = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def build(verbose: bool = False, out: str = LIB, host_asan: bool = False) -> str:
     """Compile the library (always) and return its path."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB + ".tmp"
-    cmd = [hipcc, *FLAGS, "-o", tmp] + [os.path.join(CSRC, s) for s in SOURCES]
+    tmp = out + ".tmp"
+    cmd = [hipcc, *FLAGS, *(HOST_ASAN if host_asan else []), "-o", tmp] + \
+          [os.path.join(CSRC, s) for s in SOURCES]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    import argparse
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--host-asan", metavar="OUT",
+                    help="build a copy with host-side AddressSanitizer at OUT instead")
+    a = ap.parse_args()
+    if a.host_asan:
+        print(build(verbose=True, out=a.host_asan, host_asan=True))
+    else:
+        print(build(verbose=True))
