@@ -25,8 +25,16 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 QUANT_KERNEL = "quantize_kernel"
-KERNEL_SOURCES = ("paper_2609_35800_amd/csrc/quantize.hip", "paper_2609_35800_amd/csrc/hg_device.h",
-                  "paper_2609_35800_amd/csrc/hg_kernels.h")
+FAKE_KERNEL = "fake_quantize_kernel"
+_CSRC = "paper_2609_35800_amd/csrc/"
+# the device sources that decide what each timed call reads and writes; a
+# counter measurement is reported only while their text is unchanged
+KERNEL_SOURCES = {
+    QUANT_KERNEL: tuple(_CSRC + f for f in ("quantize.hip", "kivi_seq.hip", "retain.hip",
+                                              "hg_device.h", "hg_kernels.h")),
+    FAKE_KERNEL: tuple(_CSRC + f for f in ("fakequant.hip", "retain.hip", "hg_device.h",
+                                             "hg_kernels.h")),
+}
 
 
 def parse():
@@ -54,23 +62,35 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(kernel: str = QUANT_KERNEL) -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in KERNEL_SOURCES[kernel]:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(workload: str, bits: int):
-    """HBM bytes per quantize launch measured by rocprofv3 counters, if the
-    committed measurement was taken on the current kernel sources."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{QUANT_KERNEL}_{workload}_b{bits}.json")
+def variant_name(w) -> str:
+    """Workload name plus the options that change which kernels run:
+    e.g. qwen2.5-vl-7b_b2, llava-next-7b_kivi-whole_b2, internvl-8b_retain20_b2."""
+    name = w.name
+    if w.base == "kivi" and w.kivi_group == 0:
+        name += "_kivi-whole"
+    if w.retain_permille:
+        name += f"_retain{w.retain_permille}"
+    return f"{name}_b{w.bits}"
+
+
+def traffic_from_profile(w, kernel: str = QUANT_KERNEL):
+    """HBM bytes per call (all kernels of the timed call) measured by the
+    rocprofv3 FETCH_SIZE and WRITE_SIZE counters, if a committed measurement
+    of this workload variant exists and was taken on the current sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{variant_name(w)}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("kernel_source_hash") != kernel_source_hash():
+    if rec.get("kernel_source_hash") != kernel_source_hash(kernel):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -145,6 +165,26 @@ def cpu_baseline(w, K, V, mask, budget_s: float, threads: int = 0):
             "image_tokens_per_s": round(w.B * w.img_len * nl / w.L / per_pass, 1)}
 
 
+def device_copy_gbps(stream) -> float:
+    """A plain device-to-device copy of 1 GiB on the same stream: the practical
+    bandwidth the kernels are compared with besides the vendor peak (its
+    rocprofv3 counters also scale FETCH_SIZE and WRITE_SIZE to bytes)."""
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    cev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(5)]
+    for e0, e1 in cev:
+        e0.record(stream)
+        b.copy_(a)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in cev]))
+    del a, b
+    return 2 * n / (ms * 1e-3) / 1e9
+
+
 def bench_fakequant(args, hg, w, cfg, mask, K, V):
     """One-pass simulated quantization, out of place: every image row of K and
     V is read once and written once (protected rows copied)."""
@@ -166,6 +206,7 @@ def bench_fakequant(args, hg, w, cfg, mask, K, V):
     ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
     nbytes = 2 * (2 * w.L * w.B * w.H * w.img_len * w.D * 2)
     gbps = nbytes / (ms * 1e-3) / 1e9
+    copy_gbps = device_copy_gbps(stream)
     print(json.dumps({
         "metric": "fake-quantize (one-pass simulated quantization) HBM GB/s",
         "value": round(nbytes * args.steps / elapsed / 1e9, 2), "unit": "GB/s", "n_gpus": 1,
@@ -176,9 +217,12 @@ def bench_fakequant(args, hg, w, cfg, mask, K, V):
                    **({"kivi_group": w.kivi_group} if w.base == "kivi" else {}),
                    **({"retain_permille": w.retain_permille} if w.retain_permille else {})},
         "image_tokens_per_s": round(w.B * w.img_len / (ms * 1e-3), 1),
-        "roofline": {"bound": "hbm", "kernel": "fake_quantize_kernel", "achieved": round(gbps, 1),
+        "device_copy_GBps": round(copy_gbps, 1),
+        "pct_of_device_copy": round(100 * gbps / copy_gbps, 1),
+        "roofline": {"bound": "hbm", "kernel": FAKE_KERNEL, "achieved": round(gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
-                     "bytes_per_launch": nbytes, "ms": round(ms, 4)},
+                     "bytes_per_launch": nbytes, "ms": round(ms, 4),
+                     "traffic": traffic_from_profile(w, FAKE_KERNEL)},
     }), flush=True)
 
 
@@ -245,22 +289,9 @@ def main():
     value = step_bytes * args.steps / elapsed / 1e9
     q_gbps = ab["quant"] / (q_avg * 1e-3) / 1e9
     d_gbps = ab["dequant"] / (d_avg * 1e-3) / 1e9 if not args.quant_only else None
-    traffic = traffic_from_profile(w.name, w.bits)
+    traffic = traffic_from_profile(w)
 
-    # a plain device-to-device copy of 1 GiB on the same stream: the practical
-    # bandwidth the quantizer is compared with besides the vendor peak
-    n = 1 << 30
-    a = torch.empty(n, dtype=torch.uint8, device="cuda")
-    b = torch.empty_like(a)
-    b.copy_(a)
-    cev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(5)]
-    for e0, e1 in cev:
-        e0.record(stream)
-        b.copy_(a)
-        e1.record(stream)
-    torch.cuda.synchronize()
-    copy_gbps = 2 * n / (float(np.mean([e0.elapsed_time(e1) for e0, e1 in cev])) * 1e-3) / 1e9
-    del a, b
+    copy_gbps = device_copy_gbps(stream)
 
     out = {
         "metric": "quantize+pack+dequant HBM GB/s (% of MI355X peak); image KV tokens/s",

@@ -284,8 +284,7 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
                           : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream);
   if (e == hipSuccess && quantize && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, false, stream);
   if (e == hipSuccess && p.k > 0 && quantize) {
-    e = hg::launch_retain_select(p, stream);
-    if (e == hipSuccess) e = hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kGather, stream);
+    e = hg::launch_retain_select(p, cfg->D, hg::RowCopy::kGather, stream);
   }
   if (e == hipSuccess && p.k > 0 && !quantize) e = hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kScatter, stream);
   if (e != hipSuccess) return fail(HG_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
@@ -362,16 +361,14 @@ int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
     p.k = z.retain_count;
     if (!fused) {
       e = hg::launch_key_norms(p, cfg->D, stream);
-      if (e == hipSuccess) e = hg::launch_retain_select(p, stream);
-      if (e == hipSuccess) e = hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kGather, stream);
+      if (e == hipSuccess) e = hg::launch_retain_select(p, cfg->D, hg::RowCopy::kGather, stream);
     }
   }
   if (e == hipSuccess)
     e = hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), fused, stream);
   if (e == hipSuccess && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, true, stream);
   if (e == hipSuccess && fused) {
-    e = hg::launch_retain_select(p, stream);
-    if (e == hipSuccess) e = hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kCacheToOut, stream);
+    e = hg::launch_retain_select(p, cfg->D, hg::RowCopy::kCacheToOut, stream);
   } else if (e == hipSuccess && retain) {
     e = hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kScatter, stream);
   }

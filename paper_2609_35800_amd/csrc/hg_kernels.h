@@ -63,10 +63,11 @@ hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, hipStrea
 // Token retention: squared key norms of every image token (p.norm); the k
 // largest per (l, b, h) into p.ret_idx; their rows gathered from p.cache into
 // p.ret, written back from p.ret into p.out, or copied from p.cache straight
-// into p.out.
+// into p.out.  The selection copies the rows it selects (kGather or
+// kCacheToOut) in the same launch.
 hipError_t launch_key_norms(const Params& p, int D, hipStream_t stream);
-hipError_t launch_retain_select(const Params& p, hipStream_t stream);
 enum class RowCopy { kGather, kScatter, kCacheToOut };
+hipError_t launch_retain_select(const Params& p, int D, RowCopy mode, hipStream_t stream);
 hipError_t launch_retain_rows(const Params& p, int D, RowCopy mode, hipStream_t stream);
 
 // Routing of one (tensor, slice): whether it is kept in BF16 and its slot in

@@ -9,12 +9,15 @@
 // (l, b, h):
 //  - retain_select_kernel (norms staged in LDS) finds the k-th largest norm by
 //    a most-significant-digit-first radix select over the fp32 bit patterns
-//    (non-negative, so they order as unsigned integers) and lists the retained
-//    tokens in ascending order (all larger norms, then the lowest-index ties);
-//  - retain_rows_kernel gathers their K and V rows for each tensor the head
-//    does not keep in BF16, or writes them back over the reconstruction; an
-//    out-of-place one-pass call, which computes the norms in its own pass,
-//    copies them from the input straight to the output.
+//    (non-negative, so they order as unsigned integers), starting below the
+//    bits every norm of the head shares and stopping once the chosen digit's
+//    candidates are all taken; lists the retained tokens in ascending order
+//    (all larger norms, then the lowest-index ties); and, in the same
+//    workgroup, gathers their K and V rows for each tensor the head does not
+//    keep in BF16 (an out-of-place one-pass call, which computes the norms in
+//    its own pass, copies them from the input straight to the output);
+//  - retain_rows_kernel writes the gathered rows back over the
+//    reconstruction.
 
 #include "hg_device.h"
 #include "hg_kernels.h"
@@ -57,14 +60,72 @@ __global__ __launch_bounds__(kThreads) void key_norm_kernel(const Params p) {
 // Keys held in LDS by the selection when the span fits this many tokens;
 // longer spans read them from global memory (L2) in every pass.
 constexpr int kResidentKeys = 12288;
+constexpr int kRowsInFlight = 8;  // 16-byte row pieces in flight per thread when copying rows
 
-// One workgroup per (l, b, h); requires 1 <= k <= n.  Writes ret_idx only.
-template <bool RESIDENT>
+// Copies the k retained rows of every tensor the head does not keep in BF16:
+// kGather from p.cache into p.ret, kScatter from p.ret over p.out's image
+// rows, kCacheToOut from p.cache straight into p.out.  `idx` lists the rows;
+// an entry outside the span is not stored.
+template <int D, RowCopy MODE>
+__device__ __forceinline__ void copy_retained_rows(const Params& p, uint32_t s, const int32_t* idx) {
+  constexpr int VPT = D / 8;  // 16-byte vectors per row
+  constexpr int U = kRowsInFlight;
+  const uint32_t k = (uint32_t)p.k;
+  const size_t span = ((size_t)s * p.T + p.s0) * D;
+  // sources and destinations of the tensors to copy: the first one not kept
+  // in BF16, then V when both are copied
+  const uint16_t* src[2];
+  uint16_t* dst[2];
+#pragma unroll
+  for (int X = 0; X < 2; ++X) {
+    const SliceRoute r = route_slice(p, X, s);
+    uint16_t* ret = MODE == RowCopy::kCacheToOut ? nullptr : p.ret[X] + ((size_t)r.slot * p.B + r.b) * k * D;
+    src[X] = MODE == RowCopy::kScatter ? ret : p.cache[X] + span;
+    dst[X] = MODE == RowCopy::kGather ? ret : p.out[X] + span;
+  }
+  const bool k_kept = route_slice(p, 0, s).kept, v_kept = route_slice(p, 1, s).kept;
+  const int nx = (k_kept ? 0 : 1) + (v_kept ? 0 : 1);
+  if (k_kept) {
+    src[0] = src[1];
+    dst[0] = dst[1];
+  }
+  // row pieces of the first tensor, then of the second; retained-row buffers
+  // are indexed by list position, image rows by token
+  const uint32_t per = k * VPT, total = (uint32_t)nx * per;
+  for (uint32_t i0 = threadIdx.x; i0 < total; i0 += U * kThreads) {
+    u32x4 v[U];
+    uint32_t tok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t i = min(i0 + u * kThreads, total - 1);
+      const bool second = i >= per;
+      const uint32_t e = second ? i - per : i, row = e / VPT, c = e % VPT;
+      tok[u] = (uint32_t)idx[row];
+      const uint32_t t = min(tok[u], (uint32_t)p.n - 1);
+      const uint32_t at = MODE == RowCopy::kScatter ? row : t;
+      v[u] = *(const u32x4*)((second ? src[1] : src[0]) + (size_t)at * D + 8 * c);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t i = i0 + u * kThreads;
+      if (i >= total || tok[u] >= (uint32_t)p.n) continue;
+      const bool second = i >= per;
+      const uint32_t e = second ? i - per : i, row = e / VPT, c = e % VPT;
+      const uint32_t at = MODE == RowCopy::kGather ? row : tok[u];
+      store_nt((u32x4*)((second ? dst[1] : dst[0]) + (size_t)at * D + 8 * c), v[u]);
+    }
+  }
+}
+
+// One workgroup per (l, b, h); requires 1 <= k <= n.  Writes ret_idx, then
+// copies the retained rows (kGather or kCacheToOut).
+template <bool RESIDENT, int D, RowCopy MODE>
 __global__ __launch_bounds__(kThreads) void retain_select_kernel(const Params p) {
+  static_assert(kThreads == 256, "one histogram bin per thread");
   constexpr int WAVES = kThreads / 64;
   extern __shared__ uint32_t lds_keys[];  // n keys when RESIDENT
   __shared__ uint32_t hist[256];
-  __shared__ uint32_t pick[2];
+  __shared__ uint32_t pick[3];
   __shared__ uint32_t wsum[WAVES][2];
 
   const uint32_t s = blockIdx.x;  // (l*B + b)*H + h
@@ -72,22 +133,51 @@ __global__ __launch_bounds__(kThreads) void retain_select_kernel(const Params p)
   const uint32_t k = (uint32_t)p.k;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint32_t* gkeys = (const uint32_t*)(p.norm + (size_t)s * n);
-  if constexpr (RESIDENT) {
-    for (int t0 = tid; t0 < n; t0 += 4 * kThreads) {
-      uint32_t u[4];
+  uint32_t vmax = 0, vmin = ~0u;
+  for (int t0 = tid; t0 < n; t0 += 4 * kThreads) {
+    uint32_t u[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) u[i] = gkeys[min(t0 + i * kThreads, n - 1)];
+    for (int i = 0; i < 4; ++i) u[i] = gkeys[min(t0 + i * kThreads, n - 1)];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (t0 + i * kThreads < n) lds_keys[t0 + i * kThreads] = u[i];
+    for (int i = 0; i < 4; ++i) {
+      vmax = max(vmax, u[i]);  // clamped repeats of key n-1 change neither bound
+      vmin = min(vmin, u[i]);
+      if (RESIDENT && t0 + i * kThreads < n) lds_keys[t0 + i * kThreads] = u[i];
     }
   }
   const uint32_t* key = RESIDENT ? lds_keys : gkeys;
 
-  // 1. The k-th largest key: one 8-bit digit per pass from the top.  `want` is
-  //    how many of the candidates sharing `prefix` are still to be taken.
-  uint32_t prefix = 0, pmask = 0, want = k;
-  for (int shift = 24; shift >= 0; shift -= 8) {
+  // 0. Bounds of the keys: the bits above the highest bit in which the largest
+  //    and smallest keys differ are common to every key, so the digits start
+  //    below them.
+#pragma unroll
+  for (int off = 1; off < 64; off *= 2) {
+    vmax = max(vmax, (uint32_t)__shfl_xor((int)vmax, off));
+    vmin = min(vmin, (uint32_t)__shfl_xor((int)vmin, off));
+  }
+  if (lane == 0) {
+    wsum[wave][0] = vmax;
+    wsum[wave][1] = vmin;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    vmax = max(vmax, wsum[w][0]);
+    vmin = min(vmin, wsum[w][1]);
+  }
+  const uint32_t diff = vmax ^ vmin;
+  const int hb = diff ? 32 - __clz((int)diff) : 0;  // low bits that vary between keys
+  uint32_t pmask = hb == 32 ? 0u : ~((1u << hb) - 1u);
+
+  // 1. The k-th largest key, one 8-bit digit per pass from the top of the
+  //    varying bits.  Candidates are the keys that match `prefix` under
+  //    `pmask`; `want` of them are still to be taken.  The passes end once the
+  //    digits are exhausted or every candidate of the chosen digit is taken
+  //    (then no key outside the candidates ties with them).
+  uint32_t prefix = vmax & pmask, want = k;
+  bool done = hb == 0;  // all keys equal
+  for (int shift = hb - 8; !done; shift -= 8) {
+    shift = max(shift, 0);  // the last digit may repeat already fixed bits
     hist[tid] = 0;
     __syncthreads();
     for (int t = tid; t < n; t += kThreads) {
@@ -115,6 +205,7 @@ __global__ __launch_bounds__(kThreads) void retain_select_kernel(const Params p)
         if (above < want && above + cnt[i] >= want) {
           pick[0] = 255u - 4u * lane - i;
           pick[1] = want - above;
+          pick[2] = cnt[i];
         }
         above += cnt[i];
       }
@@ -123,22 +214,23 @@ __global__ __launch_bounds__(kThreads) void retain_select_kernel(const Params p)
     prefix |= pick[0] << shift;
     pmask |= 255u << shift;
     want = pick[1];
+    done = shift == 0 || pick[1] == pick[2];
   }
-  const uint32_t thr = prefix;  // the k-th largest key
-  const uint32_t need = want;   // keys equal to thr that are retained (lowest indices)
+  const uint32_t need = want;  // keys matching prefix that are retained (lowest indices)
 
-  // 2. Retained tokens in ascending order.  Each thread owns a contiguous run
-  //    of tokens; a block-wide exclusive scan of the per-run counts of larger
-  //    and equal keys gives every run its starting counts, and the position of
-  //    a retained token is (larger keys before it) + min(equal keys before it,
-  //    need).
+  // 2. Retained tokens in ascending order: every key above prefix under pmask,
+  //    then the first `need` matching it.  Each thread owns a contiguous run of
+  //    tokens; a block-wide exclusive scan of the per-run counts of larger and
+  //    matching keys gives every run its starting counts, and the position of
+  //    a retained token is (larger keys before it) + min(matching keys before
+  //    it, need).
   const int run = (n + kThreads - 1) / kThreads;
   const int t_lo = min(tid * run, n), t_hi = min(t_lo + run, n);
   uint32_t cg = 0, ce = 0;
   for (int t = t_lo; t < t_hi; ++t) {
-    const uint32_t u = key[t];
-    cg += u > thr;
-    ce += u == thr;
+    const uint32_t u = key[t] & pmask;
+    cg += u > prefix;
+    ce += u == prefix;
   }
   uint32_t ig = cg, ie = ce;  // inclusive scans within the wavefront
 #pragma unroll
@@ -164,56 +256,27 @@ __global__ __launch_bounds__(kThreads) void retain_select_kernel(const Params p)
   }
   int32_t* idx = p.ret_idx + (size_t)s * k;
   for (int t = t_lo; t < t_hi; ++t) {
-    const uint32_t u = key[t];
-    const bool gt = u > thr, eq = u == thr;
+    const uint32_t u = key[t] & pmask;
+    const bool gt = u > prefix, eq = u == prefix;
     const uint32_t pos = pg + min(pe, need);
     if ((gt || (eq && pe < need)) && pos < k) idx[pos] = t;  // exactly k positions are taken
     pg += gt;
     pe += eq;
   }
+
+  // 3. The retained rows, read back from the list just written (a workgroup
+  //    barrier makes the global stores visible within the workgroup).
+  __syncthreads();
+  copy_retained_rows<D, MODE>(p, s, idx);
 }
 
 // ------------------------------------------------------------ retained rows
 
-// Grid (l*B*H, 2): one workgroup per (l, b, h) and tensor, skipping tensors the
-// head keeps in BF16.  kGather copies the retained image rows of p.cache into
-// p.ret, kScatter writes p.ret back over p.out's image rows, kCacheToOut copies
-// them from p.cache to p.out directly.
+// Grid l*B*H: the retained rows of one (l, b, h) per workgroup, listed in
+// p.ret_idx (the dequantize direction, and an in-place one-pass call).
 template <int D, RowCopy MODE>
 __global__ __launch_bounds__(kThreads) void retain_rows_kernel(const Params p) {
-  constexpr int VPT = D / 8;  // 16-byte vectors per row
-  constexpr int U = 4;        // vectors in flight per thread
-  const uint32_t s = blockIdx.x;
-  const int X = blockIdx.y;
-  const SliceRoute r = route_slice(p, X, s);
-  if (r.kept) return;
-  const uint32_t k = (uint32_t)p.k;
-  const int32_t* idx = p.ret_idx + (size_t)s * k;
-  uint16_t* ret = MODE == RowCopy::kCacheToOut ? nullptr : p.ret[X] + ((size_t)r.slot * p.B + r.b) * k * D;
-  const size_t span = ((size_t)s * p.T + p.s0) * D;
-  const uint32_t total = k * VPT;
-  for (uint32_t i0 = threadIdx.x; i0 < total; i0 += U * kThreads) {
-    u32x4 v[U];
-    uint32_t tok[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t i = min(i0 + u * kThreads, total - 1);
-      const uint32_t row = i / VPT, c = i % VPT;
-      tok[u] = (uint32_t)idx[row];
-      const uint32_t t = min(tok[u], (uint32_t)p.n - 1);  // an out-of-span entry is not stored
-      v[u] = MODE == RowCopy::kScatter ? *(const u32x4*)(ret + (size_t)row * D + 8 * c)
-                                       : *(const u32x4*)(p.cache[X] + span + (size_t)t * D + 8 * c);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t i = i0 + u * kThreads;
-      if (i >= total || tok[u] >= (uint32_t)p.n) continue;
-      const uint32_t row = i / VPT, c = i % VPT;
-      u32x4* dst = MODE == RowCopy::kGather ? (u32x4*)(ret + (size_t)row * D + 8 * c)
-                                            : (u32x4*)(p.out[X] + span + (size_t)tok[u] * D + 8 * c);
-      store_nt(dst, v[u]);
-    }
-  }
+  copy_retained_rows<D, MODE>(p, blockIdx.x, p.ret_idx + (size_t)blockIdx.x * (uint32_t)p.k);
 }
 
 // ------------------------------------------------------------ launchers
@@ -233,7 +296,7 @@ hipError_t launch_key_norms(const Params& p, int D, hipStream_t stream) {
 
 template <int D>
 static hipError_t launch_rows_d(const Params& p, RowCopy mode, hipStream_t stream) {
-  const dim3 grid((uint32_t)p.L * p.B * p.H, 2);
+  const dim3 grid((uint32_t)p.L * p.B * p.H);
   switch (mode) {
     case RowCopy::kGather:
       hipLaunchKernelGGL((retain_rows_kernel<D, RowCopy::kGather>), grid, dim3(kThreads), 0, stream, p);
@@ -255,13 +318,34 @@ hipError_t launch_retain_rows(const Params& p, int D, RowCopy mode, hipStream_t 
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_retain_select(const Params& p, hipStream_t stream) {
-  const uint32_t blocks = (uint32_t)p.L * p.B * p.H;
-  if (p.n <= kResidentKeys)
-    hipLaunchKernelGGL((retain_select_kernel<true>), dim3(blocks), dim3(kThreads),
-                       (size_t)p.n * sizeof(uint32_t), stream, p);
+template <bool RESIDENT, int D>
+static void launch_select_r(const Params& p, RowCopy mode, dim3 grid, size_t lds, hipStream_t stream) {
+  if (mode == RowCopy::kGather)
+    hipLaunchKernelGGL((retain_select_kernel<RESIDENT, D, RowCopy::kGather>), grid, dim3(kThreads), lds, stream, p);
   else
-    hipLaunchKernelGGL((retain_select_kernel<false>), dim3(blocks), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL((retain_select_kernel<RESIDENT, D, RowCopy::kCacheToOut>), grid, dim3(kThreads), lds,
+                       stream, p);
+}
+
+template <int D>
+static void launch_select_d(const Params& p, RowCopy mode, hipStream_t stream) {
+  const dim3 grid((uint32_t)p.L * p.B * p.H);
+  if (p.n <= kResidentKeys)
+    launch_select_r<true, D>(p, mode, grid, (size_t)p.n * sizeof(uint32_t), stream);
+  else
+    launch_select_r<false, D>(p, mode, grid, 0, stream);
+}
+
+hipError_t launch_retain_select(const Params& p, int D, RowCopy mode, hipStream_t stream) {
+  if (mode == RowCopy::kScatter) return hipErrorInvalidValue;
+  if (D == 64)
+    launch_select_d<64>(p, mode, stream);
+  else if (D == 128)
+    launch_select_d<128>(p, mode, stream);
+  else if (D == 256)
+    launch_select_d<256>(p, mode, stream);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
