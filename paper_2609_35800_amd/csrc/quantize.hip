@@ -48,6 +48,8 @@ __device__ __forceinline__ void quantize_tokens(const uint16_t* __restrict__ row
   constexpr int PIECE = E * BITS / 8;  // packed bytes per lane
   const int j = lane % G;
   const int q = lane / G;
+  uint32_t mw[PASSES];  // metadata word of this lane's token in each pass
+  float nw[PASSES];     // its squared key norm (token retention)
 
 #pragma unroll
   for (int p0 = 0; p0 < PASSES; p0 += 2) {
@@ -78,10 +80,7 @@ __device__ __forceinline__ void quantize_tokens(const uint16_t* __restrict__ row
         x[8 * k + 6] = bf16_lo(raw[pass][k].w);
         x[8 * k + 7] = bf16_hi(raw[pass][k].w);
       }
-      if constexpr (NORM) {
-        const float sq = quad_sqnorm<E, G>(x);
-        if (t < n && j == 0) __builtin_nontemporal_store(sq, norm + t);
-      }
+      if constexpr (NORM) nw[p0 + pass] = quad_sqnorm<E, G>(x);
       if constexpr (ROTATE) fwht_quad<E, G>(x, j, fwht_scale<D>());
 
       float mn = x[0], mx = x[0];
@@ -98,10 +97,27 @@ __device__ __forceinline__ void quantize_tokens(const uint16_t* __restrict__ row
 #pragma unroll
       for (int e = 0; e < E; ++e) c[e] = code_bits(x[e], g);
       const Packed<E, BITS> pk = pack_code_bits<E, BITS>(c);
-      if (t < n) {
-        store_packed<E, BITS>(codes + (size_t)t * ROW + j * PIECE, pk);
-        if (j == 0) __builtin_nontemporal_store(g.meta, meta + t);
-      }
+      if (t < n) store_packed<E, BITS>(codes + (size_t)t * ROW + j * PIECE, pk);
+      mw[p0 + pass] = g.meta;
+    }
+  }
+  // The wave's 32 metadata words (and squared norms) in one instruction each,
+  // one whole 128-byte line: lane j of token group q writes the word of pass
+  // j, token j*TPP + q.  Every lane of a group holds the group's word and
+  // norm, so no exchange is needed.
+  static_assert(PASSES <= G, "a lane per pass");
+  if (j < PASSES) {
+    uint32_t w = mw[0];
+    float sq = NORM ? nw[0] : 0.0f;
+#pragma unroll
+    for (int i = 1; i < PASSES; ++i) {
+      w = j == i ? mw[i] : w;
+      if constexpr (NORM) sq = j == i ? nw[i] : sq;
+    }
+    const int t = t_first + j * TPP + q;
+    if (t < n) {
+      __builtin_nontemporal_store(w, meta + t);
+      if constexpr (NORM) __builtin_nontemporal_store(sq, norm + t);
     }
   }
 }
@@ -168,10 +184,14 @@ __device__ __forceinline__ void quantize_kivi_keys(const uint16_t* __restrict__ 
       const Packed<8, BITS> pk = pack_code_bits<8, BITS>(cq);
       if (t < n) store_packed<8, BITS>(codes + (size_t)t * ROW + c8 * BITS, pk);
     }
-    if (r == 0) {
-      uint32_t* m = meta + (size_t)(g_first / kWaveTokens) * D + 8 * c8;
-      __builtin_nontemporal_store(u32x4{g[0].meta, g[1].meta, g[2].meta, g[3].meta}, (u32x4*)m);
-      __builtin_nontemporal_store(u32x4{g[4].meta, g[5].meta, g[6].meta, g[7].meta}, (u32x4*)m + 1);
+    // The group's DH metadata words in one instruction of whole lines: rows 0
+    // and 1 (every row holds the reduced ranges) write the low and high four
+    // words of each channel octet.
+    if (r < 2) {
+      uint32_t* m = meta + (size_t)(g_first / kWaveTokens) * D + 8 * c8 + 4 * r;
+      const u32x4 lo = {g[0].meta, g[1].meta, g[2].meta, g[3].meta};
+      const u32x4 hi = {g[4].meta, g[5].meta, g[6].meta, g[7].meta};
+      __builtin_nontemporal_store(r ? hi : lo, (u32x4*)m);
     }
   }
 }
