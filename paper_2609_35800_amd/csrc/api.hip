@@ -155,6 +155,7 @@ void fill_params(hg::Params& p, const hg_config* c, const uint8_t* mask) {
     p.route.prefix[w] = running;
     running += (uint32_t)__builtin_popcount(word);
   }
+  p.n_unprot_k = LH - (int32_t)running;
 }
 
 }  // namespace

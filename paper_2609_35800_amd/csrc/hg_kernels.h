@@ -41,6 +41,7 @@ struct Params {
   int32_t kivi_whole;        // KIVI keys: one range over the whole sequence (kivi_seq.hip)
   int32_t ngroups;           // KIVI key groups per slice
   int32_t tiles;             // kBlockTokens tiles per slice
+  int32_t n_unprot_k;        // heads (l, h) whose keys are quantized
   uint32_t blocks_k;         // blocks of tensor K
   // AKVQ-style token retention
   float* norm;               // [L][B][H][n] squared key norms

@@ -3,25 +3,37 @@
 // base recomputes key ranges over the supplied sequence, including text,
 // while text KV stays BF16).  Selected by kivi_group = 0.
 //
-// A persistent grid of kSeqBlocksPerCU workgroups of kSeqThreads threads per
-// compute unit walks the key slices (l, b, h); for each slice:
-//  1. per-channel min / max over all T rows of the slice (the load layout
-//     holds a token row across D/8 lanes, 8 channels per lane, so each lane
-//     reduces its 8 channels over its rows in registers);
-//  2. the four wavefronts' partial ranges are combined through LDS and every
-//     lane forms the group scale of its 8 channels;
-//  3. the image rows are read again and quantized with those scales (codes
-//     and one metadata word per channel) or, for the one-pass simulated
-//     quantization, reconstructed to BF16.
+// Every code depends on the range of its channel over all T rows of the
+// slice, so a slice must be fully read before any of its codes is formed.
+// Two kernels:
+//
+// Resident (T <= kResRows): a persistent grid, one 1024-thread workgroup per
+// compute unit.  A workgroup takes one 64-channel part of a key slice (l, b, h)
+// and holds all T rows of that part on chip — 9 row slots in LDS, filled by
+// direct global-to-LDS loads, and 15 in registers, 128 rows per slot — so each
+// slice is read from HBM exactly once:
+//  1. per-channel min / max over the resident rows (each lane holds 8
+//     channels of one row per slot), reduced across the wavefront's rows by
+//     shuffles and across the 16 wavefronts through LDS; 64 lanes form the
+//     part's group scales and write its metadata words;
+//  2. codes (or, for the one-pass simulated quantization, the BF16
+//     reconstruction) of the image rows from the resident copy; as each slot
+//     is consumed, the loads of the same slot of the workgroup's next slice
+//     are issued into it, so the next slice streams in while this one is
+//     coded.
+// The parts of one slice go to workgroups whose indices differ by multiples
+// of 8, which the dispatcher places on the same XCD: the parts' pieces of a
+// packed code row then meet in one L2.
+//
+// Two-pass (longer slices): a persistent grid of kSeqBlocksPerCU workgroups
+// of kSeqThreads threads per compute unit walks the key slices; per slice a
+// range pass over all T rows, the wavefronts' partial ranges combined through
+// LDS, then a second pass over the image rows for the codes.  The grid is
+// sized so that the slices in flight at once stay within the 256 MB Infinity
+// Cache, which then serves much of the second read.
+//
 // Values, protected slices and the rest of the cache are handled by the
 // regular kernels of the same call.
-//
-// The second read of a slice's image rows is what makes this mode costlier
-// than the grouped one.  The grid is sized so that the slices in flight at
-// once (one per workgroup, ~770 KB each for a 3000-token slice) stay well
-// within the 256 MB Infinity Cache, so that read is served from it rather
-// than from HBM; large workgroups keep enough loads in flight to stream the
-// first pass at full HBM rate.
 
 #include <algorithm>
 
@@ -154,6 +166,274 @@ __global__ __launch_bounds__(kSeqThreads) void kivi_seq_kernel(const Params p) {
   }
 }
 
+// ------------------------------------------------------ resident variant
+
+constexpr int kResThreads = 1024;
+constexpr int kResWaves = kResThreads / 64;
+constexpr int kResPart = 64;                                  // channels per workgroup part
+constexpr int kResLanesPerRow = kResPart / 8;                 // 8 channels per lane
+constexpr int kResRowsPerWave = 64 / kResLanesPerRow;         // rows per load instruction
+constexpr int kResRowsPerSlot = kResWaves * kResRowsPerWave;  // 128
+constexpr int kResLdsSlots = 9;
+constexpr int kResRegSlots = 15;
+constexpr int kResSlots = kResLdsSlots + kResRegSlots;
+constexpr int kResRows = kResSlots * kResRowsPerSlot;         // 3072
+
+typedef __attribute__((address_space(1))) const void* global_cptr;
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+// s_waitcnt immediates (gfx9 encoding): every vector memory operation done;
+// every LDS operation done.
+constexpr int kWaitVmem0 = 0x0F70;
+constexpr int kWaitLds0 = 0xC07F;
+
+// Work item i of the resident kernel: the i-th (unprotected key head, batch
+// row) pair, heads in row-major (l, h) order.  Its slab in the packed key
+// buffers is i itself (slot u = i / B is the head's rank among quantized key
+// heads).  Scalar work.
+struct ResItem {
+  uint32_t s;  // slice (l*B + b)*H + h
+  bool valid;
+};
+
+__device__ __forceinline__ ResItem res_item(const Params& p, uint32_t item, uint32_t n_items) {
+  ResItem it;
+  it.valid = item < n_items;
+  it.s = 0;
+  if (!it.valid) return it;
+  const uint32_t u = item / (uint32_t)p.B;
+  const uint32_t b = item % (uint32_t)p.B;
+  // word w holding the u-th unprotected head: the last word with fewer than
+  // u + 1 unprotected heads before it (unprotected before word w: 32w - prefix[w])
+  const uint32_t words = ((uint32_t)p.L * p.H + 31u) / 32u;
+  uint32_t lo = 0, hi = words - 1;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi + 1) / 2;
+    if (32u * mid - p.route.prefix[mid] <= u) lo = mid; else hi = mid - 1;
+  }
+  uint32_t zeros = ~p.route.mask[lo];  // unprotected heads of word lo (bits past L*H never reached)
+  for (uint32_t k = u - (32u * lo - p.route.prefix[lo]); k > 0; --k) zeros &= zeros - 1u;
+  const uint32_t i = 32u * lo + (uint32_t)__builtin_ctz(zeros);
+  const uint32_t l = i / (uint32_t)p.H, h = i % (uint32_t)p.H;
+  it.s = (l * p.B + b) * p.H + h;
+  return it;
+}
+
+// Buffer resource over `bytes` bytes at `base` (gfx9 raw buffer, no swizzle):
+// a store whose offset is at or past `bytes` is dropped by the hardware.
+constexpr uint32_t kRawBufferWord3 = 0x00020000u;
+constexpr int kNonTemporal = 2;  // buffer instruction cache policy: streaming (nt)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t out_rsrc(void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, 0, bytes, kRawBufferWord3);
+}
+
+// Store of one lane's 8 codes (BITS bytes) at byte `off` of the resource.
+template <int BITS>
+__device__ __forceinline__ void store_codes8(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t w) {
+  if constexpr (BITS == 2) {
+    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)w, r, off, 0, kNonTemporal);
+  } else if constexpr (BITS == 4) {
+    __builtin_amdgcn_raw_buffer_store_b32(w, r, off, 0, kNonTemporal);
+  } else {
+    static_assert(BITS == 3, "bits");
+    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)w, r, off, 0, kNonTemporal);
+    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(w >> 8), r, off + 1, 0, kNonTemporal);
+    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(w >> 16), r, off + 2, 0, kNonTemporal);
+  }
+}
+
+template <int D, int BITS, bool FAKE>
+__global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, uint32_t n_items,
+                                                               uint32_t streams) {
+  constexpr int PARTS = D / kResPart;
+  constexpr int LEVELS = (1 << BITS) - 1;
+  constexpr int ROW = D * BITS / 8;
+  __shared__ u32x4 rows_lds[kResLdsSlots][kResThreads];
+  __shared__ float part_rng[2][kResWaves][kResPart];
+  __shared__ uint32_t g_meta[kResPart];
+  __shared__ float g_inv[kResPart];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c = lane % kResLanesPerRow;
+  const int r = lane / kResLanesPerRow;
+  const int row0 = wave * kResRowsPerWave + r;  // row of slot 0 held by this lane
+  // workgroup -> (stream, part); the parts of a stream are 8 workgroups apart
+  const uint32_t bx = blockIdx.x;
+  const int part = (int)((bx / 8u) % PARTS);
+  const uint32_t stream = (bx / (8u * PARTS)) * 8u + bx % 8u;
+  const int ch = part * kResPart + 8 * c;       // first of this lane's 8 channels
+  const int T = p.T;
+
+  uint32_t item = stream;
+  ResItem cur = res_item(p, item, n_items);
+  if (!cur.valid) return;
+
+  // Row of a slot for this lane: `rowb` is row0, made opaque to the compiler
+  // once per slice so that the 24 slots' row offsets and addresses are formed
+  // where they are used instead of being hoisted out of the slice loop (which
+  // keeps them all live and spills the resident rows).
+  int rowb = row0;
+  auto src_of = [&](uint32_t s, int slot) {
+    const int t = min(slot * kResRowsPerSlot + rowb, T - 1);  // rows past T repeat the last row
+    return p.cache[0] + ((size_t)s * T + t) * D + ch;
+  };
+  auto load_lds = [&](uint32_t s, int j) {
+    __builtin_amdgcn_global_load_lds((global_cptr)src_of(s, j), (lds_ptr)&rows_lds[j][wave * 64], 16, 0, 0);
+  };
+
+  u32x4 v[kResRegSlots];
+  float mn[8], mx[8];
+  auto range8 = [&](const u32x4 w) {
+    const float x[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
+                        bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      mn[e] = fminf(mn[e], x[e]);
+      mx[e] = fmaxf(mx[e], x[e]);
+    }
+  };
+  // Per-channel range over all T rows of the slice (slot rows past T repeat
+  // row T-1): the register slots (the compiler waits for their loads), then,
+  // after every vector memory operation has completed (the fence keeps the
+  // LDS reads behind the wait), the LDS slots.
+  auto range_pass = [&]() {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      mn[e] = __builtin_inff();
+      mx[e] = -__builtin_inff();
+    }
+#pragma unroll
+    for (int k = 0; k < kResRegSlots; ++k) range8(v[k]);
+    __builtin_amdgcn_s_waitcnt(kWaitVmem0);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < kResLdsSlots; ++j) range8(rows_lds[j][tid]);
+  };
+
+  // prologue: the first slice's loads (every store of this lane comes after
+  // them, so the range pass waits as if no store followed)
+#pragma unroll
+  for (int j = 0; j < kResLdsSlots; ++j) load_lds(cur.s, j);
+#pragma unroll
+  for (int k = 0; k < kResRegSlots; ++k) v[k] = *(const u32x4*)src_of(cur.s, kResLdsSlots + k);
+  range_pass();
+
+  for (;;) {
+    const ResItem nxt = res_item(p, item + streams, n_items);
+
+    // scales: the wavefront's rows by shuffles, the 16 wavefronts through LDS
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+#pragma unroll
+      for (int off = kResLanesPerRow; off < 64; off *= 2) {
+        mn[e] = fminf(mn[e], __shfl_xor(mn[e], off));
+        mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], off));
+      }
+    }
+    if (r == 0) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        part_rng[0][wave][8 * c + e] = mn[e];
+        part_rng[1][wave][8 * c + e] = mx[e];
+      }
+    }
+    __syncthreads();
+    const size_t slab = (size_t)item;  // [slot][B] with slot = item / B
+    if (tid < kResPart) {
+      float a = part_rng[0][0][tid], b = part_rng[1][0][tid];
+#pragma unroll
+      for (int w = 1; w < kResWaves; ++w) {
+        a = fminf(a, part_rng[0][w][tid]);
+        b = fmaxf(b, part_rng[1][w][tid]);
+      }
+      const GroupScale g = group_scale<LEVELS>(a, b);
+      g_meta[tid] = g.meta;
+      g_inv[tid] = g.inv;
+      if (!FAKE) __builtin_nontemporal_store(g.meta, p.meta[0] + slab * D + part * kResPart + tid);
+    }
+    __syncthreads();
+    GroupScale g[8];  // .meta unused below
+    float S[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t w = g_meta[8 * c + e];
+      g[e].meta = 0;
+      g[e].m = bf16_as_float(w >> 16);
+      g[e].inv = g_inv[8 * c + e];
+      S[e] = FAKE ? bf16_as_float(w & 0xFFFFu) : 0.0f;
+    }
+
+    // Codes (or the reconstruction) of the image rows, through buffer
+    // resources over this slice's outputs: a text row, or a slot row past T,
+    // has an offset outside the resource and its store is dropped, so the
+    // code pass has no branches.
+    rowb = row0;
+    asm volatile("" : "+v"(rowb));
+    // (the resource is wave-uniform, the slice's image rows; the lane's
+    // channels are part of its offset)
+    const __amdgpu_buffer_rsrc_t res =
+        FAKE ? out_rsrc(p.out[0] + ((size_t)cur.s * T + p.s0) * D, (uint32_t)p.n * D * 2)
+             : out_rsrc(p.codes[0] + slab * p.n * ROW, (uint32_t)p.n * ROW);
+    const uint32_t lane_off = FAKE ? (uint32_t)ch * 2 : (uint32_t)(ch / 8) * BITS;
+    auto emit = [&](u32x4 w, int slot) {
+      asm volatile("" : "+v"(w));  // convert here, not reuse the range pass's values
+      const int t = slot * kResRowsPerSlot + rowb;
+      const int ti = t - p.s0;  // row within the image span (negative: text before it)
+      const uint32_t off = ((uint32_t)ti * (FAKE ? D * 2 : ROW) + lane_off) | (t < T ? 0u : 0x80000000u);
+      const float x[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
+                          bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
+      uint32_t cb[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) cb[e] = code_bits(x[e], g[e]);
+      if constexpr (FAKE) {
+        float y[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf((float)(cb[e] - kMagicBits), S[e], g[e].m);
+        const u32x4 o = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
+                         pack_bf16x2_hw(y[6], y[7])};
+        __builtin_amdgcn_raw_buffer_store_b128(o, res, off, 0, kNonTemporal);
+      } else {
+        store_codes8<BITS>(res, off, pack_code_bits<8, BITS>(cb).w[0]);
+      }
+    };
+    // The LDS slots are all read before any of them is refilled: the compiler
+    // cannot tell the slots apart, and an LDS read issued after a pending
+    // direct-to-LDS load makes it wait for that load.  The register slots are
+    // refilled one by one (scheduling barriers keep each refill after the
+    // slot's use: hoisted refills would need a second copy of the rows).
+    auto code_pass = [&](bool refill) {
+#pragma unroll
+      for (int j = 0; j < kResLdsSlots; ++j) {
+        emit(rows_lds[j][tid], j);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (refill) {
+        __builtin_amdgcn_s_waitcnt(kWaitLds0);  // every slot read before it is refilled
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < kResLdsSlots; ++j) load_lds(nxt.s, j);
+      }
+#pragma unroll
+      for (int k = 0; k < kResRegSlots; ++k) {
+        emit(v[k], kResLdsSlots + k);
+        __builtin_amdgcn_sched_barrier(0);
+        if (refill) v[k] = *(const u32x4*)src_of(nxt.s, kResLdsSlots + k);
+      }
+    };
+    if (!nxt.valid) {
+      code_pass(false);
+      break;
+    }
+    code_pass(true);
+    range_pass();
+    cur = nxt;
+    item += streams;
+  }
+}
+
 template <int D, int BITS>
 static hipError_t launch_k(const Params& p, bool fake, hipStream_t stream) {
   int dev = 0, cus = 0;
@@ -161,6 +441,22 @@ static hipError_t launch_k(const Params& p, bool fake, hipStream_t stream) {
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
   const uint32_t slices = (uint32_t)p.L * p.B * p.H;
+  if (p.T <= kResRows) {
+    // one workgroup per compute unit, in whole groups of 8 * PARTS (a stream's parts 8 apart)
+    constexpr uint32_t PARTS = D / kResPart;
+    const uint32_t unit = 8u * PARTS;
+    const uint32_t n_items = (uint32_t)p.n_unprot_k * (uint32_t)p.B;
+    const uint32_t want = (n_items + 7u) / 8u * unit;  // no more streams than items (rounded up)
+    const uint32_t blocks = std::max(unit, std::min((uint32_t)std::max(cus, 1) / unit * unit, want));
+    const uint32_t streams = blocks / PARTS;
+    if (fake)
+      hipLaunchKernelGGL((kivi_res_kernel<D, BITS, true>), dim3(blocks), dim3(kResThreads), 0, stream, p,
+                         n_items, streams);
+    else
+      hipLaunchKernelGGL((kivi_res_kernel<D, BITS, false>), dim3(blocks), dim3(kResThreads), 0, stream, p,
+                         n_items, streams);
+    return hipGetLastError();
+  }
   const uint32_t blocks = std::min<uint32_t>(slices, (uint32_t)std::max(cus, 1) * kSeqBlocksPerCU);
   if (fake)
     hipLaunchKernelGGL((kivi_seq_kernel<D, BITS, true>), dim3(blocks), dim3(kSeqThreads), 0, stream, p);

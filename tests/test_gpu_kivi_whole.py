@@ -2,7 +2,13 @@
 supplied sequence, text included (kivi_group = 0; §4 Quantization setup),
 against the oracle: codes, metadata, side store and reconstruction
 bit-exact for quantize / dequantize and for the one-pass simulated
-quantization; full-size sampled slices on the LLaVA-NeXT-7B-shaped cache."""
+quantization; full-size sampled slices on the LLaVA-NeXT-7B-shaped cache.
+
+Slices of up to 3072 rows go through the resident kernel (each workgroup
+holds a 64-channel part of a slice on chip and refills its row slots with
+its next slice while coding); longer slices through the two-pass kernel.
+Both are covered, including several slices per workgroup stream and the
+boundary at 3072 / 3073 rows."""
 import numpy as np
 import pytest
 import torch
@@ -65,3 +71,51 @@ def test_full_size_llava():
         assert np.array_equal(codes[slot, b].cpu().numpy(), oc)
         assert np.array_equal(meta[slot, b].cpu().numpy().view(np.uint32), om)
         checked += 1
+
+
+# Enough (head, row) items that every workgroup stream of the resident kernel
+# takes several slices (streams: 256 / 128 / 64 at head_dim 64 / 128 / 256),
+# so each slot's refill with the next slice is exercised.
+STREAM_CASES = [small("kivi", D, bits, ko, img_len=150, img_start=20, text=30, L=2, B=20, H=8,
+                      n_protected=2).with_(kivi_group=0, name=f"kiviseq-streams-D{D}-b{bits}-ko{ko}")
+                for D in (64, 128, 256) for bits in (2, 3) for ko in (0, 1)]
+
+
+@pytest.mark.parametrize("w", STREAM_CASES, ids=lambda w: w.name)
+def test_resident_streams(w):
+    K, V = synthkv.gen_kv(w)
+    _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), w.name)
+
+
+@pytest.mark.parametrize("w", STREAM_CASES[2:4], ids=lambda w: w.name)
+@pytest.mark.parametrize("inplace", [False, True])
+def test_resident_streams_fake(w, inplace):
+    K, V = synthkv.gen_kv(w)
+    check_fake(w, K, V, synthkv.protect_mask(w), inplace)
+
+
+# Slices at the resident capacity (3072 rows: every row slot filled), one row
+# past it (the two-pass kernel), and longer; image spans at the start, in the
+# middle and at the end of the slice.
+BOUNDARY = [(3072, 3000, 40), (3073, 3000, 40), (3072, 3072, 0), (3072, 100, 2972),
+            (3200, 3100, 0), (4000, 1000, 1500)]
+
+
+@pytest.mark.parametrize("D", [128, 256])
+@pytest.mark.parametrize("T,img_len,img_start", BOUNDARY, ids=lambda v: str(v))
+def test_capacity_boundary(D, T, img_len, img_start):
+    w = small("kivi", D, 3, 0, img_len=img_len, img_start=img_start, text=T - img_len - img_start,
+              L=1, B=2, H=2, n_protected=1).with_(kivi_group=0)
+    assert w.T == T
+    K, V = synthkv.gen_kv(w)
+    K[0, :, :, T - 1, 5] = -4000.0  # an extreme in the last row of every slice
+    _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), f"T{T}-n{img_len}-s{img_start}")
+
+
+@pytest.mark.parametrize("T,img_len,img_start", BOUNDARY[:2], ids=lambda v: str(v))
+@pytest.mark.parametrize("inplace", [False, True])
+def test_capacity_boundary_fake(T, img_len, img_start, inplace):
+    w = small("kivi", 128, 2, 1, img_len=img_len, img_start=img_start, text=T - img_len - img_start,
+              L=1, B=2, H=2, n_protected=1).with_(kivi_group=0)
+    K, V = synthkv.gen_kv(w)
+    check_fake(w, K, V, synthkv.protect_mask(w), inplace)
