@@ -32,8 +32,8 @@ _CSRC = "paper_2609_35800_amd/csrc/"
 KERNEL_SOURCES = {
     QUANT_KERNEL: tuple(_CSRC + f for f in ("quantize.hip", "kivi_seq.hip", "retain.hip",
                                               "hg_device.h", "hg_kernels.h")),
-    FAKE_KERNEL: tuple(_CSRC + f for f in ("fakequant.hip", "retain.hip", "hg_device.h",
-                                             "hg_kernels.h")),
+    FAKE_KERNEL: tuple(_CSRC + f for f in ("fakequant.hip", "kivi_seq.hip", "retain.hip",
+                                             "hg_device.h", "hg_kernels.h")),
 }
 
 

@@ -228,18 +228,23 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t out_rsrc(void* base, uint32_t 
   return __builtin_amdgcn_make_buffer_rsrc(base, 0, bytes, kRawBufferWord3);
 }
 
-// Store of one lane's 8 codes (BITS bytes) at byte `off` of the resource.
+// Store of one lane's 8 codes (BITS bytes) at byte `off` of the resource,
+// with the default (write-back) cache policy: the parts of a packed code row
+// are written by different workgroups, and a streaming store of a partial
+// line goes to memory as a whole line, so each line would be written once per
+// part; through L2 the parts' pieces of a line (their workgroups share an XCD)
+// merge before the line is written back.
 template <int BITS>
 __device__ __forceinline__ void store_codes8(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t w) {
   if constexpr (BITS == 2) {
-    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)w, r, off, 0, kNonTemporal);
+    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)w, r, off, 0, 0);
   } else if constexpr (BITS == 4) {
-    __builtin_amdgcn_raw_buffer_store_b32(w, r, off, 0, kNonTemporal);
+    __builtin_amdgcn_raw_buffer_store_b32(w, r, off, 0, 0);
   } else {
     static_assert(BITS == 3, "bits");
-    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)w, r, off, 0, kNonTemporal);
-    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(w >> 8), r, off + 1, 0, kNonTemporal);
-    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(w >> 16), r, off + 2, 0, kNonTemporal);
+    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)w, r, off, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(w >> 8), r, off + 1, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(w >> 16), r, off + 2, 0, 0);
   }
 }
 
