@@ -119,3 +119,17 @@ def test_capacity_boundary_fake(T, img_len, img_start, inplace):
               L=1, B=2, H=2, n_protected=1).with_(kivi_group=0)
     K, V = synthkv.gen_kv(w)
     check_fake(w, K, V, synthkv.protect_mask(w), inplace)
+
+
+@pytest.mark.parametrize("which", ["none", "all", "last"])
+@pytest.mark.parametrize("keys_only", [0, 1])
+def test_degenerate_masks(which, keys_only):
+    """No key head protected, every one (no work item for the key kernel),
+    and only the last head quantized (the rank search lands in the last word)."""
+    w = small("kivi", 128, 2, keys_only, img_len=90, img_start=5, text=9, L=3, B=2, H=12,
+              n_protected=0).with_(kivi_group=0)
+    K, V = synthkv.gen_kv(w)
+    mask = np.full(w.L * w.H, 1 if which != "none" else 0, np.uint8)
+    if which == "last":
+        mask[-1] = 0
+    _assert_exact(compare_full(w, K, V, mask), f"mask-{which}-ko{keys_only}")

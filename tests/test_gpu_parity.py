@@ -73,14 +73,17 @@ def test_degenerate_masks(base, which, keys_only):
     _assert_exact(rep, f"{base}-{which}")
 
 
-@pytest.mark.parametrize("base,keys_only,retain", [("minmax", 0, 0), ("kivi", 1, 0), ("akvq", 0, 100)])
-def test_maximum_head_count(base, keys_only, retain):
+@pytest.mark.parametrize("base,keys_only,retain,kivi_group",
+                         [("minmax", 0, 0, 32), ("kivi", 1, 0, 32), ("kivi", 0, 0, 0), ("akvq", 0, 100, 32)])
+def test_maximum_head_count(base, keys_only, retain, kivi_group):
     """L*H at the routing limit (8192 heads): the mask bitmap and its prefix
-    counts span every word; protected heads sit in the first and last words."""
+    counts span every word; protected heads sit in the first and last words.
+    With whole-sequence KIVI keys the resident kernel finds each work item's
+    head by its rank among the quantized heads across all 256 words."""
     import paper_2609_35800_amd as hg
-    w = synthkv.Workload(f"maxheads-{base}", L=128, B=1, H=64, T=40, D=64, img_start=3,
+    w = synthkv.Workload(f"maxheads-{base}-{kivi_group}", L=128, B=1, H=64, T=40, D=64, img_start=3,
                          img_len=33, bits=3, base=base, keys_only=keys_only, n_protected=0,
-                         k_outliers=2, k_outlier_scale=10.0, kivi_group=32, retain_permille=retain)
+                         k_outliers=2, k_outlier_scale=10.0, kivi_group=kivi_group, retain_permille=retain)
     assert w.L * w.H == hg.HG_MAX_HEADS
     rng = np.random.default_rng(8192)
     mask = (rng.random(w.L * w.H) < 0.125).astype(np.uint8)
