@@ -17,13 +17,12 @@
 //     shuffles and across the 16 wavefronts through LDS; 64 lanes form the
 //     part's group scales and write its metadata words;
 //  2. codes (or, for the one-pass simulated quantization, the BF16
-//     reconstruction) of the image rows from the resident copy; as each slot
-//     is consumed, the loads of the same slot of the workgroup's next slice
-//     are issued into it, so the next slice streams in while this one is
-//     coded.
+//     reconstruction) of the image rows from the resident copy; as the slots
+//     are consumed, the loads of the workgroup's next slice are issued into
+//     them, so the next slice streams in while this one is coded.
 // The parts of one slice go to workgroups whose indices differ by multiples
-// of 8, which the dispatcher places on the same XCD: the parts' pieces of a
-// packed code row then meet in one L2.
+// of 8 (the dispatcher places those on the same XCD), so a slice's parts are
+// processed at the same time.
 //
 // Two-pass (longer slices): a persistent grid of kSeqBlocksPerCU workgroups
 // of kSeqThreads threads per compute unit walks the key slices; per slice a
@@ -316,8 +315,7 @@ __global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, u
     for (int j = 0; j < kResLdsSlots; ++j) range8(rows_lds[j][tid]);
   };
 
-  // prologue: the first slice's loads (every store of this lane comes after
-  // them, so the range pass waits as if no store followed)
+  // prologue: the first slice's loads and its range pass
 #pragma unroll
   for (int j = 0; j < kResLdsSlots; ++j) load_lds(cur.s, j);
 #pragma unroll
