@@ -155,7 +155,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
 
 template <int BASE, int D, int BITS>
 static hipError_t launch_d(const Params& p, uint32_t blocks, hipStream_t stream) {
-  hipLaunchKernelGGL((dequantize_kernel<BASE, D, BITS>), dim3(blocks), dim3(kThreads), 0, stream, p);
+  hipLaunchKernelGGL((dequantize_kernel<BASE, D, BITS>), dim3(blocks), dim3(kThreads),
+                     occupancy_lds(kDequantizeWaves), stream, p);
   return hipGetLastError();
 }
 

@@ -232,8 +232,8 @@ void fake_quantize_kernel(const Params p) {
       fake_copy<D, false>(rows, out, nullptr, t_first, p.n, lane);
     return;
   }
+  if (sl.X == 0 && p.kivi_whole) return;  // whole-sequence KIVI key ranges: kivi_seq.hip
   if (BASE == HG_BASE_KIVI && sl.X == 0) {
-    if (p.kivi_whole) return;  // whole-sequence key ranges: kivi_seq.hip
     fake_kivi_keys<D, BITS>(rows, out, t_first, p.n, lane);
   } else {
     __shared__ u32x4 stage_all[kThreads / 64][(64 / kTokenLanes<D>) * (D / 8)];
@@ -278,14 +278,22 @@ static hipError_t launch_f_dim(const Params& p, int D, int bits, uint32_t blocks
   }
 }
 
+// Value tiles of the KIVI-style and AKVQ-style bases run as a launch of the
+// min-max instantiation, which needs fewer registers than their key paths
+// (as in launch_quantize); with KIVI keys over the whole sequence the whole
+// launch does.
 hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, uint32_t blocks, bool norms,
                                 hipStream_t stream) {
-  switch (base) {
-    case HG_BASE_MINMAX: return launch_f_dim<HG_BASE_MINMAX>(p, D, bits, blocks, norms, stream);
-    case HG_BASE_KIVI: return launch_f_dim<HG_BASE_KIVI>(p, D, bits, blocks, norms, stream);
-    case HG_BASE_AKVQ: return launch_f_dim<HG_BASE_AKVQ>(p, D, bits, blocks, norms, stream);
-    default: return hipErrorInvalidValue;
-  }
+  if (base == HG_BASE_MINMAX || (base == HG_BASE_KIVI && p.kivi_whole))
+    return launch_f_dim<HG_BASE_MINMAX>(p, D, bits, blocks, norms, stream);
+  if (base != HG_BASE_KIVI && base != HG_BASE_AKVQ) return hipErrorInvalidValue;
+  const uint32_t blocks_v = blocks - p.blocks_k;
+  hipError_t e = base == HG_BASE_KIVI ? launch_f_dim<HG_BASE_KIVI>(p, D, bits, p.blocks_k, norms, stream)
+                                      : launch_f_dim<HG_BASE_AKVQ>(p, D, bits, p.blocks_k, norms, stream);
+  if (e != hipSuccess || blocks_v == 0) return e;
+  Params pv = p;
+  pv.blocks_k = 0;  // every block of this launch is a value tile
+  return launch_f_dim<HG_BASE_MINMAX>(pv, D, bits, blocks_v, false, stream);
 }
 
 }  // namespace hg

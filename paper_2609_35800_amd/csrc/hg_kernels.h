@@ -17,6 +17,19 @@ constexpr int kBlockTokens = 128;    // tokens per workgroup tile (4 x 32)
 constexpr int kMinWaves = 4;
 constexpr int kMaskWords = HG_MAX_HEADS / 32;
 
+// Occupancy cap through a launch-time LDS reservation: gfx950 has 160 KiB of
+// LDS per compute unit, and a workgroup that reserves just over 1/(w + 1) of
+// it leaves room for w workgroups per compute unit but not w + 1 — for a
+// 4-wavefront workgroup, w wavefronts per SIMD.  0: no cap.
+constexpr size_t kLdsPerCU = 160 * 1024;
+constexpr size_t occupancy_lds(int waves) { return waves > 0 ? kLdsPerCU / (waves + 1) + 512 : 0; }
+// Wavefronts per SIMD of the quantize and dequantize kernels: at the 8 their
+// registers allow, the memory system is oversubscribed (6 measured faster
+// than 8, 5 and 4 over the workloads; quantize kernels whose registers
+// already allow fewer, such as KIVI key groups at 4, are not affected).
+constexpr int kQuantizeWaves = 6;
+constexpr int kDequantizeWaves = 6;
+
 // Mask routing in kernel arguments: bit i of `mask` marks protected head
 // i = l*H + h; `prefix[w]` counts protected heads in words before w, so the
 // rank of i among protected heads is prefix[i/32] + popcount of the lower

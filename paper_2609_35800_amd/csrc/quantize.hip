@@ -247,9 +247,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
       copy_rows<D, false>(rows, p.side[sl.X] + slab * p.n * D, nullptr, t_first, p.n, lane);
     return;
   }
+  if (sl.X == 0 && p.kivi_whole) return;  // whole-sequence KIVI key ranges: kivi_seq.hip
   uint8_t* codes = p.codes[sl.X] + slab * p.n * (D * BITS / 8);
   if (BASE == HG_BASE_KIVI && sl.X == 0) {
-    if (p.kivi_whole) return;  // whole-sequence key ranges: kivi_seq.hip
     uint32_t* meta = p.meta[0] + slab * p.ngroups * D;
     quantize_kivi_keys<D, BITS>(rows, codes, meta, t_first, p.n, lane);
   } else {
@@ -265,12 +265,14 @@ template <int BASE, int D, int BITS>
 static hipError_t launch_q(const Params& p, uint32_t blocks, bool norms, hipStream_t stream) {
   if constexpr (BASE == HG_BASE_AKVQ) {
     if (norms) {
-      hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, true>), dim3(blocks), dim3(kThreads), 0, stream, p);
+      hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, true>), dim3(blocks), dim3(kThreads),
+                         occupancy_lds(kQuantizeWaves), stream, p);
       return hipGetLastError();
     }
   }
   if (norms) return hipErrorInvalidValue;  // key norms belong to the AKVQ base
-  hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, false>), dim3(blocks), dim3(kThreads), 0, stream, p);
+  hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, false>), dim3(blocks), dim3(kThreads),
+                     occupancy_lds(kQuantizeWaves), stream, p);
   return hipGetLastError();
 }
 
@@ -295,14 +297,25 @@ static hipError_t launch_q_dim(const Params& p, int D, int bits, uint32_t blocks
   }
 }
 
+// The KIVI-style and AKVQ-style bases quantize values exactly as min-max
+// does (per token, unrotated), so their value tiles run as a launch of the
+// min-max instantiation: a kernel holds the registers of its largest path,
+// and the key paths (KIVI groups, rotation) need more than the per-token
+// path, which would leave the value tiles with fewer waves per SIMD.  With
+// KIVI keys over the whole sequence this launch only copies protected keys
+// and quantizes values, so all of it runs as the min-max instantiation.
 hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t blocks, bool norms,
                            hipStream_t stream) {
-  switch (base) {
-    case HG_BASE_MINMAX: return launch_q_dim<HG_BASE_MINMAX>(p, D, bits, blocks, norms, stream);
-    case HG_BASE_KIVI: return launch_q_dim<HG_BASE_KIVI>(p, D, bits, blocks, norms, stream);
-    case HG_BASE_AKVQ: return launch_q_dim<HG_BASE_AKVQ>(p, D, bits, blocks, norms, stream);
-    default: return hipErrorInvalidValue;
-  }
+  if (base == HG_BASE_MINMAX || (base == HG_BASE_KIVI && p.kivi_whole))
+    return launch_q_dim<HG_BASE_MINMAX>(p, D, bits, blocks, norms, stream);
+  if (base != HG_BASE_KIVI && base != HG_BASE_AKVQ) return hipErrorInvalidValue;
+  const uint32_t blocks_v = blocks - p.blocks_k;
+  hipError_t e = base == HG_BASE_KIVI ? launch_q_dim<HG_BASE_KIVI>(p, D, bits, p.blocks_k, norms, stream)
+                                      : launch_q_dim<HG_BASE_AKVQ>(p, D, bits, p.blocks_k, norms, stream);
+  if (e != hipSuccess || blocks_v == 0) return e;
+  Params pv = p;
+  pv.blocks_k = 0;  // every block of this launch is a value tile
+  return launch_q_dim<HG_BASE_MINMAX>(pv, D, bits, blocks_v, false, stream);
 }
 
 }  // namespace hg
