@@ -40,8 +40,22 @@ def build(verbose: bool = False, out: str = LIB, host_asan: bool = False) -> str
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
+    check_launch_stubs(tmp)
     os.replace(tmp, out)
     return out
+
+
+def check_launch_stubs(lib: str) -> None:
+    """Fail the build if a kernel's host launch stub is left undefined (the
+    host pass can drop it when a kernel template does not instantiate there);
+    such a library would not load."""
+    nm = os.environ.get("NM", "nm")
+    syms = subprocess.run([nm, "-D", "--undefined-only", lib], check=True, capture_output=True,
+                          text=True).stdout
+    missing = [line.split()[-1] for line in syms.splitlines() if "__device_stub__" in line]
+    if missing:
+        os.remove(lib)
+        raise RuntimeError(f"{len(missing)} kernel launch stub(s) undefined, e.g. {missing[0]}")
 
 
 if __name__ == "__main__":

@@ -178,7 +178,6 @@ constexpr int kResRegSlots = 15;
 constexpr int kResSlots = kResLdsSlots + kResRegSlots;
 constexpr int kResRows = kResSlots * kResRowsPerSlot;         // 3072
 
-typedef __attribute__((address_space(1))) const void* global_cptr;
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
 // s_waitcnt immediates (gfx9 encoding): every vector memory operation done;
@@ -225,6 +224,16 @@ constexpr int kNonTemporal = 2;  // buffer instruction cache policy: streaming (
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t out_rsrc(void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(base, 0, bytes, kRawBufferWord3);
+}
+
+// 16-byte load at byte `off` of a buffer resource, into registers or, for
+// the whole wavefront, into 64 consecutive 16-byte LDS slots at `dst` (lane i
+// at dst + 16 i).
+__device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+__device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t r, lds_ptr dst, uint32_t off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, off, 0, 0, 0);
 }
 
 // Store of one lane's 8 codes (BITS bytes) at byte `off` of the resource,
@@ -274,16 +283,22 @@ __global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, u
   if (!cur.valid) return;
 
   // Row of a slot for this lane: `rowb` is row0, made opaque to the compiler
-  // once per slice so that the 24 slots' row offsets and addresses are formed
-  // where they are used instead of being hoisted out of the slice loop (which
-  // keeps them all live and spills the resident rows).
+  // once per slice so that the 24 slots' row offsets are formed where they
+  // are used instead of being hoisted out of the slice loop (which keeps them
+  // all live and spills the resident rows).
   int rowb = row0;
-  auto src_of = [&](uint32_t s, int slot) {
-    const int t = min(slot * kResRowsPerSlot + rowb, T - 1);  // rows past T repeat the last row
-    return p.cache[0] + ((size_t)s * T + t) * D + ch;
+  // Loads go through a buffer resource over the slice (wave-uniform), with a
+  // 32-bit per-lane byte offset: rows past T repeat row T-1.
+  auto slice_rsrc = [&](uint32_t s) {
+    return __builtin_amdgcn_make_buffer_rsrc((void*)(p.cache[0] + (size_t)s * T * D), 0,
+                                             (uint32_t)T * D * 2, kRawBufferWord3);
   };
-  auto load_lds = [&](uint32_t s, int j) {
-    __builtin_amdgcn_global_load_lds((global_cptr)src_of(s, j), (lds_ptr)&rows_lds[j][wave * 64], 16, 0, 0);
+  auto src_off = [&](int slot) {
+    return (uint32_t)min(slot * kResRowsPerSlot + rowb, T - 1) * (D * 2) + (uint32_t)ch * 2;
+  };
+  auto load_reg = [&](__amdgpu_buffer_rsrc_t r, int slot) { return buffer_load16(r, src_off(slot)); };
+  auto load_lds = [&](__amdgpu_buffer_rsrc_t r, int j) {
+    buffer_load16_lds(r, (lds_ptr)&rows_lds[j][wave * 64], src_off(j));
   };
 
   u32x4 v[kResRegSlots];
@@ -316,10 +331,13 @@ __global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, u
   };
 
   // prologue: the first slice's loads and its range pass
+  {
+    const __amdgpu_buffer_rsrc_t r = slice_rsrc(cur.s);
 #pragma unroll
-  for (int j = 0; j < kResLdsSlots; ++j) load_lds(cur.s, j);
+    for (int j = 0; j < kResLdsSlots; ++j) load_lds(r, j);
 #pragma unroll
-  for (int k = 0; k < kResRegSlots; ++k) v[k] = *(const u32x4*)src_of(cur.s, kResLdsSlots + k);
+    for (int k = 0; k < kResRegSlots; ++k) v[k] = load_reg(r, kResLdsSlots + k);
+  }
   range_pass();
 
   for (;;) {
@@ -378,12 +396,14 @@ __global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, u
     const __amdgpu_buffer_rsrc_t res =
         FAKE ? out_rsrc(p.out[0] + ((size_t)cur.s * T + p.s0) * D, (uint32_t)p.n * D * 2)
              : out_rsrc(p.codes[0] + slab * p.n * ROW, (uint32_t)p.n * ROW);
-    const uint32_t lane_off = FAKE ? (uint32_t)ch * 2 : (uint32_t)(ch / 8) * BITS;
+    // Byte offset of a slot row's piece: rows before the span wrap to huge
+    // offsets and rows at or past its end (slot rows past T included, as
+    // s0 + n <= T) land at or past n rows; both fall outside the resource.
+    constexpr uint32_t kStride = FAKE ? D * 2 : ROW;
+    const uint32_t lane_off = (FAKE ? (uint32_t)ch * 2 : (uint32_t)(ch / 8) * BITS) - (uint32_t)p.s0 * kStride;
     auto emit = [&](u32x4 w, int slot) {
       asm volatile("" : "+v"(w));  // convert here, not reuse the range pass's values
-      const int t = slot * kResRowsPerSlot + rowb;
-      const int ti = t - p.s0;  // row within the image span (negative: text before it)
-      const uint32_t off = ((uint32_t)ti * (FAKE ? D * 2 : ROW) + lane_off) | (t < T ? 0u : 0x80000000u);
+      const uint32_t off = (uint32_t)(slot * kResRowsPerSlot + rowb) * kStride + lane_off;
       const float x[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
                           bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
       uint32_t cb[8];
@@ -406,6 +426,7 @@ __global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, u
     // refilled one by one (scheduling barriers keep each refill after the
     // slot's use: hoisted refills would need a second copy of the rows).
     auto code_pass = [&](bool refill) {
+      const __amdgpu_buffer_rsrc_t r = slice_rsrc(nxt.s);
 #pragma unroll
       for (int j = 0; j < kResLdsSlots; ++j) {
         emit(rows_lds[j][tid], j);
@@ -415,13 +436,13 @@ __global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, u
         __builtin_amdgcn_s_waitcnt(kWaitLds0);  // every slot read before it is refilled
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int j = 0; j < kResLdsSlots; ++j) load_lds(nxt.s, j);
+        for (int j = 0; j < kResLdsSlots; ++j) load_lds(r, j);
       }
 #pragma unroll
       for (int k = 0; k < kResRegSlots; ++k) {
         emit(v[k], kResLdsSlots + k);
         __builtin_amdgcn_sched_barrier(0);
-        if (refill) v[k] = *(const u32x4*)src_of(nxt.s, kResLdsSlots + k);
+        if (refill) v[k] = load_reg(r, kResLdsSlots + k);
       }
     };
     if (!nxt.valid) {
