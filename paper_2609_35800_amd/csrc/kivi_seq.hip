@@ -201,14 +201,24 @@ __device__ __forceinline__ ResItem res_item(const Params& p, uint32_t item, uint
   if (!it.valid) return it;
   const uint32_t u = item / (uint32_t)p.B;
   const uint32_t b = item % (uint32_t)p.B;
-  // word w holding the u-th unprotected head: the last word with fewer than
-  // u + 1 unprotected heads before it (unprotected before word w: 32w - prefix[w])
+  // Word holding the u-th unprotected head: the last word with fewer than
+  // u + 1 unprotected heads before it (unprotected before word w:
+  // 32w - prefix[w], non-decreasing in w), i.e. the number of words with at
+  // most u of them, minus one.  The lanes test 64 words at a time (at most
+  // four rounds), so the search is one round of loads, not a chain of
+  // dependent ones.
   const uint32_t words = ((uint32_t)p.L * p.H + 31u) / 32u;
-  uint32_t lo = 0, hi = words - 1;
-  while (lo < hi) {
-    const uint32_t mid = (lo + hi + 1) / 2;
-    if (32u * mid - p.route.prefix[mid] <= u) lo = mid; else hi = mid - 1;
+  uint32_t lane = threadIdx.x & 63u;
+  asm volatile("" : "+v"(lane));  // keeps the lanes' word addresses in the call (not hoisted and spilled)
+  uint32_t count = 0;
+#pragma unroll
+  for (uint32_t w0 = 0; w0 < (uint32_t)kMaskWords; w0 += 64u) {
+    if (w0 >= words) break;
+    const uint32_t w = min(w0 + lane, words - 1u);
+    const bool le = w0 + lane < words && 32u * w - p.route.prefix[w] <= u;
+    count += (uint32_t)__popcll(__ballot(le));
   }
+  const uint32_t lo = count - 1u;
   uint32_t zeros = ~p.route.mask[lo];  // unprotected heads of word lo (bits past L*H never reached)
   for (uint32_t k = u - (32u * lo - p.route.prefix[lo]); k > 0; --k) zeros &= zeros - 1u;
   const uint32_t i = 32u * lo + (uint32_t)__builtin_ctz(zeros);
@@ -420,13 +430,21 @@ __global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, u
         store_codes8<BITS>(res, off, pack_code_bits<8, BITS>(cb).w[0]);
       }
     };
-    // The LDS slots are all read before any of them is refilled: the compiler
-    // cannot tell the slots apart, and an LDS read issued after a pending
-    // direct-to-LDS load makes it wait for that load.  The register slots are
-    // refilled one by one (scheduling barriers keep each refill after the
-    // slot's use: hoisted refills would need a second copy of the rows).
+    // The register slots come first, each refilled as soon as it is coded
+    // (scheduling barriers keep each refill after the slot's use: hoisted
+    // refills would need a second copy of the rows), so the next slice's
+    // loads start at once.  The LDS slots are then all read before any of
+    // them is refilled: the compiler cannot tell the slots apart, and an LDS
+    // read issued after a pending direct-to-LDS load makes it wait for that
+    // load.
     auto code_pass = [&](bool refill) {
       const __amdgpu_buffer_rsrc_t r = slice_rsrc(nxt.s);
+#pragma unroll
+      for (int k = 0; k < kResRegSlots; ++k) {
+        emit(v[k], kResLdsSlots + k);
+        __builtin_amdgcn_sched_barrier(0);
+        if (refill) v[k] = load_reg(r, kResLdsSlots + k);
+      }
 #pragma unroll
       for (int j = 0; j < kResLdsSlots; ++j) {
         emit(rows_lds[j][tid], j);
@@ -437,12 +455,6 @@ __global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, u
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int j = 0; j < kResLdsSlots; ++j) load_lds(r, j);
-      }
-#pragma unroll
-      for (int k = 0; k < kResRegSlots; ++k) {
-        emit(v[k], kResLdsSlots + k);
-        __builtin_amdgcn_sched_barrier(0);
-        if (refill) v[k] = load_reg(r, kResLdsSlots + k);
       }
     };
     if (!nxt.valid) {
