@@ -10,8 +10,8 @@
 // Resident (T <= kResRows): a persistent grid, one 1024-thread workgroup per
 // compute unit.  A workgroup takes one 64-channel part of a key slice (l, b, h)
 // and holds all T rows of that part on chip — 9 row slots in LDS, filled by
-// direct global-to-LDS loads, and 15 in registers, 128 rows per slot — so each
-// slice is read from HBM exactly once:
+// buffer loads that write LDS directly, and 15 in registers, 128 rows per
+// slot — so each slice is read from HBM exactly once:
 //  1. per-channel min / max over the resident rows (each lane holds 8
 //     channels of one row per slot), reduced across the wavefront's rows by
 //     shuffles and across the 16 wavefronts through LDS; 64 lanes form the
