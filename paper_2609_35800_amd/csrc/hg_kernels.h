@@ -72,7 +72,9 @@ hipError_t launch_dequantize(const Params& p, int base, int D, int bits, uint32_
                              hipStream_t stream);
 hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
                                 bool norms, hipStream_t stream);
-// KIVI keys over the whole sequence: one workgroup per key slice.
+// KIVI keys over the whole sequence: a persistent grid over the quantized key
+// slices (a 64-channel part of a slice per workgroup, held on chip, when
+// T <= 3072; else a range pass and a code pass per slice).
 hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, hipStream_t stream);
 // Token retention: squared key norms of every image token (p.norm); the k
 // largest per (l, b, h) into p.ret_idx; their rows gathered from p.cache into
