@@ -284,31 +284,39 @@ def main():
     Vo = torch.empty_like(V)
     stream = torch.cuda.current_stream()
 
-    def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
+    # Step i's calls are timed between events bound[i] (recorded before its
+    # quantize: the end of step i-1), mid[i] (between quantize and dequantize)
+    # and bound[i+1]: two event records per step.
+    def step(mid=None, end=None):
         hg.hg_quantize(cfg, K, V, mask, packed, stream=stream)
-        if ev is not None:
-            ev[1].record(stream)
+        if mid is not None and not args.quant_only:
+            mid.record(stream)
         if not args.quant_only:
             hg.hg_dequantize(cfg, mask, packed, Ko, Vo, stream=stream)
-            if ev is not None:
-                ev[2].record(stream)
+        if end is not None:
+            end.record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    new_ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    bound = [new_ev() for _ in range(args.steps + 1)]
+    mid = [new_ev() for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    bound[0].record(stream)
     for i in range(args.steps):
-        step(events[i])
+        step(mid[i], bound[i + 1])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
-    q_ms = [e[0].elapsed_time(e[1]) for e in events]
-    d_ms = [e[1].elapsed_time(e[2]) for e in events] if not args.quant_only else [0.0]
+    if args.quant_only:
+        q_ms = [bound[i].elapsed_time(bound[i + 1]) for i in range(args.steps)]
+        d_ms = [0.0]
+    else:
+        q_ms = [bound[i].elapsed_time(mid[i]) for i in range(args.steps)]
+        d_ms = [mid[i].elapsed_time(bound[i + 1]) for i in range(args.steps)]
     q_avg = float(np.mean(q_ms))
     d_avg = float(np.mean(d_ms))
     step_bytes = ab["quant"] + (0 if args.quant_only else ab["dequant"])
