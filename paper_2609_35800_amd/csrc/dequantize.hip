@@ -107,24 +107,6 @@ __device__ __forceinline__ void dequantize_kivi_keys(const uint8_t* __restrict__
   }
 }
 
-template <int D>
-__device__ __forceinline__ void restore_rows(const uint16_t* __restrict__ side, uint16_t* __restrict__ rows,
-                                             int t_first, int n, int lane) {
-  constexpr int VPT = D / 8;
-  const int nvec = min(kWaveTokens, n - t_first) * VPT;
-  const u32x4* s = (const u32x4*)(side + (size_t)t_first * D);
-  u32x4* d = (u32x4*)(rows + (size_t)t_first * D);
-  constexpr int kMax = kWaveTokens * VPT / 64;
-  u32x4 v[kMax];
-#pragma unroll
-  for (int k = 0; k < kMax; ++k) v[k] = s[min(lane + 64 * k, nvec - 1)];
-#pragma unroll
-  for (int k = 0; k < kMax; ++k) {
-    const int i = lane + 64 * k;
-    if (i < nvec) store_nt(d + i, v[k]);
-  }
-}
-
 template <int BASE, int D, int BITS>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWaves))) void dequantize_kernel(const Params p) {
   const Slice sl = decode_block(p, blockIdx.x);
@@ -137,7 +119,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
   const size_t slab = (size_t)sl.slot * p.B + sl.b;
 
   if (sl.kept) {
-    restore_rows<D>(p.side[sl.X] + slab * p.n * D, rows, t_first, p.n, lane);
+    copy_wave_rows<D, kWaveTokens>(p.side[sl.X] + slab * p.n * D, rows, nullptr, t_first, p.n, lane);
     return;
   }
   const uint8_t* codes = p.codes[sl.X] + slab * p.n * (D * BITS / 8);

@@ -183,33 +183,6 @@ __device__ __forceinline__ void fake_kivi_keys(const uint16_t* rows, uint16_t* o
   }
 }
 
-template <int D, bool NORM>
-__device__ __forceinline__ void fake_copy(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
-                                          float* __restrict__ norm, int t_first, int n, int lane) {
-  constexpr int VPT = D / 8;
-  const int nvec = min(kWaveTokens, n - t_first) * VPT;
-  const u32x4* s = (const u32x4*)(src + (size_t)t_first * D);
-  u32x4* d = (u32x4*)(dst + (size_t)t_first * D);
-  constexpr int kMax = kWaveTokens * VPT / 64;
-  u32x4 v[kMax];
-#pragma unroll
-  for (int k = 0; k < kMax; ++k) v[k] = s[min(lane + 64 * k, nvec - 1)];
-#pragma unroll
-  for (int k = 0; k < kMax; ++k) {
-    const int i = lane + 64 * k;
-    if (i < nvec) store_nt(d + i, v[k]);
-  }
-  if constexpr (NORM) {
-    // vector i holds channels [8c, 8c + 8) of token i / VPT, c = i % VPT
-#pragma unroll
-    for (int k = 0; k < kMax; ++k) {
-      const float sq = row_sqnorm<D>(v[k]);
-      const int i = lane + 64 * k;
-      if (i < nvec && i % VPT == 0) norm[t_first + i / VPT] = sq;
-    }
-  }
-}
-
 // NORM (AKVQ keys, out of place only): also write every image key's squared
 // norm for token retention, from the rows this pass reads anyway.
 template <int BASE, int D, int BITS, bool NORM>
@@ -227,9 +200,9 @@ void fake_quantize_kernel(const Params p) {
   float* norm = NORM ? p.norm + (size_t)sl.s * p.n : nullptr;  // used for K only
   if (sl.kept) {
     if (NORM && sl.X == 0)
-      fake_copy<D, NORM>(rows, out, norm, t_first, p.n, lane);
+      copy_wave_rows<D, kWaveTokens, NORM, false>(rows, out, norm, t_first, p.n, lane);
     else if (out != rows)
-      fake_copy<D, false>(rows, out, nullptr, t_first, p.n, lane);
+      copy_wave_rows<D, kWaveTokens>(rows, out, nullptr, t_first, p.n, lane);
     return;
   }
   if (sl.X == 0 && p.kivi_whole) return;  // whole-sequence KIVI key ranges: kivi_seq.hip

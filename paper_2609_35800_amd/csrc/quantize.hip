@@ -196,36 +196,6 @@ __device__ __forceinline__ void quantize_kivi_keys(const uint16_t* __restrict__ 
   }
 }
 
-// ---------------------------------------------------------- protected copy
-
-template <int D, bool NORM>
-__device__ __forceinline__ void copy_rows(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
-                                          float* __restrict__ norm, int t_first, int n, int lane) {
-  constexpr int VPT = D / 8;  // 16-byte vectors per token
-  const int ntok = min(kWaveTokens, n - t_first);
-  const int nvec = ntok * VPT;
-  const u32x4* s = (const u32x4*)(src + (size_t)t_first * D);
-  u32x4* d = (u32x4*)(dst + (size_t)t_first * D);
-  constexpr int kMax = kWaveTokens * VPT / 64;
-  u32x4 v[kMax];
-#pragma unroll
-  for (int k = 0; k < kMax; ++k) v[k] = s[min(lane + 64 * k, nvec - 1)];
-#pragma unroll
-  for (int k = 0; k < kMax; ++k) {
-    const int i = lane + 64 * k;
-    if (i < nvec) store_nt(d + i, v[k]);
-  }
-  if constexpr (NORM) {
-    // vector i holds channels [8c, 8c + 8) of token i / VPT, c = i % VPT
-#pragma unroll
-    for (int k = 0; k < kMax; ++k) {
-      const float sq = row_sqnorm<D>(v[k]);
-      const int i = lane + 64 * k;
-      if (i < nvec && i % VPT == 0) __builtin_nontemporal_store(sq, norm + t_first + i / VPT);
-    }
-  }
-}
-
 // ---------------------------------------------------------------- kernel
 
 template <int BASE, int D, int BITS, bool NORM>
@@ -242,9 +212,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
   float* norm = NORM ? p.norm + (size_t)sl.s * p.n : nullptr;  // used for K only
   if (sl.kept) {
     if (NORM && sl.X == 0)
-      copy_rows<D, NORM>(rows, p.side[0] + slab * p.n * D, norm, t_first, p.n, lane);
+      copy_wave_rows<D, kWaveTokens, NORM>(rows, p.side[0] + slab * p.n * D, norm, t_first, p.n, lane);
     else
-      copy_rows<D, false>(rows, p.side[sl.X] + slab * p.n * D, nullptr, t_first, p.n, lane);
+      copy_wave_rows<D, kWaveTokens>(rows, p.side[sl.X] + slab * p.n * D, nullptr, t_first, p.n, lane);
     return;
   }
   if (sl.X == 0 && p.kivi_whole) return;  // whole-sequence KIVI key ranges: kivi_seq.hip
