@@ -24,9 +24,8 @@ from conftest import GOLDEN
 # ------------------------------------------------------------- BF16 helpers
 
 def _all_bf16_sorted():
-    bits = (np.arange(65536, dtype=np.uint32) << 16).view(np.float32)
-    vals = bits.astype(np.float64)
-    vals = vals[np.isfinite(vals)]
+    vals = (np.arange(65536, dtype=np.uint32) << 16).view(np.float32)
+    vals = vals[np.isfinite(vals)].astype(np.float64)  # NaN patterns dropped before the cast
     return np.unique(vals)  # sorted, -0 and +0 merge
 
 
