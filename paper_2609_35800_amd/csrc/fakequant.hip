@@ -18,13 +18,6 @@
 
 namespace hg {
 
-// LDS slot of (token, chunk) in a one-pass stage (16 tokens, 8 at head_dim
-// 256) of D/8 16-byte chunks per token, XOR-swizzled by token so that the
-// per-token-group writes spread over the banks.
-template <int D>
-__device__ __forceinline__ constexpr int fq_slot(int t, int c) {
-  return t * (D / 8) + (c ^ (D == 64 ? ((t >> 1) & 1) : (t & 3)));
-}
 
 template <int D, int BITS, bool ROTATE, bool NORM>
 // rows and out may be the same memory (in place): no restrict qualifiers.
@@ -103,7 +96,7 @@ __device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out,
       for (int k = 0; k < NV; ++k) {
         const u32x4 v = {pack_bf16x2_hw(x[8 * k + 0], x[8 * k + 1]), pack_bf16x2_hw(x[8 * k + 2], x[8 * k + 3]),
                          pack_bf16x2_hw(x[8 * k + 4], x[8 * k + 5]), pack_bf16x2_hw(x[8 * k + 6], x[8 * k + 7])};
-        stage[fq_slot<D>(q, j * NV + k)] = v;
+        stage[stage_slot<D>(q, j * NV + k)] = v;
       }
       // LDS operations of one wavefront execute in order; the fences keep the
       // compiler from moving the accesses across each other.
@@ -114,7 +107,7 @@ __device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out,
       for (int k = 0; k < NSP; ++k) {
         const int tl = r + RPL * k;
         const int t = t_first + (p0 + pass) * TPP + tl;
-        const u32x4 v = stage[fq_slot<D>(tl, c)];
+        const u32x4 v = stage[stage_slot<D>(tl, c)];
         if (t < n) store_nt((u32x4*)(out + (size_t)t * D + 8 * c), v);
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -209,7 +202,7 @@ void fake_quantize_kernel(const Params p) {
   if (BASE == HG_BASE_KIVI && sl.X == 0) {
     fake_kivi_keys<D, BITS>(rows, out, t_first, p.n, lane);
   } else {
-    __shared__ u32x4 stage_all[kThreads / 64][(64 / kTokenLanes<D>) * (D / 8)];
+    __shared__ u32x4 stage_all[kThreads / 64][(64 / kTokenLanes<D>) * (D / 8)];  // one pass of tokens
     if (BASE == HG_BASE_AKVQ && sl.X == 0)
       fake_tokens<D, BITS, true, NORM>(rows, out, norm, t_first, p.n, lane, stage_all[wave]);
     else

@@ -458,6 +458,15 @@ __device__ __forceinline__ uint32_t load_piece8(const uint8_t* row, int c) {
   }
 }
 
+// Slot of 16-byte chunk c of token t in a wavefront's LDS stage of D/8
+// chunks per token, XOR-swizzled so that both the row layout (a token row
+// across D/8 lanes) and the quad layout (a token across 4 or 8 lanes) access
+// the stage without heavy bank conflicts.
+template <int D>
+__device__ __forceinline__ constexpr int stage_slot(int t, int c) {
+  return t * (D / 8) + (c ^ (D == 64 ? ((t >> 1) & 1) : (t & 3)));
+}
+
 __device__ __forceinline__ void store_nt(u32x4* dst, u32x4 v) {
   __builtin_nontemporal_store(v, dst);
 }
