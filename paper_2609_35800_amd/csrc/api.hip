@@ -282,7 +282,7 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
     return fail(HG_ERR_SHAPE, "grid of %llu workgroups too large", (unsigned long long)(2 * blocks_k));
   p.blocks_k = (uint32_t)blocks_k;
   hipError_t e = quantize ? hg::launch_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), retain, stream)
-                          : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), stream);
+                          : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, stream);
   if (e == hipSuccess && quantize && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, false, stream);
   if (e == hipSuccess && p.k > 0 && quantize) {
     e = hg::launch_retain_select(p, cfg->D, hg::RowCopy::kGather, stream);

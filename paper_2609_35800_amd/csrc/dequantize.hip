@@ -7,28 +7,37 @@
 // even, subnormals kept).  AKVQ keys are rotated back in fp32 before the BF16 rounding.
 // Protected rows come back from the side store; text rows are not written.
 //
-// Same tiling as the quantize kernels (a workgroup owns one (tensor, l, b, h)
-// slice and 128 image tokens, a wavefront 32 of them), but every path holds a
-// token row across D/8 lanes so that stores are whole contiguous rows.
+// A workgroup owns one (tensor, l, b, h) slice and 4 wavefront tiles of
+// consecutive image tokens (kDequantTokens per wavefront), and every path
+// holds a token row across D/8 lanes so that stores are whole contiguous rows.
 
 #include "hg_device.h"
 #include "hg_kernels.h"
 
 namespace hg {
 
+// Tokens per wavefront tile.  Stores are 80 % of the traffic, and write
+// throughput falls with the store instructions a wavefront issues back to
+// back (measured write-only: one 1 KiB store per wavefront 6.8 TB/s, two
+// 6.1-6.4, eight 5.5-5.8), so the min-max and KIVI-style paths at head_dim
+// 128 take 16 tokens (four stores of whole rows).  The rotated AKVQ keys and
+// head_dim 256 measured slower with the shorter tile and keep 32.
+template <int BASE, int D>
+constexpr int kDequantTokens = (D == 128 && BASE != HG_BASE_AKVQ) ? 16 : kWaveTokens;
+
 // Per-token groups.  A token row is held by D/8 lanes, lane c holding
 // channels [8c, 8c + 8), so each 16-byte store instruction of the wavefront
 // writes 64/(D/8) whole consecutive token rows (one contiguous 1 KiB run for
 // D = 128; two 512-byte rows at 256).  AKVQ keys are rotated back across the
 // row's lanes first.
-template <int D, int BITS, bool ROTATE>
+template <int D, int BITS, bool ROTATE, int TOKENS>
 __device__ __forceinline__ void dequantize_tokens(const uint8_t* __restrict__ codes,
                                                   const uint32_t* __restrict__ meta,
                                                   uint16_t* __restrict__ rows,
                                                   int t_first, int n, int lane) {
   constexpr int LPT = D / 8;               // lanes per token row
   constexpr int TPI = 64 / LPT;            // token rows per instruction
-  constexpr int NP = kWaveTokens / TPI;    // instructions per wavefront tile
+  constexpr int NP = TOKENS / TPI;         // instructions per wavefront tile
   constexpr int ROW = D * BITS / 8;
   constexpr uint32_t kMask = (1u << BITS) - 1u;
   const int c = lane % LPT;
@@ -59,7 +68,7 @@ __device__ __forceinline__ void dequantize_tokens(const uint8_t* __restrict__ co
   }
 }
 
-template <int D, int BITS>
+template <int D, int BITS, int TOKENS>
 __device__ __forceinline__ void dequantize_kivi_keys(const uint8_t* __restrict__ codes,
                                                      const uint32_t* __restrict__ meta,
                                                      uint16_t* __restrict__ rows,
@@ -67,7 +76,7 @@ __device__ __forceinline__ void dequantize_kivi_keys(const uint8_t* __restrict__
   constexpr int DH = D < 128 ? D : 128;  // channels per pass (head_dim 256: two passes)
   constexpr int LPR = DH / 8;
   constexpr int RPL = 64 / LPR;
-  constexpr int NL = kWaveTokens / RPL;
+  constexpr int NL = TOKENS / RPL;
   constexpr int ROW = D * BITS / 8;
   const int r = lane / LPR;
 
@@ -112,62 +121,69 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
   const Slice sl = decode_block(p, blockIdx.x);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int t_first = sl.tile * kBlockTokens + wave * kWaveTokens;
+  constexpr int kTokens = kDequantTokens<BASE, D>;
+  const int t_first = sl.tile * (kThreads / 64) * kTokens + wave * kTokens;
   if (t_first >= p.n) return;
 
   uint16_t* rows = const_cast<uint16_t*>(p.cache[sl.X]) + ((size_t)sl.s * p.T + p.s0) * D;
   const size_t slab = (size_t)sl.slot * p.B + sl.b;
 
   if (sl.kept) {
-    copy_wave_rows<D, kWaveTokens>(p.side[sl.X] + slab * p.n * D, rows, nullptr, t_first, p.n, lane);
+    copy_wave_rows<D, kTokens>(p.side[sl.X] + slab * p.n * D, rows, nullptr, t_first, p.n, lane);
     return;
   }
   const uint8_t* codes = p.codes[sl.X] + slab * p.n * (D * BITS / 8);
   if (BASE == HG_BASE_KIVI && sl.X == 0) {
-    const int group = p.kivi_whole ? 0 : t_first / kWaveTokens;
-    dequantize_kivi_keys<D, BITS>(codes, p.meta[0] + slab * p.ngroups * D, rows, t_first, group, p.n, lane);
+    const int group = p.kivi_whole ? 0 : t_first / kWaveTokens;  // 32-token key groups
+    dequantize_kivi_keys<D, BITS, kTokens>(codes, p.meta[0] + slab * p.ngroups * D, rows, t_first, group, p.n, lane);
   } else {
     const uint32_t* meta = p.meta[sl.X] + slab * p.n;
     if (BASE == HG_BASE_AKVQ && sl.X == 0)
-      dequantize_tokens<D, BITS, true>(codes, meta, rows, t_first, p.n, lane);
+      dequantize_tokens<D, BITS, true, kTokens>(codes, meta, rows, t_first, p.n, lane);
     else
-      dequantize_tokens<D, BITS, false>(codes, meta, rows, t_first, p.n, lane);
+      dequantize_tokens<D, BITS, false, kTokens>(codes, meta, rows, t_first, p.n, lane);
   }
 }
 
+// The workgroup tiles of the launch follow this kernel's tile size.
 template <int BASE, int D, int BITS>
-static hipError_t launch_d(const Params& p, uint32_t blocks, hipStream_t stream) {
-  hipLaunchKernelGGL((dequantize_kernel<BASE, D, BITS>), dim3(blocks), dim3(kThreads),
-                     occupancy_lds(kDequantizeWaves), stream, p);
+static hipError_t launch_d(const Params& p, hipStream_t stream) {
+  constexpr int kTile = (kThreads / 64) * kDequantTokens<BASE, D>;
+  Params pd = p;
+  pd.tiles = (p.n + kTile - 1) / kTile;
+  const uint64_t blocks_k = (uint64_t)p.L * p.B * p.H * (uint64_t)pd.tiles;
+  if (2 * blocks_k > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
+  pd.blocks_k = (uint32_t)blocks_k;
+  hipLaunchKernelGGL((dequantize_kernel<BASE, D, BITS>), dim3((uint32_t)(2 * blocks_k)), dim3(kThreads),
+                     occupancy_lds(kDequantizeWaves), stream, pd);
   return hipGetLastError();
 }
 
 template <int BASE, int D>
-static hipError_t launch_d_bits(const Params& p, int bits, uint32_t blocks, hipStream_t stream) {
+static hipError_t launch_d_bits(const Params& p, int bits, hipStream_t stream) {
   switch (bits) {
-    case 2: return launch_d<BASE, D, 2>(p, blocks, stream);
-    case 3: return launch_d<BASE, D, 3>(p, blocks, stream);
-    case 4: return launch_d<BASE, D, 4>(p, blocks, stream);
+    case 2: return launch_d<BASE, D, 2>(p, stream);
+    case 3: return launch_d<BASE, D, 3>(p, stream);
+    case 4: return launch_d<BASE, D, 4>(p, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int BASE>
-static hipError_t launch_d_dim(const Params& p, int D, int bits, uint32_t blocks, hipStream_t stream) {
+static hipError_t launch_d_dim(const Params& p, int D, int bits, hipStream_t stream) {
   switch (D) {
-    case 64: return launch_d_bits<BASE, 64>(p, bits, blocks, stream);
-    case 128: return launch_d_bits<BASE, 128>(p, bits, blocks, stream);
-    case 256: return launch_d_bits<BASE, 256>(p, bits, blocks, stream);
+    case 64: return launch_d_bits<BASE, 64>(p, bits, stream);
+    case 128: return launch_d_bits<BASE, 128>(p, bits, stream);
+    case 256: return launch_d_bits<BASE, 256>(p, bits, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_dequantize(const Params& p, int base, int D, int bits, uint32_t blocks,
-                             hipStream_t stream) {
+hipError_t launch_dequantize(const Params& p, int base, int D, int bits, hipStream_t stream) {
   switch (base) {
-    case HG_BASE_MINMAX: return launch_d_dim<HG_BASE_MINMAX>(p, D, bits, blocks, stream);
-    case HG_BASE_KIVI: return launch_d_dim<HG_BASE_KIVI>(p, D, bits, blocks, stream);
-    case HG_BASE_AKVQ: return launch_d_dim<HG_BASE_AKVQ>(p, D, bits, blocks, stream);
+    case HG_BASE_MINMAX: return launch_d_dim<HG_BASE_MINMAX>(p, D, bits, stream);
+    case HG_BASE_KIVI: return launch_d_dim<HG_BASE_KIVI>(p, D, bits, stream);
+    case HG_BASE_AKVQ: return launch_d_dim<HG_BASE_AKVQ>(p, D, bits, stream);
     default: return hipErrorInvalidValue;
   }
 }

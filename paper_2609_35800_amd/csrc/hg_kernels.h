@@ -68,8 +68,9 @@ struct Params {
 // With `norms`, the quantize kernel also writes the squared key norms (AKVQ).
 hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
                            bool norms, hipStream_t stream);
-hipError_t launch_dequantize(const Params& p, int base, int D, int bits, uint32_t blocks,
-                             hipStream_t stream);
+// (The dequantize launch sizes its own grid: its tiles can be shorter than
+// kBlockTokens.)
+hipError_t launch_dequantize(const Params& p, int base, int D, int bits, hipStream_t stream);
 hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
                                 bool norms, hipStream_t stream);
 // KIVI keys over the whole sequence: a persistent grid over the quantized key
