@@ -366,7 +366,7 @@ int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
     }
   }
   if (e == hipSuccess)
-    e = hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), fused, stream);
+    e = hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, fused, stream);
   if (e == hipSuccess && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, true, stream);
   if (e == hipSuccess && fused) {
     e = hg::launch_retain_select(p, cfg->D, hg::RowCopy::kCacheToOut, stream);

@@ -18,8 +18,16 @@
 
 namespace hg {
 
+// Tokens per wavefront tile.  Half of the traffic is stores, and write
+// throughput falls with the store instructions a wavefront issues back to
+// back, so the min-max instantiation at head_dim 128 (min-max caches, and
+// the value tiles of the other bases) takes 16 tokens, one pass.  KIVI key
+// groups need their 32 tokens in one wavefront.
+template <int BASE, int D>
+constexpr int kFakeTokens = (D == 128 && BASE == HG_BASE_MINMAX) ? 16 : kWaveTokens;
 
-template <int D, int BITS, bool ROTATE, bool NORM>
+
+template <int D, int BITS, bool ROTATE, bool NORM, int TOKENS>
 // rows and out may be the same memory (in place): no restrict qualifiers.
 __device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out, float* norm,
                                             int t_first, int n, int lane, u32x4* __restrict__ stage) {
@@ -27,7 +35,8 @@ __device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out,
   constexpr int E = D / G;             // elements per lane
   constexpr int NV = E / 8;            // 16-byte chunks per lane
   constexpr int TPP = 64 / G;          // tokens per pass
-  constexpr int PASSES = kWaveTokens / TPP;
+  constexpr int PASSES = TOKENS / TPP;
+  constexpr int PB = PASSES < 2 ? PASSES : 2;  // passes whose loads are issued together
   constexpr int CPT = D / 8;           // chunks per token row
   constexpr int RPL = 64 / CPT;        // token rows per store instruction
   constexpr int NSP = TPP / RPL;       // store instructions per pass
@@ -36,11 +45,11 @@ __device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out,
   const int q = lane / G;
 
 #pragma unroll
-  for (int p0 = 0; p0 < PASSES; p0 += 2) {
+  for (int p0 = 0; p0 < PASSES; p0 += PB) {
     // Tokens past the span's end load the last token (never stored).
-    u32x4 raw[2][NV];
+    u32x4 raw[PB][NV];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < PB; ++b) {
       const int t = min(t_first + (p0 + b) * TPP + q, n - 1);
       const u32x4* src = (const u32x4*)(rows + (size_t)t * D + j * E);
 #pragma unroll
@@ -49,9 +58,9 @@ __device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out,
 
     // Rotated keys unroll both passes: rolled, their per-pass register arrays
     // went to scratch memory.  The plain path is faster rolled (measured).
-    constexpr int kUnrolledPasses = ROTATE ? 2 : 1;
+    constexpr int kUnrolledPasses = ROTATE ? PB : 1;
 #pragma unroll kUnrolledPasses
-    for (int pass = 0; pass < 2; ++pass) {
+    for (int pass = 0; pass < PB; ++pass) {
       float x[E];
 #pragma unroll
       for (int k = 0; k < NV; ++k) {
@@ -184,7 +193,8 @@ void fake_quantize_kernel(const Params p) {
   const Slice sl = decode_block(p, blockIdx.x);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int t_first = sl.tile * kBlockTokens + wave * kWaveTokens;
+  constexpr int kTokens = kFakeTokens<BASE, D>;
+  const int t_first = sl.tile * (kThreads / 64) * kTokens + wave * kTokens;
   if (t_first >= p.n) return;
 
   const size_t base = ((size_t)sl.s * p.T + p.s0) * D;
@@ -193,53 +203,66 @@ void fake_quantize_kernel(const Params p) {
   float* norm = NORM ? p.norm + (size_t)sl.s * p.n : nullptr;  // used for K only
   if (sl.kept) {
     if (NORM && sl.X == 0)
-      copy_wave_rows<D, kWaveTokens, NORM, false>(rows, out, norm, t_first, p.n, lane);
+      copy_wave_rows<D, kTokens, NORM, false>(rows, out, norm, t_first, p.n, lane);
     else if (out != rows)
-      copy_wave_rows<D, kWaveTokens>(rows, out, nullptr, t_first, p.n, lane);
+      copy_wave_rows<D, kTokens>(rows, out, nullptr, t_first, p.n, lane);
     return;
   }
   if (sl.X == 0 && p.kivi_whole) return;  // whole-sequence KIVI key ranges: kivi_seq.hip
   if (BASE == HG_BASE_KIVI && sl.X == 0) {
+    static_assert(BASE != HG_BASE_KIVI || kTokens == kWaveTokens, "a wavefront holds a whole key group");
     fake_kivi_keys<D, BITS>(rows, out, t_first, p.n, lane);
   } else {
     __shared__ u32x4 stage_all[kThreads / 64][(64 / kTokenLanes<D>) * (D / 8)];  // one pass of tokens
     if (BASE == HG_BASE_AKVQ && sl.X == 0)
-      fake_tokens<D, BITS, true, NORM>(rows, out, norm, t_first, p.n, lane, stage_all[wave]);
+      fake_tokens<D, BITS, true, NORM, kTokens>(rows, out, norm, t_first, p.n, lane, stage_all[wave]);
     else
-      fake_tokens<D, BITS, false, false>(rows, out, nullptr, t_first, p.n, lane, stage_all[wave]);
+      fake_tokens<D, BITS, false, false, kTokens>(rows, out, nullptr, t_first, p.n, lane, stage_all[wave]);
   }
 }
 
+// Tensors a launch covers: K and V, or one of them.
+enum class Tensors { kBoth, kKeys, kValues };
+
+// The workgroup tiles of a launch follow its kernel's tile size.
 template <int BASE, int D, int BITS>
-static hipError_t launch_f(const Params& p, uint32_t blocks, bool norms, hipStream_t stream) {
+static hipError_t launch_f(const Params& p, Tensors which, bool norms, hipStream_t stream) {
+  constexpr int kTile = (kThreads / 64) * kFakeTokens<BASE, D>;
+  Params pf = p;
+  pf.tiles = (p.n + kTile - 1) / kTile;
+  const uint64_t per_tensor = (uint64_t)p.L * p.B * p.H * (uint64_t)pf.tiles;
+  const uint64_t blocks = which == Tensors::kBoth ? 2 * per_tensor : per_tensor;
+  if (blocks > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
+  pf.blocks_k = which == Tensors::kValues ? 0u : (uint32_t)per_tensor;
   if constexpr (BASE == HG_BASE_AKVQ) {
     if (norms) {
-      hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS, true>), dim3(blocks), dim3(kThreads), 0, stream, p);
+      hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS, true>), dim3((uint32_t)blocks), dim3(kThreads), 0,
+                         stream, pf);
       return hipGetLastError();
     }
   }
   if (norms) return hipErrorInvalidValue;  // key norms belong to the AKVQ base
-  hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS, false>), dim3(blocks), dim3(kThreads), 0, stream, p);
+  hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS, false>), dim3((uint32_t)blocks), dim3(kThreads), 0,
+                     stream, pf);
   return hipGetLastError();
 }
 
 template <int BASE, int D>
-static hipError_t launch_f_bits(const Params& p, int bits, uint32_t blocks, bool norms, hipStream_t stream) {
+static hipError_t launch_f_bits(const Params& p, int bits, Tensors which, bool norms, hipStream_t stream) {
   switch (bits) {
-    case 2: return launch_f<BASE, D, 2>(p, blocks, norms, stream);
-    case 3: return launch_f<BASE, D, 3>(p, blocks, norms, stream);
-    case 4: return launch_f<BASE, D, 4>(p, blocks, norms, stream);
+    case 2: return launch_f<BASE, D, 2>(p, which, norms, stream);
+    case 3: return launch_f<BASE, D, 3>(p, which, norms, stream);
+    case 4: return launch_f<BASE, D, 4>(p, which, norms, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int BASE>
-static hipError_t launch_f_dim(const Params& p, int D, int bits, uint32_t blocks, bool norms,
-                               hipStream_t stream) {
+static hipError_t launch_f_dim(const Params& p, int D, int bits, Tensors which, bool norms, hipStream_t stream) {
   switch (D) {
-    case 64: return launch_f_bits<BASE, 64>(p, bits, blocks, norms, stream);
-    case 128: return launch_f_bits<BASE, 128>(p, bits, blocks, norms, stream);
-    case 256: return launch_f_bits<BASE, 256>(p, bits, blocks, norms, stream);
+    case 64: return launch_f_bits<BASE, 64>(p, bits, which, norms, stream);
+    case 128: return launch_f_bits<BASE, 128>(p, bits, which, norms, stream);
+    case 256: return launch_f_bits<BASE, 256>(p, bits, which, norms, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -248,18 +271,14 @@ static hipError_t launch_f_dim(const Params& p, int D, int bits, uint32_t blocks
 // min-max instantiation, which needs fewer registers than their key paths
 // (as in launch_quantize); with KIVI keys over the whole sequence the whole
 // launch does.
-hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, uint32_t blocks, bool norms,
-                                hipStream_t stream) {
+hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, bool norms, hipStream_t stream) {
   if (base == HG_BASE_MINMAX || (base == HG_BASE_KIVI && p.kivi_whole))
-    return launch_f_dim<HG_BASE_MINMAX>(p, D, bits, blocks, norms, stream);
+    return launch_f_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kBoth, norms, stream);
   if (base != HG_BASE_KIVI && base != HG_BASE_AKVQ) return hipErrorInvalidValue;
-  const uint32_t blocks_v = blocks - p.blocks_k;
-  hipError_t e = base == HG_BASE_KIVI ? launch_f_dim<HG_BASE_KIVI>(p, D, bits, p.blocks_k, norms, stream)
-                                      : launch_f_dim<HG_BASE_AKVQ>(p, D, bits, p.blocks_k, norms, stream);
-  if (e != hipSuccess || blocks_v == 0) return e;
-  Params pv = p;
-  pv.blocks_k = 0;  // every block of this launch is a value tile
-  return launch_f_dim<HG_BASE_MINMAX>(pv, D, bits, blocks_v, false, stream);
+  hipError_t e = base == HG_BASE_KIVI ? launch_f_dim<HG_BASE_KIVI>(p, D, bits, Tensors::kKeys, norms, stream)
+                                      : launch_f_dim<HG_BASE_AKVQ>(p, D, bits, Tensors::kKeys, norms, stream);
+  if (e != hipSuccess) return e;
+  return launch_f_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kValues, false, stream);
 }
 
 }  // namespace hg

@@ -41,7 +41,9 @@ struct Route {
 
 // One launch covers K (tensor 0) and V (tensor 1): blocks [0, blocks_k) take
 // K tiles, the rest V tiles.  Each block takes one (tensor, l, b, h) slice and
-// kBlockTokens consecutive image tokens of it.
+// one of its `tiles` runs of consecutive image tokens: kBlockTokens as the
+// host sets them; the dequantize and one-pass launchers reset tiles and
+// blocks_k for kernels whose wavefronts take fewer tokens.
 struct Params {
   const uint16_t* cache[2];  // quantize, fake quantize: K, V input; dequantize: K_out, V_out
   uint16_t* out[2];          // fake quantize: K_out, V_out (may equal the input)
@@ -53,7 +55,7 @@ struct Params {
   int32_t keys_only;
   int32_t kivi_whole;        // KIVI keys: one range over the whole sequence (kivi_seq.hip)
   int32_t ngroups;           // KIVI key groups per slice
-  int32_t tiles;             // kBlockTokens tiles per slice
+  int32_t tiles;             // workgroup tiles per slice
   int32_t n_unprot_k;        // heads (l, h) whose keys are quantized
   uint32_t blocks_k;         // blocks of tensor K
   // AKVQ-style token retention
@@ -68,11 +70,10 @@ struct Params {
 // With `norms`, the quantize kernel also writes the squared key norms (AKVQ).
 hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
                            bool norms, hipStream_t stream);
-// (The dequantize launch sizes its own grid: its tiles can be shorter than
-// kBlockTokens.)
+// (The dequantize and one-pass launches size their own grids: their tiles can
+// be shorter than kBlockTokens.)
 hipError_t launch_dequantize(const Params& p, int base, int D, int bits, hipStream_t stream);
-hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
-                                bool norms, hipStream_t stream);
+hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, bool norms, hipStream_t stream);
 // KIVI keys over the whole sequence: a persistent grid over the quantized key
 // slices (a 64-channel part of a slice per workgroup, held on chip, when
 // T <= 3072; else a range pass and a code pass per slice).
