@@ -147,43 +147,49 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
 
 // The workgroup tiles of the launch follow this kernel's tile size.
 template <int BASE, int D, int BITS>
-static hipError_t launch_d(const Params& p, hipStream_t stream) {
+static hipError_t launch_d(const Params& p, Tensors which, hipStream_t stream) {
   constexpr int kTile = (kThreads / 64) * kDequantTokens<BASE, D>;
   Params pd = p;
   pd.tiles = (p.n + kTile - 1) / kTile;
-  const uint64_t blocks_k = (uint64_t)p.L * p.B * p.H * (uint64_t)pd.tiles;
-  if (2 * blocks_k > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
-  pd.blocks_k = (uint32_t)blocks_k;
-  hipLaunchKernelGGL((dequantize_kernel<BASE, D, BITS>), dim3((uint32_t)(2 * blocks_k)), dim3(kThreads),
+  const uint64_t per_tensor = (uint64_t)p.L * p.B * p.H * (uint64_t)pd.tiles;
+  const uint64_t blocks = which == Tensors::kBoth ? 2 * per_tensor : per_tensor;
+  if (blocks > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
+  pd.blocks_k = which == Tensors::kValues ? 0u : (uint32_t)per_tensor;
+  hipLaunchKernelGGL((dequantize_kernel<BASE, D, BITS>), dim3((uint32_t)blocks), dim3(kThreads),
                      occupancy_lds(kDequantizeWaves), stream, pd);
   return hipGetLastError();
 }
 
 template <int BASE, int D>
-static hipError_t launch_d_bits(const Params& p, int bits, hipStream_t stream) {
+static hipError_t launch_d_bits(const Params& p, int bits, Tensors which, hipStream_t stream) {
   switch (bits) {
-    case 2: return launch_d<BASE, D, 2>(p, stream);
-    case 3: return launch_d<BASE, D, 3>(p, stream);
-    case 4: return launch_d<BASE, D, 4>(p, stream);
+    case 2: return launch_d<BASE, D, 2>(p, which, stream);
+    case 3: return launch_d<BASE, D, 3>(p, which, stream);
+    case 4: return launch_d<BASE, D, 4>(p, which, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int BASE>
-static hipError_t launch_d_dim(const Params& p, int D, int bits, hipStream_t stream) {
+static hipError_t launch_d_dim(const Params& p, int D, int bits, Tensors which, hipStream_t stream) {
   switch (D) {
-    case 64: return launch_d_bits<BASE, 64>(p, bits, stream);
-    case 128: return launch_d_bits<BASE, 128>(p, bits, stream);
-    case 256: return launch_d_bits<BASE, 256>(p, bits, stream);
+    case 64: return launch_d_bits<BASE, 64>(p, bits, which, stream);
+    case 128: return launch_d_bits<BASE, 128>(p, bits, which, stream);
+    case 256: return launch_d_bits<BASE, 256>(p, bits, which, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
+// AKVQ-style values are dequantized per token exactly as min-max ones, so
+// they run as a launch of the min-max instantiation, with its shorter tiles.
 hipError_t launch_dequantize(const Params& p, int base, int D, int bits, hipStream_t stream) {
   switch (base) {
-    case HG_BASE_MINMAX: return launch_d_dim<HG_BASE_MINMAX>(p, D, bits, stream);
-    case HG_BASE_KIVI: return launch_d_dim<HG_BASE_KIVI>(p, D, bits, stream);
-    case HG_BASE_AKVQ: return launch_d_dim<HG_BASE_AKVQ>(p, D, bits, stream);
+    case HG_BASE_MINMAX: return launch_d_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kBoth, stream);
+    case HG_BASE_KIVI: return launch_d_dim<HG_BASE_KIVI>(p, D, bits, Tensors::kBoth, stream);
+    case HG_BASE_AKVQ: {
+      const hipError_t e = launch_d_dim<HG_BASE_AKVQ>(p, D, bits, Tensors::kKeys, stream);
+      return e != hipSuccess ? e : launch_d_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kValues, stream);
+    }
     default: return hipErrorInvalidValue;
   }
 }

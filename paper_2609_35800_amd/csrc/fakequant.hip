@@ -221,9 +221,6 @@ void fake_quantize_kernel(const Params p) {
   }
 }
 
-// Tensors a launch covers: K and V, or one of them.
-enum class Tensors { kBoth, kKeys, kValues };
-
 // The workgroup tiles of a launch follow its kernel's tile size.
 template <int BASE, int D, int BITS>
 static hipError_t launch_f(const Params& p, Tensors which, bool norms, hipStream_t stream) {

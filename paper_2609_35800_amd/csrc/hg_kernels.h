@@ -66,6 +66,9 @@ struct Params {
   Route route;
 };
 
+// Tensors a launch covers: K and V, or one of them.
+enum class Tensors { kBoth, kKeys, kValues };
+
 // Dispatch over (base, D, bits); return hipSuccess or the launch error.
 // With `norms`, the quantize kernel also writes the squared key norms (AKVQ).
 hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
