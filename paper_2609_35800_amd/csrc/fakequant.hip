@@ -7,8 +7,9 @@
 // of traffic per element instead of about 4.6.  Protected rows are copied
 // (or left alone when the output is the input); text rows are not written.
 //
-// Work decomposition as in quantize.hip (a workgroup per slice and 128 image
-// tokens, 32 per wavefront).  Per-token groups are computed with a lane quad
+// Work decomposition as in quantize.hip (a workgroup per slice and four
+// wavefront tiles of 32 image tokens; 16 in the min-max instantiation at
+// head_dim 128, see kFakeTokens).  Per-token groups are computed with a lane quad
 // per token and the reconstructed rows are transposed through LDS so that
 // every store instruction writes whole consecutive token rows; KIVI keys are
 // computed and stored in the whole-row load layout directly.
