@@ -63,7 +63,7 @@ def test_small(w, inplace):
 
 
 @pytest.mark.parametrize("base", ["minmax", "kivi", "akvq"])
-@pytest.mark.parametrize("img_len", [1, 31, 33, 129, 257])
+@pytest.mark.parametrize("img_len", [1, 16, 17, 31, 33, 63, 65, 129, 257])  # 16- and 64-token tiles too
 def test_ragged(base, img_len):
     w = small(base, img_len=img_len, img_start=3, text=2, L=1, B=2, H=2, n_protected=1)
     K, V = synthkv.gen_kv(w)

@@ -3,8 +3,8 @@ bytes.  Packed codes, metadata and the BF16 side store must be bit-exact;
 dequantized BF16 within 1 BF16 ulp (expected: 0).  Text rows must stay
 untouched and canary bytes after every output buffer intact.
 
-Small shapes are compared element by element and span several 128-token
-workgroup tiles with ragged tails; every base, head_dim, bit width and
+Small shapes are compared element by element and span several workgroup
+tiles (128 tokens; 64 in dequantize) with ragged tails; every base, head_dim, bit width and
 protection mode is covered, with special values (constant tokens, signed
 zeros, tiny/subnormal ranges, exact ties, large magnitudes) and degenerate
 masks and spans."""
@@ -55,7 +55,9 @@ def test_tiny_workload():
 
 
 @pytest.mark.parametrize("base", ["minmax", "kivi", "akvq"])
-@pytest.mark.parametrize("img_len", [1, 5, 31, 32, 33, 127, 128, 129, 257])
+# (16, 17, 48, 63 and 65 end at or just past the 16-token wavefront tiles and
+# 64-token workgroup tiles of the dequantize kernels)
+@pytest.mark.parametrize("img_len", [1, 5, 16, 17, 31, 32, 33, 48, 63, 65, 127, 128, 129, 257])
 def test_ragged_spans(base, img_len):
     w = small(base, img_len=img_len, img_start=3, text=2, L=1, B=2, H=2, n_protected=1)
     K, V = synthkv.gen_kv(w)
