@@ -222,6 +222,13 @@ void fake_quantize_kernel(const Params p) {
   }
 }
 
+// Dynamic LDS of a one-pass launch: the occupancy cap's reservation, less the
+// static stage of the per-token path.
+template <int D>
+constexpr size_t fake_lds() {
+  return occupancy_lds(kFakeQuantizeWaves) - (kThreads / 64) * (64 / kTokenLanes<D>) * (D / 8) * 16;
+}
+
 // The workgroup tiles of a launch follow its kernel's tile size.
 template <int BASE, int D, int BITS>
 static hipError_t launch_f(const Params& p, Tensors which, bool norms, hipStream_t stream) {
@@ -234,13 +241,13 @@ static hipError_t launch_f(const Params& p, Tensors which, bool norms, hipStream
   pf.blocks_k = which == Tensors::kValues ? 0u : (uint32_t)per_tensor;
   if constexpr (BASE == HG_BASE_AKVQ) {
     if (norms) {
-      hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS, true>), dim3((uint32_t)blocks), dim3(kThreads), 0,
+      hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS, true>), dim3((uint32_t)blocks), dim3(kThreads), fake_lds<D>(),
                          stream, pf);
       return hipGetLastError();
     }
   }
   if (norms) return hipErrorInvalidValue;  // key norms belong to the AKVQ base
-  hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS, false>), dim3((uint32_t)blocks), dim3(kThreads), 0,
+  hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS, false>), dim3((uint32_t)blocks), dim3(kThreads), fake_lds<D>(),
                      stream, pf);
   return hipGetLastError();
 }

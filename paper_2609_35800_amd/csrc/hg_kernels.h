@@ -29,6 +29,9 @@ constexpr size_t occupancy_lds(int waves) { return waves > 0 ? kLdsPerCU / (wave
 // already allow fewer, such as KIVI key groups at 4, are not affected).
 constexpr int kQuantizeWaves = 6;
 constexpr int kDequantizeWaves = 6;
+// The one-pass kernels: 4 (0.3-1 % faster than uncapped or 6 on the Qwen-,
+// 72B- and LLaVA-NeXT-shaped caches, InternVL-shaped unchanged).
+constexpr int kFakeQuantizeWaves = 4;
 
 // Mask routing in kernel arguments: bit i of `mask` marks protected head
 // i = l*H + h; `prefix[w]` counts protected heads in words before w, so the
