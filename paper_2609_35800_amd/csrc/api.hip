@@ -134,6 +134,16 @@ int check_buffers(const Buf* bufs, int nb) {
   return HG_OK;
 }
 
+// The call's largest tiled grid (K and V, workgroup tiles of as few as
+// kMinBlockTokens tokens) must fit the launch limit; checked before any launch.
+int check_grid(const hg_config* c) {
+  const uint64_t tiles = ((uint64_t)c->img_len + hg::kMinBlockTokens - 1) / hg::kMinBlockTokens;
+  const uint64_t blocks = 2 * (uint64_t)c->L * c->B * c->H * tiles;
+  if (blocks > 0x7FFFFFFFull)
+    return fail(HG_ERR_SHAPE, "grid of %llu workgroups too large", (unsigned long long)blocks);
+  return HG_OK;
+}
+
 void fill_params(hg::Params& p, const hg_config* c, const uint8_t* mask) {
   memset(&p, 0, sizeof p);
   p.L = c->L;
@@ -219,6 +229,7 @@ int hg_packed_sizes(const hg_config* cfg, const uint8_t* mask, hg_sizes* out) {
 static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uint16_t* V,
                const uint8_t* mask, const hg_packed* pk, hipStream_t stream) {
   int s = check_config(cfg, mask);
+  if (!s) s = check_grid(cfg);
   if (s) return s;
   if (!pk) return fail(HG_ERR_NULL, "packed buffer descriptor is NULL");
   hg_sizes z;
@@ -276,10 +287,7 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
   p.k = z.retain_count;
   p.out[0] = quantize ? nullptr : (uint16_t*)K;
   p.out[1] = quantize ? nullptr : (uint16_t*)V;
-  const uint64_t slices = (uint64_t)cfg->L * cfg->B * cfg->H;
-  const uint64_t blocks_k = slices * (uint64_t)p.tiles;
-  if (2 * blocks_k > 0x7FFFFFFFull)
-    return fail(HG_ERR_SHAPE, "grid of %llu workgroups too large", (unsigned long long)(2 * blocks_k));
+  const uint64_t blocks_k = (uint64_t)cfg->L * cfg->B * cfg->H * (uint64_t)p.tiles;
   p.blocks_k = (uint32_t)blocks_k;
   hipError_t e = quantize ? hg::launch_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), retain, stream)
                           : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, stream);
@@ -295,6 +303,7 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
 int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, const uint8_t* mask,
                      uint16_t* K_out, uint16_t* V_out, hipStream_t stream) {
   int s = check_config(cfg, mask);
+  if (!s) s = check_grid(cfg);
   if (s) return s;
   const uint64_t cache_bytes = (uint64_t)cfg->L * cfg->B * cfg->H * cfg->T * cfg->D * 2;
   const uint64_t need = cfg->img_len > 0 ? cache_bytes : 0;
@@ -328,10 +337,6 @@ int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
   p.cache[1] = V;
   p.out[0] = K_out;
   p.out[1] = V_out;
-  const uint64_t blocks_k = (uint64_t)cfg->L * cfg->B * cfg->H * (uint64_t)p.tiles;
-  if (2 * blocks_k > 0x7FFFFFFFull)
-    return fail(HG_ERR_SHAPE, "grid of %llu workgroups too large", (unsigned long long)(2 * blocks_k));
-  p.blocks_k = (uint32_t)blocks_k;
 
   // Token retention (a stream-ordered workspace holds the norms and the
   // selection).  Out of place, the one-pass kernel writes the key norms from

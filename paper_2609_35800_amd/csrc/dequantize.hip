@@ -149,6 +149,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
 template <int BASE, int D, int BITS>
 static hipError_t launch_d(const Params& p, Tensors which, hipStream_t stream) {
   constexpr int kTile = (kThreads / 64) * kDequantTokens<BASE, D>;
+  static_assert(kTile >= kMinBlockTokens, "the host's grid check assumes this tile at least");
   Params pd = p;
   pd.tiles = (p.n + kTile - 1) / kTile;
   const uint64_t per_tensor = (uint64_t)p.L * p.B * p.H * (uint64_t)pd.tiles;

@@ -233,6 +233,7 @@ constexpr size_t fake_lds() {
 template <int BASE, int D, int BITS>
 static hipError_t launch_f(const Params& p, Tensors which, bool norms, hipStream_t stream) {
   constexpr int kTile = (kThreads / 64) * kFakeTokens<BASE, D>;
+  static_assert(kTile >= kMinBlockTokens, "the host's grid check assumes this tile at least");
   Params pf = p;
   pf.tiles = (p.n + kTile - 1) / kTile;
   const uint64_t per_tensor = (uint64_t)p.L * p.B * p.H * (uint64_t)pf.tiles;

@@ -12,6 +12,7 @@ namespace hg {
 constexpr int kThreads = 256;        // 4 wavefronts of 64
 constexpr int kWaveTokens = 32;      // tokens per wavefront tile
 constexpr int kBlockTokens = 128;    // tokens per workgroup tile (4 x 32)
+constexpr int kMinBlockTokens = 64;  // smallest workgroup tile of any launch (dequantize, one-pass)
 // Register budget: at least this many wavefronts per SIMD, so enough 16-byte
 // loads are in flight per CU to cover HBM latency.
 constexpr int kMinWaves = 4;

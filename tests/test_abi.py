@@ -116,6 +116,22 @@ def test_invalid_config(kw, status):
     assert rc == status
 
 
+def test_grid_too_large_is_a_shape_error():
+    """A call whose tiled grid (K and V, workgroup tiles of 64 tokens, the
+    smallest any launch uses) would exceed 2^31 - 1 workgroups is rejected
+    from the configuration alone, before any device or pointer check."""
+    f = _cfg(L=1, H=1, D=64, B=1 << 20, T=(1 << 16) + 2, img_start=1, img_len=1 << 16)
+    cfg = hg.make_config(**f)  # 2 * 2^20 * 2^10 = 2^31 workgroups
+    mask = np.zeros(1, np.uint8)
+    lib = hg.library()
+    pk = hg.hg_packed()
+    m = mask.ctypes.data_as(C.c_void_p)
+    assert lib.hg_quantize(C.byref(cfg), 16, 32, m, C.byref(pk), None) == hg.HG_ERR_SHAPE
+    assert "too large" in hg.hg_last_error()
+    assert lib.hg_dequantize(C.byref(cfg), m, C.byref(pk), 16, 32, None) == hg.HG_ERR_SHAPE
+    assert lib.hg_fake_quantize(C.byref(cfg), 16, 32, m, 48, 64, None) == hg.HG_ERR_SHAPE
+
+
 def test_mask_values_and_nulls():
     cfg = hg.make_config(**_cfg())
     lib = hg.library()
