@@ -44,24 +44,48 @@ __device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out,
   constexpr int LEVELS = (1 << BITS) - 1;
   const int j = lane % G;
   const int q = lane / G;
+  // Head_dim 256: whole-row streaming loads moved into the quad layout through
+  // the stage, as in the quantize kernel.
+  constexpr bool kStaged = D == 256;
+  constexpr int LPR = D / 8;           // staged loads: lanes per token row,
+  constexpr int RPI = 64 / LPR;        // token rows per load instruction,
+  constexpr int IPP = TPP / RPI;       // load instructions per pass
 
 #pragma unroll
   for (int p0 = 0; p0 < PASSES; p0 += PB) {
     // Tokens past the span's end load the last token (never stored).
     u32x4 raw[PB][NV];
+    u32x4 whole[kStaged ? PB * IPP : 1];
+    if constexpr (kStaged) {
 #pragma unroll
-    for (int b = 0; b < PB; ++b) {
-      const int t = min(t_first + (p0 + b) * TPP + q, n - 1);
-      const u32x4* src = (const u32x4*)(rows + (size_t)t * D + j * E);
+      for (int i = 0; i < PB * IPP; ++i) {
+        const int t = min(t_first + p0 * TPP + i * RPI + lane / LPR, n - 1);
+        whole[i] = __builtin_nontemporal_load((const u32x4*)(rows + (size_t)t * D) + lane % LPR);
+      }
+    } else {
 #pragma unroll
-      for (int k = 0; k < NV; ++k) raw[b][k] = src[k];
+      for (int b = 0; b < PB; ++b) {
+        const int t = min(t_first + (p0 + b) * TPP + q, n - 1);
+        const u32x4* src = (const u32x4*)(rows + (size_t)t * D + j * E);
+#pragma unroll
+        for (int k = 0; k < NV; ++k) raw[b][k] = src[k];
+      }
     }
 
-    // Rotated keys unroll both passes: rolled, their per-pass register arrays
-    // went to scratch memory.  The plain path is faster rolled (measured).
-    constexpr int kUnrolledPasses = ROTATE ? PB : 1;
+    // Rotated keys (and the staged loads) unroll both passes: rolled, their
+    // per-pass register arrays went to scratch memory.  The plain path is
+    // faster rolled (measured).
+    constexpr int kUnrolledPasses = ROTATE || kStaged ? PB : 1;
 #pragma unroll kUnrolledPasses
     for (int pass = 0; pass < PB; ++pass) {
+      if constexpr (kStaged) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+#pragma unroll
+        for (int i = 0; i < IPP; ++i) stage[stage_slot<D>(i * RPI + lane / LPR, lane % LPR)] = whole[pass * IPP + i];
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int k = 0; k < NV; ++k) raw[pass][k] = stage[stage_slot<D>(q, j * NV + k)];
+      }
       float x[E];
 #pragma unroll
       for (int k = 0; k < NV; ++k) {
