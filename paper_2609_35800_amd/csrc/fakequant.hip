@@ -167,7 +167,7 @@ __device__ __forceinline__ void fake_kivi_keys(const uint16_t* rows, uint16_t* o
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
       const int t = min(g_first + r + RPL * k, n - 1);  // past-the-end rows: excluded below
-      raw[k] = *(const u32x4*)(rows + (size_t)t * D + 8 * c8);
+      raw[k] = __builtin_nontemporal_load((const u32x4*)(rows + (size_t)t * D + 8 * c8));  // whole rows: streaming
     }
     float x[NL][8];
 #pragma unroll
