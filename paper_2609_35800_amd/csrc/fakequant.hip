@@ -228,9 +228,9 @@ void fake_quantize_kernel(const Params p) {
   float* norm = NORM ? p.norm + (size_t)sl.s * p.n : nullptr;  // used for K only
   if (sl.kept) {
     if (NORM && sl.X == 0)
-      copy_wave_rows<D, kTokens, NORM, false>(rows, out, norm, t_first, p.n, lane);
+      copy_wave_rows<D, kTokens, NORM, false, true>(rows, out, norm, t_first, p.n, lane);
     else if (out != rows)
-      copy_wave_rows<D, kTokens>(rows, out, nullptr, t_first, p.n, lane);
+      copy_wave_rows<D, kTokens, false, true, true>(rows, out, nullptr, t_first, p.n, lane);
     return;
   }
   if (sl.X == 0 && p.kivi_whole) return;  // whole-sequence KIVI key ranges: kivi_seq.hip

@@ -474,12 +474,13 @@ __device__ __forceinline__ void store_nt(u32x4* dst, u32x4 v) {
 // Bit-exact copy of a wavefront's token rows [t_first, t_first + TOKENS),
 // clipped to n, from src to dst (rows of D BF16 at the same offsets): 16-byte
 // vectors, vector i of the tile on lane i % 64, all loads issued before the
-// streaming stores.  With NORM, every row's squared norm (row tree,
+// streaming stores; with NT_LOADS the loads stream too (the rows are read
+// once: the input cache; dequantize's side-store reads measured faster plain).  With NORM, every row's squared norm (row tree,
 // row_sqnorm) also goes to norm[t], by a streaming store if NORM_NT.
 // (Copying a head_dim-256 tile in two rounds of 8 vectors per lane lowers the
 // kernels' register counts from 88-90 to 64-70, but measured no faster for
 // quantize and 2 % slower for dequantize at the higher occupancy.)
-template <int D, int TOKENS, bool NORM = false, bool NORM_NT = true>
+template <int D, int TOKENS, bool NORM = false, bool NORM_NT = true, bool NT_LOADS = false>
 __device__ __forceinline__ void copy_wave_rows(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
                                                float* __restrict__ norm, int t_first, int n, int lane) {
   constexpr int VPT = D / 8;                // 16-byte vectors per row
@@ -489,7 +490,10 @@ __device__ __forceinline__ void copy_wave_rows(const uint16_t* __restrict__ src,
   u32x4* d = (u32x4*)(dst + (size_t)t_first * D);
   u32x4 v[kVec];
 #pragma unroll
-  for (int k = 0; k < kVec; ++k) v[k] = s[min(lane + 64 * k, nvec - 1)];
+  for (int k = 0; k < kVec; ++k) {
+    const u32x4* a = s + min(lane + 64 * k, nvec - 1);
+    v[k] = NT_LOADS ? __builtin_nontemporal_load(a) : *a;
+  }
 #pragma unroll
   for (int k = 0; k < kVec; ++k) {
     const int i = lane + 64 * k;

@@ -240,10 +240,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t out_rsrc(void* base, uint32_t 
 // the whole wavefront, into 64 consecutive 16-byte LDS slots at `dst` (lane i
 // at dst + 16 i).
 __device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal);
 }
 __device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t r, lds_ptr dst, uint32_t off) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, off, 0, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, off, 0, 0, kNonTemporal);
 }
 
 // Store of one lane's 8 codes (BITS bytes) at byte `off` of the resource,

@@ -242,9 +242,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
   float* norm = NORM ? p.norm + (size_t)sl.s * p.n : nullptr;  // used for K only
   if (sl.kept) {
     if (NORM && sl.X == 0)
-      copy_wave_rows<D, kWaveTokens, NORM>(rows, p.side[0] + slab * p.n * D, norm, t_first, p.n, lane);
+      copy_wave_rows<D, kWaveTokens, NORM, true, true>(rows, p.side[0] + slab * p.n * D, norm, t_first, p.n, lane);
     else
-      copy_wave_rows<D, kWaveTokens>(rows, p.side[sl.X] + slab * p.n * D, nullptr, t_first, p.n, lane);
+      copy_wave_rows<D, kWaveTokens, false, true, true>(rows, p.side[sl.X] + slab * p.n * D, nullptr, t_first, p.n,
+                                                        lane);
     return;
   }
   if (sl.X == 0 && p.kivi_whole) return;  // whole-sequence KIVI key ranges: kivi_seq.hip
