@@ -287,9 +287,7 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
   p.k = z.retain_count;
   p.out[0] = quantize ? nullptr : (uint16_t*)K;
   p.out[1] = quantize ? nullptr : (uint16_t*)V;
-  const uint64_t blocks_k = (uint64_t)cfg->L * cfg->B * cfg->H * (uint64_t)p.tiles;
-  p.blocks_k = (uint32_t)blocks_k;
-  hipError_t e = quantize ? hg::launch_quantize(p, cfg->base, cfg->D, cfg->bits, (uint32_t)(2 * blocks_k), retain, stream)
+  hipError_t e = quantize ? hg::launch_quantize(p, cfg->base, cfg->D, cfg->bits, retain, stream)
                           : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, stream);
   if (e == hipSuccess && quantize && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, false, stream);
   if (e == hipSuccess && p.k > 0 && quantize) {

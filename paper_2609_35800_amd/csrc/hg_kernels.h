@@ -43,11 +43,12 @@ struct Route {
   uint32_t prefix[kMaskWords];  // 32-bit so the kernels read it with scalar loads
 };
 
-// One launch covers K (tensor 0) and V (tensor 1): blocks [0, blocks_k) take
-// K tiles, the rest V tiles.  Each block takes one (tensor, l, b, h) slice and
-// one of its `tiles` runs of consecutive image tokens: kBlockTokens as the
-// host sets them; the dequantize and one-pass launchers reset tiles and
-// blocks_k for kernels whose wavefronts take fewer tokens.
+// A tiled launch covers K (tensor 0) and V (tensor 1), or one of them: blocks
+// [0, blocks_k) take K tiles, the rest V tiles.  Each block takes one
+// (tensor, l, b, h) slice and one of its `tiles` runs of consecutive image
+// tokens.  The host sets tiles for kBlockTokens (the key-norm pass uses
+// them); each quantize, dequantize and one-pass launcher sets tiles and
+// blocks_k for its kernel's tile size.
 struct Params {
   const uint16_t* cache[2];  // quantize, fake quantize: K, V input; dequantize: K_out, V_out
   uint16_t* out[2];          // fake quantize: K_out, V_out (may equal the input)
@@ -75,10 +76,7 @@ enum class Tensors { kBoth, kKeys, kValues };
 
 // Dispatch over (base, D, bits); return hipSuccess or the launch error.
 // With `norms`, the quantize kernel also writes the squared key norms (AKVQ).
-hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t blocks,
-                           bool norms, hipStream_t stream);
-// (The dequantize and one-pass launches size their own grids: their tiles can
-// be shorter than kBlockTokens.)
+hipError_t launch_quantize(const Params& p, int base, int D, int bits, bool norms, hipStream_t stream);
 hipError_t launch_dequantize(const Params& p, int base, int D, int bits, hipStream_t stream);
 hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, bool norms, hipStream_t stream);
 // KIVI keys over the whole sequence: a persistent grid over the quantized key

@@ -275,38 +275,44 @@ constexpr size_t quantize_lds() {
   return occupancy_lds(kQuantizeWaves) - stage;
 }
 
+// The workgroup tiles of a launch: kBlockTokens tokens each.
 template <int BASE, int D, int BITS>
-static hipError_t launch_q(const Params& p, uint32_t blocks, bool norms, hipStream_t stream) {
+static hipError_t launch_q(const Params& p, Tensors which, bool norms, hipStream_t stream) {
+  Params pq = p;
+  pq.tiles = (p.n + kBlockTokens - 1) / kBlockTokens;
+  const uint64_t per_tensor = (uint64_t)p.L * p.B * p.H * (uint64_t)pq.tiles;
+  const uint64_t blocks = which == Tensors::kBoth ? 2 * per_tensor : per_tensor;
+  if (blocks > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
+  pq.blocks_k = which == Tensors::kValues ? 0u : (uint32_t)per_tensor;
   if constexpr (BASE == HG_BASE_AKVQ) {
     if (norms) {
-      hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, true>), dim3(blocks), dim3(kThreads),
-                         quantize_lds<D>(), stream, p);
+      hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, true>), dim3((uint32_t)blocks), dim3(kThreads),
+                         quantize_lds<D>(), stream, pq);
       return hipGetLastError();
     }
   }
   if (norms) return hipErrorInvalidValue;  // key norms belong to the AKVQ base
-  hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, false>), dim3(blocks), dim3(kThreads),
-                     quantize_lds<D>(), stream, p);
+  hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, false>), dim3((uint32_t)blocks), dim3(kThreads),
+                     quantize_lds<D>(), stream, pq);
   return hipGetLastError();
 }
 
 template <int BASE, int D>
-static hipError_t launch_q_bits(const Params& p, int bits, uint32_t blocks, bool norms, hipStream_t stream) {
+static hipError_t launch_q_bits(const Params& p, int bits, Tensors which, bool norms, hipStream_t stream) {
   switch (bits) {
-    case 2: return launch_q<BASE, D, 2>(p, blocks, norms, stream);
-    case 3: return launch_q<BASE, D, 3>(p, blocks, norms, stream);
-    case 4: return launch_q<BASE, D, 4>(p, blocks, norms, stream);
+    case 2: return launch_q<BASE, D, 2>(p, which, norms, stream);
+    case 3: return launch_q<BASE, D, 3>(p, which, norms, stream);
+    case 4: return launch_q<BASE, D, 4>(p, which, norms, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int BASE>
-static hipError_t launch_q_dim(const Params& p, int D, int bits, uint32_t blocks, bool norms,
-                               hipStream_t stream) {
+static hipError_t launch_q_dim(const Params& p, int D, int bits, Tensors which, bool norms, hipStream_t stream) {
   switch (D) {
-    case 64: return launch_q_bits<BASE, 64>(p, bits, blocks, norms, stream);
-    case 128: return launch_q_bits<BASE, 128>(p, bits, blocks, norms, stream);
-    case 256: return launch_q_bits<BASE, 256>(p, bits, blocks, norms, stream);
+    case 64: return launch_q_bits<BASE, 64>(p, bits, which, norms, stream);
+    case 128: return launch_q_bits<BASE, 128>(p, bits, which, norms, stream);
+    case 256: return launch_q_bits<BASE, 256>(p, bits, which, norms, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -318,18 +324,14 @@ static hipError_t launch_q_dim(const Params& p, int D, int bits, uint32_t blocks
 // path, which would leave the value tiles with fewer waves per SIMD.  With
 // KIVI keys over the whole sequence this launch only copies protected keys
 // and quantizes values, so all of it runs as the min-max instantiation.
-hipError_t launch_quantize(const Params& p, int base, int D, int bits, uint32_t blocks, bool norms,
-                           hipStream_t stream) {
+hipError_t launch_quantize(const Params& p, int base, int D, int bits, bool norms, hipStream_t stream) {
   if (base == HG_BASE_MINMAX || (base == HG_BASE_KIVI && p.kivi_whole))
-    return launch_q_dim<HG_BASE_MINMAX>(p, D, bits, blocks, norms, stream);
+    return launch_q_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kBoth, norms, stream);
   if (base != HG_BASE_KIVI && base != HG_BASE_AKVQ) return hipErrorInvalidValue;
-  const uint32_t blocks_v = blocks - p.blocks_k;
-  hipError_t e = base == HG_BASE_KIVI ? launch_q_dim<HG_BASE_KIVI>(p, D, bits, p.blocks_k, norms, stream)
-                                      : launch_q_dim<HG_BASE_AKVQ>(p, D, bits, p.blocks_k, norms, stream);
-  if (e != hipSuccess || blocks_v == 0) return e;
-  Params pv = p;
-  pv.blocks_k = 0;  // every block of this launch is a value tile
-  return launch_q_dim<HG_BASE_MINMAX>(pv, D, bits, blocks_v, false, stream);
+  hipError_t e = base == HG_BASE_KIVI ? launch_q_dim<HG_BASE_KIVI>(p, D, bits, Tensors::kKeys, norms, stream)
+                                      : launch_q_dim<HG_BASE_AKVQ>(p, D, bits, Tensors::kKeys, norms, stream);
+  if (e != hipSuccess) return e;
+  return launch_q_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kValues, false, stream);
 }
 
 }  // namespace hg
