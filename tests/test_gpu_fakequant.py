@@ -71,6 +71,17 @@ def test_ragged(base, img_len):
 
 
 @pytest.mark.parametrize("base", ["minmax", "kivi", "akvq"])
+@pytest.mark.parametrize("img_len", [1, 7, 9, 33])
+@pytest.mark.parametrize("inplace", [False, True])
+def test_ragged_head_dim_256(base, img_len, inplace):
+    """Head_dim 256: whole-row loads staged through LDS, spans ending inside a
+    pass; in place, each wavefront's loads precede its stores."""
+    w = small(base, D=256, img_len=img_len, img_start=3, text=2, L=1, B=2, H=2, n_protected=1)
+    K, V = synthkv.gen_kv(w)
+    check(w, K, V, synthkv.protect_mask(w), inplace=inplace)
+
+
+@pytest.mark.parametrize("base", ["minmax", "kivi", "akvq"])
 def test_special_values(base):
     w = small(base, bits=2, img_len=96, n_protected=0)
     K, V = synthkv.gen_kv(w)

@@ -65,6 +65,16 @@ def test_ragged_spans(base, img_len):
 
 
 @pytest.mark.parametrize("base", ["minmax", "kivi", "akvq"])
+@pytest.mark.parametrize("img_len", [1, 7, 8, 9, 31, 33, 41])
+def test_ragged_spans_head_dim_256(base, img_len):
+    """Head_dim 256 loads whole rows into an LDS stage 8 tokens (one pass) at
+    a time; spans ending inside a pass or a 32-token tile."""
+    w = small(base, D=256, img_len=img_len, img_start=3, text=2, L=1, B=2, H=2, n_protected=1)
+    K, V = synthkv.gen_kv(w)
+    _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), w.name)
+
+
+@pytest.mark.parametrize("base", ["minmax", "kivi", "akvq"])
 @pytest.mark.parametrize("which", ["none", "all"])
 @pytest.mark.parametrize("keys_only", [0, 1])
 def test_degenerate_masks(base, which, keys_only):
