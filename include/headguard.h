@@ -89,7 +89,10 @@ typedef enum { HG_BASE_MINMAX = 0, HG_BASE_KIVI = 1, HG_BASE_AKVQ = 2 } hg_base;
 enum {
   HG_OK = 0,
   HG_ERR_NULL = 1,      /* a required pointer is NULL                          */
-  HG_ERR_SHAPE = 2,     /* L, B, H, T not positive, or L*H > HG_MAX_HEADS      */
+  HG_ERR_SHAPE = 2,     /* L, B, H, T not positive, L*H > HG_MAX_HEADS,
+                           keys_only not 0 or 1, or (quantize, dequantize,
+                           one-pass) 2*L*B*H*ceil(img_len/64) > 2^31 - 1
+                           workgroups                                        */
   HG_ERR_SPAN = 3,      /* image span outside [0, T]                           */
   HG_ERR_BITS = 4,      /* bits not in {2, 3, 4}                               */
   HG_ERR_BASE = 5,      /* unknown base, kivi_group not 32 or 0, retain_permille
