@@ -459,12 +459,19 @@ __device__ __forceinline__ uint32_t load_piece8(const uint8_t* row, int c) {
 }
 
 // Slot of 16-byte chunk c of token t in a wavefront's LDS stage of D/8
-// chunks per token, XOR-swizzled so that both the row layout (a token row
-// across D/8 lanes) and the quad layout (a token across 4 or 8 lanes) access
-// the stage without heavy bank conflicts.
+// chunks per token, XOR-swizzled so that the row layout (a token row across
+// D/8 lanes) and the quad layout (a token across 4 or 8 lanes, 4 chunks per
+// lane) both read and write it without bank conflicts.  Measured on gfx950
+// with 16-byte accesses: a write conflicts when two of 8 consecutive lanes
+// hit equal slots modulo 8, a read when two of 16 consecutive lanes hit
+// equal slots modulo 16; the XOR terms below keep both apart for each head
+// dim (quad-layout writes took 8 (head_dim 128) and 24 (256) extra cycles
+// per instruction with a plain token XOR).
 template <int D>
 __device__ __forceinline__ constexpr int stage_slot(int t, int c) {
-  return t * (D / 8) + (c ^ (D == 64 ? ((t >> 1) & 1) : (t & 3)));
+  if constexpr (D == 64) return t * 8 + (c ^ ((t & 1) + ((t >> 1) & 1)));
+  else if constexpr (D == 128) return t * 16 + (c ^ ((((c >> 3) << 1) | (t & 1)) ^ (((t >> 1) & 1) << 1)));
+  else return t * 32 + (c ^ ((c >> 3) | ((t & 1) << 3)));
 }
 
 __device__ __forceinline__ void store_nt(u32x4* dst, u32x4 v) {
