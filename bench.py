@@ -2,14 +2,17 @@
 (every layer, batch row and KV head; K and V) through libheadguard on one
 MI355X.  Prints one JSON line.
 
-Default workload: the Qwen2.5-VL-7B-shaped cache (28 layers x 8 rows x 4 KV
-heads x 1360 tokens x head_dim 128, 1296 image tokens, 2-bit per-token
-min-max, 14 of 112 heads protected, K+V), inputs resident in HBM.
+Default workload: the LLaVA-NeXT-7B-shaped cache, the largest of the five
+single-GPU workloads (32 layers x 4 rows x 32 KV heads x 3008 tokens x
+head_dim 128, 2880 image tokens, KIVI-style 2-bit: keys per channel over
+groups of 32 image tokens, values per token; 128 of 1024 heads protected,
+keys only), inputs resident in HBM.
 
 Algorithmic bytes per call: every image row of K and V is read once
 (2 bytes per element) and the packed outputs (codes, metadata, BF16 side
 store) are written once; dequantize moves the same bytes in the other
-direction.  Text rows are never touched.
+direction.  Text rows are never written; they are read only where the
+method needs them, by KIVI-style keys with one range over the whole sequence.
 """
 from __future__ import annotations
 
@@ -42,7 +45,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="qwen2.5-vl-7b")
+    ap.add_argument("--workload", default="llava-next-7b")
     ap.add_argument("--bits", type=int, default=None, help="override the workload's bit width")
     ap.add_argument("--kivi-group", type=int, default=None,
                     help="override the KIVI key group (0: one range over the whole sequence)")
@@ -123,19 +126,34 @@ def traffic_from_profile(w, kernel: str = QUANT_KERNEL):
 
 def algorithmic_bytes(w, sizes) -> dict:
     """Bytes each call must move at least.  Quantize: the image rows of K and V
-    read once, every packed buffer written once; with token retention also the
-    key norms read back by the selection and the retained rows read again
-    (the selection needs every norm first).  Dequantize: the packed buffers
-    read, the image rows written; with retention the retained rows are
+    read once, every packed buffer written once; KIVI-style keys with one range
+    over the whole sequence (kivi_group 0) also read the text rows of every
+    quantized key slice, whose values enter the range; with token retention
+    also the key norms read back by the selection and the retained rows read
+    again (the selection needs every norm first).  Dequantize: the packed
+    buffers read, the image rows written; with retention the retained rows are
     written over the reconstruction."""
     img_elems = w.L * w.B * w.H * w.img_len * w.D
     read = 2 * img_elems * 2  # K and V image rows, BF16
+    if w.base == "kivi" and w.kivi_group == 0 and w.img_len > 0:
+        read += sizes["n_unprot_k"] * w.B * (w.T - w.img_len) * w.D * 2
     write = sum(sizes[n] for n in ("codes_k", "meta_k", "side_k", "codes_v", "meta_v", "side_v"))
     rows = sizes.get("ret_k", 0) + sizes.get("ret_v", 0)
     quant_extra = 2 * sizes.get("norm_k", 0) + sizes.get("ret_idx", 0) + 2 * rows
     dequant_extra = sizes.get("ret_idx", 0) + 2 * rows
-    return {"quant": read + write + quant_extra, "dequant": read + write + dequant_extra,
+    text = read - 2 * img_elems * 2  # text rows the range reads (quantize only)
+    return {"quant": read + write + quant_extra, "dequant": read - text + write + dequant_extra,
             "read": read, "write": write}
+
+
+def fake_quantize_bytes(w, sizes) -> int:
+    """Bytes the one-pass call must move: every image row of K and V read once
+    and written once, plus the text rows of quantized key slices that
+    KIVI-style keys over the whole sequence read for the range (retention
+    extras not counted)."""
+    ab = algorithmic_bytes(w, sizes)
+    img = 2 * w.L * w.B * w.H * w.img_len * w.D * 2
+    return img + ab["read"]
 
 
 def cpu_model() -> str:
@@ -191,6 +209,29 @@ def cpu_baseline(w, K, V, mask, budget_s: float, threads: int = 0):
             "image_tokens_per_s": round(w.B * w.img_len * nl / w.L / per_pass, 1)}
 
 
+def host_call_us(hg, cfg, K, V, mask, packed, stream, calls: int = 50) -> float:
+    """Host time of one hg_quantize call: argument and pointer checks, mask
+    routing and the kernel launches, through ctypes with the arguments
+    prepared once; median over `calls` calls (their GPU work is drained
+    afterwards)."""
+    import ctypes as C
+    import torch
+    lib = hg.library()
+    m = np.ascontiguousarray(mask, dtype=np.uint8)
+    pk = hg.hg_packed(**{n: (t.data_ptr() if t.numel() else None) for n, t in packed.items()})
+    args = (C.byref(cfg), K.data_ptr(), V.data_ptr(), m.ctypes.data_as(C.c_void_p), C.byref(pk),
+            stream.cuda_stream)
+    ts = []
+    for _ in range(calls):
+        t0 = time.perf_counter_ns()
+        rc = lib.hg_quantize(*args)
+        ts.append(time.perf_counter_ns() - t0)
+        if rc:
+            raise RuntimeError(hg.hg_last_error())
+    torch.cuda.synchronize()
+    return float(np.median(ts)) / 1e3
+
+
 def device_copy_gbps(stream) -> float:
     """A plain device-to-device copy of 1 GiB on the same stream: the practical
     bandwidth the kernels are compared with besides the vendor peak (its
@@ -213,24 +254,26 @@ def device_copy_gbps(stream) -> float:
 
 def bench_fakequant(args, hg, w, cfg, mask, K, V):
     """One-pass simulated quantization, out of place: every image row of K and
-    V is read once and written once (protected rows copied)."""
+    V is read once and written once (protected rows copied); see
+    fake_quantize_bytes."""
     import torch
     Ko, Vo = torch.empty_like(K), torch.empty_like(V)
+    ws = hg.alloc_fake_workspace(cfg, mask)
     stream = torch.cuda.current_stream()
     for _ in range(args.warmup):
-        hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo, stream=stream)
+        hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo, ws, stream=stream)
     torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     t0 = time.perf_counter()
     for e0, e1 in ev:
         e0.record(stream)
-        hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo, stream=stream)
+        hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo, ws, stream=stream)
         e1.record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
-    nbytes = 2 * (2 * w.L * w.B * w.H * w.img_len * w.D * 2)
+    nbytes = fake_quantize_bytes(w, hg.hg_packed_sizes(cfg, mask))
     gbps = nbytes / (ms * 1e-3) / 1e9
     copy_gbps = device_copy_gbps(stream)
     print(json.dumps({
@@ -325,6 +368,7 @@ def main():
     d_gbps = ab["dequant"] / (d_avg * 1e-3) / 1e9 if not args.quant_only else None
     traffic = traffic_from_profile(w)
 
+    host_us = host_call_us(hg, cfg, K, V, mask, packed, stream)
     copy_gbps = device_copy_gbps(stream)
 
     out = {
@@ -350,6 +394,7 @@ def main():
         "device_copy_GBps": round(copy_gbps, 1),
         "quantize_pct_of_device_copy": round(100 * q_gbps / copy_gbps, 1),
         "image_tokens_per_s": round(w.B * w.img_len * args.steps / elapsed, 1),
+        "host_us_per_quantize_call": round(host_us, 2),
         "quantize": {"ms": round(q_avg, 4), "median_ms": round(float(np.median(q_ms)), 4),
                      "min_ms": round(float(np.min(q_ms)), 4), "GBps": round(q_gbps, 1),
                      "bytes": ab["quant"], "image_tokens_per_s": round(w.B * w.img_len / (q_avg * 1e-3), 1),

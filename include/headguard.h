@@ -58,14 +58,18 @@
  *   ret_idx   int32 [L][B][H][k]     retained tokens (0-based in the span), ascending
  *   ret_X     BF16 [slot][B][k][D]   their rows, for the quantized slots of X
  *
- * Ownership and synchronisation: the caller allocates every buffer.  Device
- * buffers are device memory of the current HIP device; the mask is host
- * memory read during the call only.  The library allocates nothing (except
- * hg_fake_quantize's stream-ordered workspace with token retention), keeps no
- * state between calls and never synchronises: HG_OK means the work is
- * enqueued on `stream`; device faults surface at the caller's next
- * synchronisation.  Every argument check runs before any launch, so on error
- * no output is touched.  Calls are thread-safe; the error detail is per thread.
+ * Ownership and synchronisation: the caller allocates every buffer, the
+ * one-pass call's workspace included.  Device buffers are device memory of
+ * the current HIP device; the mask is host memory read during the call only.
+ * The library allocates no memory, keeps no state between calls and never
+ * synchronises: HG_OK means the work is enqueued on `stream`; device faults
+ * surface at the caller's next synchronisation.  The calls only launch
+ * kernels on `stream`, so they can be captured in a HIP graph.  Every
+ * argument check runs before any launch, so on an argument error no output is
+ * touched.  A launch error (HG_ERR_HIP) at the call's first kernel leaves
+ * every output untouched too; at a later kernel of the same call, the
+ * kernels before it are enqueued and may write their outputs.  Calls are
+ * thread-safe; the error detail is per thread.
  *
  * Every buffer a call writes must be disjoint from every other buffer of the
  * call (HG_ERR_POINTER, checked on the host from the pointers and the sizes
@@ -90,15 +94,17 @@ enum {
   HG_OK = 0,
   HG_ERR_NULL = 1,      /* a required pointer is NULL                          */
   HG_ERR_SHAPE = 2,     /* L, B, H, T not positive, L*H > HG_MAX_HEADS,
-                           keys_only not 0 or 1, or (quantize, dequantize,
+                           keys_only not 0 or 1, (quantize, dequantize,
                            one-pass) 2*L*B*H*ceil(img_len/64) > 2^31 - 1
-                           workgroups                                        */
+                           workgroups, a workspace too small, or a head
+                           budget fraction out of range                      */
   HG_ERR_SPAN = 3,      /* image span outside [0, T]                           */
   HG_ERR_BITS = 4,      /* bits not in {2, 3, 4}                               */
   HG_ERR_BASE = 5,      /* unknown base, kivi_group not 32 or 0, retain_permille
                            outside [0, 1000] or set with a base other than AKVQ */
   HG_ERR_HEADDIM = 6,   /* D not in {64, 128, 256}                             */
-  HG_ERR_ALIGN = 7,     /* a device pointer is not 16-byte aligned             */
+  HG_ERR_ALIGN = 7,     /* a device pointer is not 16-byte aligned (the
+                           one-pass workspace: 256-byte)                     */
   HG_ERR_MASK = 8,      /* a mask entry is neither 0 nor 1                     */
   HG_ERR_NO_DEVICE = 9, /* no usable HIP device                                */
   HG_ERR_HIP = 10,      /* the HIP runtime reported an error (launch, pointer) */
@@ -123,6 +129,9 @@ typedef struct {
 typedef struct {
   uint64_t codes_k, meta_k, side_k, codes_v, meta_v, side_v; /* bytes          */
   uint64_t norm_k, ret_idx, ret_k, ret_v;  /* bytes; 0 without token retention    */
+  uint64_t fake_workspace;     /* bytes of hg_fake_quantize's workspace: the key
+                                  norms, token lists and (in place) saved rows
+                                  of token retention; 0 without retention       */
   int32_t n_protected;         /* heads with mask = 1                             */
   int32_t n_unprot_k, n_unprot_v; /* heads whose K / V are quantized              */
   int32_t retain_count;        /* k, retained tokens per (l, b, h)                */
@@ -173,15 +182,26 @@ int hg_select_heads(const double* g, const double* o, int32_t L, int32_t Hq, int
  * input, and no output may overlap the other tensor's input or the other
  * output (HG_ERR_POINTER, checked before any device work).  Kept
  * rows are copied (left alone in place); text rows are not written.  Device
- * pointers 16-byte aligned.  With token retention the call allocates a
- * stream-ordered workspace (hipMallocAsync / hipFreeAsync on `stream`) for
- * the key norms and the retained rows, about (4n + k(4 + 4D)) bytes per
- * (l, b, h); HG_ERR_HIP if it cannot.  Without retention the call only
- * launches kernels on `stream` (as hg_quantize and hg_dequantize do), so it can
- * be captured in a HIP graph. */
+ * pointers 16-byte aligned.
+ * `workspace`: device memory of `workspace_bytes` bytes, 256-byte aligned,
+ * owned by the caller, disjoint from K, V, K_out and V_out; with token
+ * retention it holds the key norms, the retained token lists and, in place,
+ * the saved retained rows, and must be at least hg_sizes.fake_workspace
+ * bytes (out of place it needs only the norms and lists, about 4n + 4k bytes
+ * per (l, b, h)); its contents on entry do not matter and are overwritten.
+ * Without retention it is not used and may be NULL.  Errors: HG_ERR_NULL if it
+ * is NULL but needed, HG_ERR_SHAPE if workspace_bytes is too small,
+ * HG_ERR_ALIGN, HG_ERR_POINTER (overlap, or not device memory). */
 int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
                      const uint8_t* protect_mask, uint16_t* K_out, uint16_t* V_out,
-                     hipStream_t stream);
+                     void* workspace, uint64_t workspace_bytes, hipStream_t stream);
+
+/* Head budget (§3, "Selecting physical KV heads"): K = round(n_kv_heads *
+ * num / den), halves rounded up, in exact integer arithmetic; the paper's
+ * main budget is 1/8 of the physical KV heads, its sweeps 1/16 to 1/4.
+ * Requires n_kv_heads >= 1, den >= 1 and 0 <= num <= den (else
+ * HG_ERR_SHAPE); writes K to *K_out.  Pure host computation. */
+int hg_head_budget(int32_t n_kv_heads, int32_t num, int32_t den, int32_t* K_out);
 
 /* Static name of a status code. */
 const char* hg_status_string(int status);

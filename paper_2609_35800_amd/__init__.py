@@ -38,7 +38,7 @@ class hg_config(C.Structure):
 
 
 class hg_sizes(C.Structure):
-    _fields_ = [(n, C.c_uint64) for n in BUFFERS] + [
+    _fields_ = [(n, C.c_uint64) for n in BUFFERS] + [("fake_workspace", C.c_uint64)] + [
         ("n_protected", C.c_int32), ("n_unprot_k", C.c_int32), ("n_unprot_v", C.c_int32),
         ("retain_count", C.c_int32)]
 
@@ -65,9 +65,10 @@ def _load():
     lib.hg_quantize.argtypes = [C.POINTER(hg_config), P, P, P, C.POINTER(hg_packed), P]
     lib.hg_dequantize.argtypes = [C.POINTER(hg_config), P, C.POINTER(hg_packed), P, P, P]
     lib.hg_select_heads.argtypes = [P, P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, P]
-    lib.hg_fake_quantize.argtypes = [C.POINTER(hg_config), P, P, P, P, P, P]
+    lib.hg_fake_quantize.argtypes = [C.POINTER(hg_config), P, P, P, P, P, P, C.c_uint64, P]
+    lib.hg_head_budget.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_int32)]
     for f in ("hg_packed_sizes", "hg_quantize", "hg_dequantize", "hg_select_heads",
-              "hg_fake_quantize"):
+              "hg_fake_quantize", "hg_head_budget"):
         getattr(lib, f).restype = C.c_int
     lib.hg_status_string.argtypes = [C.c_int]
     lib.hg_status_string.restype = C.c_char_p
@@ -158,12 +159,17 @@ def hg_dequantize(cfg: hg_config, protect_mask, packed: Dict[str, torch.Tensor],
 
 
 def hg_fake_quantize(cfg: hg_config, K: torch.Tensor, V: torch.Tensor, protect_mask,
-                     K_out: torch.Tensor, V_out: torch.Tensor, stream=None) -> None:
+                     K_out: torch.Tensor, V_out: torch.Tensor, workspace: Optional[torch.Tensor] = None,
+                     stream=None) -> None:
     """Enqueue the one-pass quantize-and-reconstruct of the image rows of K, V
-    into K_out, V_out (which may be K, V themselves)."""
+    into K_out, V_out (which may be K, V themselves).  `workspace`: a device
+    buffer of at least hg_packed_sizes(...)["fake_workspace"] bytes, needed
+    with token retention (see alloc_fake_workspace)."""
     m = _mask_arg(protect_mask)
+    ws = _ptr(workspace)
+    nbytes = workspace.numel() * workspace.element_size() if ws is not None else 0
     _check(_lib.hg_fake_quantize(C.byref(cfg), _ptr(K), _ptr(V), m.ctypes.data_as(C.c_void_p),
-                                 _ptr(K_out), _ptr(V_out), _stream(stream)))
+                                 _ptr(K_out), _ptr(V_out), ws, nbytes, _stream(stream)))
 
 
 # ------------------------------------------------------------ allocation helper
@@ -172,6 +178,12 @@ def alloc_packed(cfg: hg_config, protect_mask, device="cuda") -> Dict[str, torch
     """Device buffers of the sizes hg_packed_sizes reports (uint8 tensors)."""
     sz = hg_packed_sizes(cfg, protect_mask)
     return {n: torch.empty(sz[n], dtype=torch.uint8, device=device) for n in BUFFERS}
+
+
+def alloc_fake_workspace(cfg: hg_config, protect_mask, device="cuda") -> Optional[torch.Tensor]:
+    """The one-pass call's workspace (uint8 tensor), or None when it needs none."""
+    n = hg_packed_sizes(cfg, protect_mask)["fake_workspace"]
+    return torch.empty(n, dtype=torch.uint8, device=device) if n else None
 
 
 # ------------------------------------------------------------ head selection
@@ -189,6 +201,8 @@ def hg_select_heads(g, o, Hkv: int, K: int) -> np.ndarray:
     return mask
 
 
-def head_budget(n_kv: int, fraction: float = 1.0 / 8.0) -> int:
-    """K = round(n_kv * fraction), halves rounded up (the paper's budget rule)."""
-    return int(np.floor(n_kv * fraction + 0.5))
+def head_budget(n_kv: int, num: int = 1, den: int = 8) -> int:
+    """hg_head_budget: K = round(n_kv * num / den), halves rounded up."""
+    out = C.c_int32()
+    _check(_lib.hg_head_budget(int(n_kv), int(num), int(den), C.byref(out)))
+    return out.value

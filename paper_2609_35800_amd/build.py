@@ -18,7 +18,7 @@ SOURCES = ["api.hip", "quantize.hip", "dequantize.hip", "fakequant.hip", "kivi_s
 ARCH = os.environ.get("HG_OFFLOAD_ARCH", "gfx950")
 
 FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-ffp-contract=off", "-fno-fast-math", "-fno-gpu-flush-denormals-to-zero",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-result",
@@ -32,11 +32,29 @@ HOST_ASAN = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-fram
 
 
 def build(verbose: bool = False, out: str = LIB, host_asan: bool = False) -> str:
-    """Compile the library (always) and return its path."""
+    """Compile the library (always) and return its path.  Each source is
+    compiled to an object of its own, in parallel, then the objects are
+    linked into the shared library."""
+    from concurrent.futures import ThreadPoolExecutor
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    tag = "asan" if host_asan else "lib"
+    objdir = os.path.join(ROOT, "_build", tag)
+    os.makedirs(objdir, exist_ok=True)
+    extra = HOST_ASAN if host_asan else []
+
+    def compile_one(src):
+        obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
+        cmd = [hipcc, *FLAGS, *extra, "-c", "-o", obj, os.path.join(CSRC, src)]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.check_call(cmd)
+        return obj
+
+    jobs = max(1, min(len(SOURCES), os.cpu_count() or 1, 8))
+    with ThreadPoolExecutor(jobs) as ex:
+        objs = list(ex.map(compile_one, SOURCES))
     tmp = out + ".tmp"
-    cmd = [hipcc, *FLAGS, *(HOST_ASAN if host_asan else []), "-o", tmp] + \
-          [os.path.join(CSRC, s) for s in SOURCES]
+    cmd = [hipcc, *FLAGS, *extra, "-shared", "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)

@@ -4,6 +4,7 @@
 
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <string>
@@ -144,6 +145,44 @@ int check_grid(const hg_config* c) {
   return HG_OK;
 }
 
+// Launch steps of one call.  Test hook: with HG_FAIL_LAUNCH=i in the
+// environment, step i (0-based) of every call reports hipErrorLaunchFailure
+// without enqueuing anything, so the mapping of a launch error to HG_ERR_HIP
+// can be exercised on a working device.  Step 0 failing leaves every output
+// untouched; a later step failing leaves the earlier steps enqueued.
+struct LaunchSteps {
+  int fail_at = -1;
+  int next = 0;
+  LaunchSteps() {
+    const char* s = getenv("HG_FAIL_LAUNCH");
+    if (s && *s) fail_at = atoi(s);
+  }
+  template <class F>
+  hipError_t operator()(F&& launch) {
+    if (next++ == fail_at) return hipErrorLaunchFailure;
+    return launch();
+  }
+};
+
+// Workspace of the one-pass call with token retention, 256-byte aligned
+// parts: the key norms, the retained token lists, then (in place only) the
+// saved retained rows of K and V.
+struct FakeWorkspace {
+  uint64_t o_idx, o_k, o_v;
+  uint64_t out_of_place, in_place;  // bytes each form needs
+};
+
+FakeWorkspace fake_workspace(const hg_sizes& z) {
+  auto up = [](uint64_t b) { return (b + 255) & ~(uint64_t)255; };
+  FakeWorkspace w;
+  w.o_idx = up(z.norm_k);
+  w.o_k = w.o_idx + up(z.ret_idx);
+  w.o_v = w.o_k + up(z.ret_k);
+  w.out_of_place = z.retain_count > 0 ? w.o_k : 0;
+  w.in_place = z.retain_count > 0 ? w.o_v + up(z.ret_v) : 0;
+  return w;
+}
+
 void fill_params(hg::Params& p, const hg_config* c, const uint8_t* mask) {
   memset(&p, 0, sizeof p);
   p.L = c->L;
@@ -223,6 +262,7 @@ int hg_packed_sizes(const hg_config* cfg, const uint8_t* mask, hg_sizes* out) {
   out->ret_idx = LHB * k.k * 4;
   out->ret_k = (uint64_t)k.uk * B * k.k * D * 2;
   out->ret_v = (uint64_t)k.uv * B * k.k * D * 2;
+  out->fake_workspace = fake_workspace(*out).in_place;
   return ok();
 }
 
@@ -287,19 +327,32 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
   p.k = z.retain_count;
   p.out[0] = quantize ? nullptr : (uint16_t*)K;
   p.out[1] = quantize ? nullptr : (uint16_t*)V;
-  hipError_t e = quantize ? hg::launch_quantize(p, cfg->base, cfg->D, cfg->bits, retain, stream)
-                          : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, stream);
-  if (e == hipSuccess && quantize && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, false, stream);
-  if (e == hipSuccess && p.k > 0 && quantize) {
-    e = hg::launch_retain_select(p, cfg->D, hg::RowCopy::kGather, stream);
-  }
-  if (e == hipSuccess && p.k > 0 && !quantize) e = hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kScatter, stream);
+  LaunchSteps step;
+  hipError_t e = step([&] {
+    return quantize ? hg::launch_quantize(p, cfg->base, cfg->D, cfg->bits, retain, stream)
+                    : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, stream);
+  });
+  if (e == hipSuccess && quantize && p.kivi_whole)
+    e = step([&] { return hg::launch_kivi_seq(p, cfg->D, cfg->bits, false, stream); });
+  if (e == hipSuccess && p.k > 0 && quantize)
+    e = step([&] { return hg::launch_retain_select(p, cfg->D, hg::RowCopy::kGather, stream); });
+  if (e == hipSuccess && p.k > 0 && !quantize)
+    e = step([&] { return hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kScatter, stream); });
   if (e != hipSuccess) return fail(HG_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }
 
-int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, const uint8_t* mask,
-                     uint16_t* K_out, uint16_t* V_out, hipStream_t stream) {
+}  // extern "C"
+
+namespace hg {
+
+// The one-pass simulated quantization with its retention workspace `ws` of
+// `ws_bytes` bytes of device memory (unused without token retention).
+// `caller_ws`: the workspace is the caller's buffer, checked like the other
+// arguments; otherwise it is library memory known to be device memory.
+int fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, const uint8_t* mask,
+                  uint16_t* K_out, uint16_t* V_out, void* ws, uint64_t ws_bytes, bool caller_ws,
+                  hipStream_t stream) {
   int s = check_config(cfg, mask);
   if (!s) s = check_grid(cfg);
   if (s) return s;
@@ -308,25 +361,54 @@ int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
   if (need && (!K || !V || !K_out || !V_out)) return fail(HG_ERR_NULL, "K, V, K_out and V_out are required");
   // Each output is its own input or disjoint from it; no output may overlap
   // the other tensor's input or the other output.
-  auto overlap = [need](const void* x, const void* y) {
+  auto overlap = [](const void* x, uint64_t nx, const void* y, uint64_t ny) {
     const uintptr_t a = (uintptr_t)x, b = (uintptr_t)y;
-    return need && a < b + need && b < a + need;
+    return nx && ny && a < b + ny && b < a + nx;
   };
   for (int X = 0; X < 2; ++X) {
     const void* in = X ? (const void*)V : (const void*)K;
     const void* out = X ? (const void*)V_out : (const void*)K_out;
     const void* other_in = X ? (const void*)K : (const void*)V;
     const char* nm = X ? "V" : "K";
-    if (out != in && overlap(in, out))
+    if (out != in && overlap(in, need, out, need))
       return fail(HG_ERR_POINTER, "%s_out partially overlaps %s (must be the same buffer or disjoint)", nm, nm);
-    if (overlap(out, other_in))
+    if (overlap(out, need, other_in, need))
       return fail(HG_ERR_POINTER, "%s_out overlaps %s", nm, X ? "K" : "V");
   }
-  if (overlap(K_out, V_out)) return fail(HG_ERR_POINTER, "K_out and V_out overlap");
-  const Buf bufs[] = {{K, need, 16, "K"}, {V, need, 16, "V"}, {K_out, need, 16, "K_out"}, {V_out, need, 16, "V_out"}};
+  if (overlap(K_out, need, V_out, need)) return fail(HG_ERR_POINTER, "K_out and V_out overlap");
+
+  // Token retention: the workspace holds the norms and the selection.  Out of
+  // place, the one-pass kernel writes the key norms from the rows it reads,
+  // and the retained rows are then copied from the inputs to the outputs.  In
+  // place (either tensor), the outputs would overwrite the rows to keep: the
+  // norms come from a pass of their own, and the retained rows are saved to
+  // the workspace first and written back last.
+  hg_sizes z;
+  hg_packed_sizes(cfg, mask, &z);
+  const bool retain = need && z.retain_count > 0;
+  const bool fused = retain && K_out != K && V_out != V;
+  const FakeWorkspace lay = fake_workspace(z);
+  const uint64_t ws_need = !retain ? 0 : fused ? lay.out_of_place : lay.in_place;
+  if (ws_need && caller_ws && !ws)
+    return fail(HG_ERR_NULL, "workspace is NULL but the call needs %llu bytes", (unsigned long long)ws_need);
+  if (ws_need > ws_bytes)
+    return fail(HG_ERR_SHAPE, "the call needs a %llu-byte workspace (%llu bytes available)",
+                (unsigned long long)ws_need, (unsigned long long)ws_bytes);
+  if (ws_need) {
+    if (!aligned(ws, 256)) return fail(HG_ERR_ALIGN, "workspace is not 256-byte aligned");
+    const void* ins[4] = {K, V, K_out, V_out};
+    const char* names[4] = {"K", "V", "K_out", "V_out"};
+    for (int i = 0; i < 4; ++i)
+      if (overlap(ws, ws_need, ins[i], need)) return fail(HG_ERR_POINTER, "workspace overlaps %s", names[i]);
+  }
+  const Buf bufs[] = {{K, need, 16, "K"},
+                      {V, need, 16, "V"},
+                      {K_out, need, 16, "K_out"},
+                      {V_out, need, 16, "V_out"},
+                      {ws, caller_ws ? ws_need : 0, 256, "workspace"}};
   s = check_device();
   if (s) return s;
-  s = check_buffers(bufs, 4);
+  s = check_buffers(bufs, 5);
   if (s) return s;
   if (cfg->img_len == 0) return ok();
   hg::Params p;
@@ -335,53 +417,43 @@ int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
   p.cache[1] = V;
   p.out[0] = K_out;
   p.out[1] = V_out;
-
-  // Token retention (a stream-ordered workspace holds the norms and the
-  // selection).  Out of place, the one-pass kernel writes the key norms from
-  // the rows it reads, and the retained rows are then copied from the inputs
-  // to the outputs.  In place (either tensor), the outputs would overwrite the
-  // rows to keep: the norms come from a pass of their own, and the retained
-  // rows are saved to the workspace first and written back last.
-  hg_sizes z;
-  hg_packed_sizes(cfg, mask, &z);
-  const bool retain = z.retain_count > 0;
-  const bool fused = retain && K_out != K && V_out != V;
-  void* ws = nullptr;
-  hipError_t e = hipSuccess;
   if (retain) {
-    auto up = [](uint64_t b) { return (b + 255) & ~(uint64_t)255; };
-    const uint64_t o_idx = up(z.norm_k), o_k = o_idx + up(z.ret_idx), o_v = o_k + up(z.ret_k);
-    const uint64_t bytes = fused ? o_k : o_v + up(z.ret_v);
-    e = hipMallocAsync(&ws, bytes, stream);
-    if (e != hipSuccess) {
-      (void)hipGetLastError();
-      return fail(HG_ERR_HIP, "workspace of %llu bytes: %s", (unsigned long long)bytes, hipGetErrorString(e));
-    }
     char* w = (char*)ws;
     p.norm = (float*)w;
-    p.ret_idx = (int32_t*)(w + o_idx);
-    p.ret[0] = fused ? nullptr : (uint16_t*)(w + o_k);
-    p.ret[1] = fused ? nullptr : (uint16_t*)(w + o_v);
+    p.ret_idx = (int32_t*)(w + lay.o_idx);
+    p.ret[0] = fused ? nullptr : (uint16_t*)(w + lay.o_k);
+    p.ret[1] = fused ? nullptr : (uint16_t*)(w + lay.o_v);
     p.k = z.retain_count;
-    if (!fused) {
-      e = hg::launch_key_norms(p, cfg->D, stream);
-      if (e == hipSuccess) e = hg::launch_retain_select(p, cfg->D, hg::RowCopy::kGather, stream);
-    }
+  }
+  LaunchSteps step;
+  hipError_t e = hipSuccess;
+  if (retain && !fused) {
+    e = step([&] { return hg::launch_key_norms(p, cfg->D, stream); });
+    if (e == hipSuccess)
+      e = step([&] { return hg::launch_retain_select(p, cfg->D, hg::RowCopy::kGather, stream); });
   }
   if (e == hipSuccess)
-    e = hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, fused, stream);
-  if (e == hipSuccess && p.kivi_whole) e = hg::launch_kivi_seq(p, cfg->D, cfg->bits, true, stream);
+    e = step([&] { return hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, fused, stream); });
+  if (e == hipSuccess && p.kivi_whole)
+    e = step([&] { return hg::launch_kivi_seq(p, cfg->D, cfg->bits, true, stream); });
   if (e == hipSuccess && fused) {
-    e = hg::launch_retain_select(p, cfg->D, hg::RowCopy::kCacheToOut, stream);
+    e = step([&] { return hg::launch_retain_select(p, cfg->D, hg::RowCopy::kCacheToOut, stream); });
   } else if (e == hipSuccess && retain) {
-    e = hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kScatter, stream);
-  }
-  if (ws) {
-    const hipError_t f = hipFreeAsync(ws, stream);
-    if (e == hipSuccess) e = f;
+    e = step([&] { return hg::launch_retain_rows(p, cfg->D, hg::RowCopy::kScatter, stream); });
   }
   if (e != hipSuccess) return fail(HG_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+}  // namespace hg
+
+extern "C" {
+
+int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, const uint8_t* mask,
+                     uint16_t* K_out, uint16_t* V_out, void* workspace, uint64_t workspace_bytes,
+                     hipStream_t stream) {
+  return hg::fake_quantize(cfg, K, V, mask, K_out, V_out, workspace, workspace ? workspace_bytes : 0, true,
+                           stream);
 }
 
 int hg_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, const uint8_t* mask,

@@ -217,6 +217,9 @@ __global__ __launch_bounds__(kThreads) void retain_select_kernel(const Params p)
     done = shift == 0 || pick[1] == pick[2];
   }
   const uint32_t need = want;  // keys matching prefix that are retained (lowest indices)
+  // Every wavefront has read the step-0 bounds from wsum before step 2 reuses
+  // it; when all keys are equal the loop above ran no barrier.
+  __syncthreads();
 
   // 2. Retained tokens in ascending order: every key above prefix under pmask,
   //    then the first `need` matching it.  Each thread owns a contiguous run of

@@ -1,8 +1,8 @@
 // Head selection (HeadGuard §3 "Selecting physical KV heads", Eq. 2), host
 // side of libheadguard: average the per-query-head image and output
 // sensitivity scores within each physical KV group, standardize each over all
-// KV heads, and mark the K heads with the largest sum.  Declared in
-// include/headguard.h.
+// KV heads, and mark the K heads with the largest sum; and the head budget
+// K = round(N_KV * f) of §3.  Declared in include/headguard.h.
 
 #include <math.h>
 #include <stdint.h>
@@ -65,5 +65,15 @@ extern "C" int hg_select_heads(const double* g, const double* o, int32_t L, int3
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return s[a] > s[b]; });
   memset(mask, 0, (size_t)n);
   for (int k = 0; k < std::min(K, n); ++k) mask[order[k]] = 1;
+  return hg::set_error(HG_OK, "");
+}
+
+extern "C" int hg_head_budget(int32_t n_kv_heads, int32_t num, int32_t den, int32_t* K_out) {
+  if (!K_out) return hg::set_error(HG_ERR_NULL, "K_out must not be NULL");
+  if (n_kv_heads < 1 || den < 1 || num < 0 || num > den)
+    return hg::set_error(HG_ERR_SHAPE, "need n_kv_heads >= 1, den >= 1 and 0 <= num <= den");
+  // round(n * num / den), halves up: floor((2 n num + den) / (2 den)), exact in 64 bits
+  const int64_t q = (2 * (int64_t)n_kv_heads * num + den) / (2 * (int64_t)den);
+  *K_out = (int32_t)q;
   return hg::set_error(HG_OK, "");
 }

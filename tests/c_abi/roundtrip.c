@@ -108,7 +108,7 @@ int main(void) {
   CHECK_HIP(hipMemcpy(codes1, pk.codes_k, z.codes_k, hipMemcpyDeviceToHost));
   CHECK_HG(hg_quantize(&cfg, K, V, mask, &pk, stream));
   CHECK_HG(hg_dequantize(&cfg, mask, &pk, Ko, Vo, stream));
-  CHECK_HG(hg_fake_quantize(&cfg, K, V, mask, Kf, Vf, stream));
+  CHECK_HG(hg_fake_quantize(&cfg, K, V, mask, Kf, Vf, NULL, 0, stream));
   CHECK_HIP(hipStreamSynchronize(stream));
   CHECK_HIP(hipMemcpy(codes2, pk.codes_k, z.codes_k, hipMemcpyDeviceToHost));
   CHECK_HIP(hipMemcpy(hKo, Ko, bytes, hipMemcpyDeviceToHost));

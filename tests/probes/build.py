@@ -15,7 +15,7 @@ def build() -> str:
     spec.loader.exec_module(hg_build)  # not the package: its __init__ loads the library
     FLAGS = hg_build.FLAGS
     tmp = LIB + ".tmp"
-    subprocess.check_call([os.environ.get("HIPCC", "/opt/rocm/bin/hipcc"), *FLAGS, "-o", tmp,
+    subprocess.check_call([os.environ.get("HIPCC", "/opt/rocm/bin/hipcc"), *FLAGS, "-shared", "-o", tmp,
                            os.path.join(HERE, "hg_probes.hip")])
     os.replace(tmp, LIB)
     return LIB

@@ -72,7 +72,12 @@ def test_sizes_match_oracle(seed):
     mask = (rng.random(L * H) < 0.2).astype(np.uint8)
     got = hg.hg_packed_sizes(hg.make_config(**f), mask)
     want = oracle.sizes(oracle.make_config(**f), mask)
-    assert got == want
+    assert {n: got[n] for n in want} == want
+    # the one-pass call's workspace: norms, lists and both tensors' saved rows,
+    # each part rounded up to 256 bytes; none without retention
+    up = lambda b: -(-b // 256) * 256  # noqa: E731
+    parts = ("norm_k", "ret_idx", "ret_k", "ret_v")
+    assert got["fake_workspace"] == (sum(up(want[n]) for n in parts) if want["retain_count"] else 0)
 
 
 def test_storage_model_bits_per_element():
@@ -129,7 +134,7 @@ def test_grid_too_large_is_a_shape_error():
     assert lib.hg_quantize(C.byref(cfg), 16, 32, m, C.byref(pk), None) == hg.HG_ERR_SHAPE
     assert "too large" in hg.hg_last_error()
     assert lib.hg_dequantize(C.byref(cfg), m, C.byref(pk), 16, 32, None) == hg.HG_ERR_SHAPE
-    assert lib.hg_fake_quantize(C.byref(cfg), 16, 32, m, 48, 64, None) == hg.HG_ERR_SHAPE
+    assert lib.hg_fake_quantize(C.byref(cfg), 16, 32, m, 48, 64, None, 0, None) == hg.HG_ERR_SHAPE
 
 
 def test_mask_values_and_nulls():
@@ -164,8 +169,38 @@ def test_fake_quantize_overlaps_are_refused_before_device_work():
              (K, V, Ko, K + 16),         # V_out overlaps K
              (K, V, Ko, Ko + 16)]        # the outputs overlap
     for k, v, ko, vo in cases:
-        assert lib.hg_fake_quantize(C.byref(cfg), k, v, mask, ko, vo, None) == hg.HG_ERR_POINTER
+        assert lib.hg_fake_quantize(C.byref(cfg), k, v, mask, ko, vo, None, 0, None) == hg.HG_ERR_POINTER
         assert "overlap" in hg.hg_last_error() or "is V" in hg.hg_last_error()
+
+
+def test_fake_quantize_workspace_is_checked_before_device_work():
+    """With token retention the one-pass call needs the caller's workspace:
+    NULL, too small, misaligned or overlapping an input or output is refused
+    before any device work (so these run without a GPU)."""
+    f = _cfg(base=2, retain_permille=20, img_len=30)
+    cfg = hg.make_config(**f)
+    mask = np.zeros(8, np.uint8)
+    sz = hg.hg_packed_sizes(cfg, mask)
+    assert sz["retain_count"] == 1 and sz["fake_workspace"] > 0
+    need_in_place = sz["fake_workspace"]
+    need_out = -(-sz["norm_k"] // 256) * 256 + -(-sz["ret_idx"] // 256) * 256
+    m = mask.ctypes.data_as(C.c_void_p)
+    lib = hg.library()
+    K, V, Ko, Vo, W = (i << 32 for i in range(1, 6))
+    cases = [  # (K_out, V_out, workspace, bytes) -> status, detail
+        ((Ko, Vo, None, 0), hg.HG_ERR_NULL, "workspace"),
+        ((Ko, Vo, W, need_out - 1), hg.HG_ERR_SHAPE, "workspace"),
+        ((K, V, W, need_in_place - 1), hg.HG_ERR_SHAPE, "workspace"),  # in place needs the rows too
+        ((Ko, Vo, W + 16, need_out), hg.HG_ERR_ALIGN, "256"),
+        ((Ko, Vo, K + 256, 1 << 30), hg.HG_ERR_POINTER, "overlaps K"),
+        ((Ko, Vo, Vo - 256, need_out), hg.HG_ERR_POINTER, "overlaps V_out"),
+    ]
+    for (ko, vo, ws, nb), status, detail in cases:
+        assert lib.hg_fake_quantize(C.byref(cfg), K, V, m, ko, vo, ws, nb, None) == status, (ws, nb)
+        assert detail in hg.hg_last_error()
+    # without retention no workspace is needed
+    cfg0 = hg.make_config(**_cfg(base=2))
+    assert hg.hg_packed_sizes(cfg0, mask)["fake_workspace"] == 0
 
 
 def test_overlapping_outputs_are_refused_before_device_work():

@@ -1,6 +1,6 @@
 """The entry points inside a captured HIP graph: hg_quantize followed by
-hg_dequantize (and, separately, the one-pass hg_fake_quantize without token
-retention) is captured once (the calls only launch kernels on the given
+hg_dequantize (and, separately, the one-pass hg_fake_quantize, out of place
+and in place) is captured once (the calls only launch kernels on the given
 stream: no allocation, no synchronisation, no memset) and replayed several
 times, with the outputs cleared by eager work in between; every replay must
 write exactly the bytes of the eager calls.  Covers the per-token, KIVI
@@ -62,23 +62,41 @@ def test_capture_and_replay(w):
     del graph
 
 
-@pytest.mark.parametrize("w", CASES[:3], ids=lambda w: w.name)
-def test_capture_one_pass(w):
-    """hg_fake_quantize without token retention only launches kernels too."""
+@pytest.mark.parametrize("inplace", [False, True])
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def test_capture_one_pass(w, inplace):
+    """hg_fake_quantize only launches kernels too, with token retention
+    included (its workspace is the caller's buffer): out of place, and in
+    place with the inputs restored by eager work before every replay."""
     import paper_2609_35800_amd as hg
     mask = synthkv.protect_mask(w)
     cfg = hg.make_config(**w.config_fields())
-    K, V = synthkv.gen_kv(w, device="cuda")
-    Ko, Vo = torch.zeros_like(K), torch.zeros_like(V)
-    hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo)
+    K0, V0 = synthkv.gen_kv(w, device="cuda")
+    K, V = K0.clone(), V0.clone()
+    Ko, Vo = (K, V) if inplace else (torch.zeros_like(K), torch.zeros_like(V))
+    ws = hg.alloc_fake_workspace(cfg, mask)
+    assert (ws is not None) == (w.retain_permille > 0)
+
+    def reset():
+        K.copy_(K0)
+        V.copy_(V0)
+        if not inplace:
+            Ko.fill_(0.0)
+            Vo.fill_(0.0)
+        if ws is not None:
+            ws.fill_(0xA5)  # the workspace's contents on entry do not matter
+
+    reset()
+    hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo, ws)
     torch.cuda.synchronize()
     want_k, want_v = Ko.clone(), Vo.clone()
+    reset()
+    torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
-        hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo)
+        hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo, ws)
     for _ in range(3):
-        Ko.fill_(0.0)
-        Vo.fill_(0.0)
+        reset()  # eager work between replays
         torch.cuda.synchronize()
         graph.replay()
         torch.cuda.synchronize()

@@ -2,7 +2,7 @@
 supplied sequence, text included (kivi_group = 0; §4 Quantization setup),
 against the oracle: codes, metadata, side store and reconstruction
 bit-exact for quantize / dequantize and for the one-pass simulated
-quantization; full-size sampled slices on the LLaVA-NeXT-7B-shaped cache.
+quantization; every slice of the full LLaVA-NeXT-7B-shaped cache.
 
 Slices of up to 3072 rows go through the resident kernel (each workgroup
 holds a 64-channel part of a slice on chip and refills its row slots with
@@ -13,8 +13,8 @@ import numpy as np
 import pytest
 import torch
 
-import oracle
 import synthkv
+import wholecache
 from hgtest import compare_full
 from test_gpu_fakequant import check as check_fake
 from test_gpu_parity import _assert_exact, small
@@ -48,29 +48,16 @@ def test_spans(img_len, img_start, text):
 
 
 def test_full_size_llava():
-    import paper_2609_35800_amd as hg
+    """The LLaVA-NeXT-7B-shaped cache with one key range per channel over the
+    whole sequence: every slice against the oracle."""
     w = synthkv.WORKLOADS["llava-next-7b"].with_(kivi_group=0)
-    mask = synthkv.protect_mask(w)
-    cfg = hg.make_config(**w.config_fields())
-    K, V = synthkv.gen_kv(w, device="cuda")
-    packed = hg.alloc_packed(cfg, mask)
-    hg.hg_quantize(cfg, K, V, mask, packed)
-    torch.cuda.synchronize()
-    ocfg = oracle.make_config(**w.config_fields())
-    row = w.D * w.bits // 8
-    codes = packed["codes_k"].view(-1, w.B, w.img_len, row)
-    meta = packed["meta_k"].view(torch.int32).view(-1, w.B, 1, w.D)
-    rng = np.random.default_rng(3)
-    checked = 0
-    while checked < 10:
-        l, b, h = int(rng.integers(w.L)), int(rng.integers(w.B)), int(rng.integers(w.H))
-        prot, slot = oracle.route(ocfg, mask, 0, l, h)
-        if prot:
-            continue
-        oc, om = oracle.quantize_slice_seq(ocfg, 0, synthkv.bf16_bits(K[l, b, h]))
-        assert np.array_equal(codes[slot, b].cpu().numpy(), oc)
-        assert np.array_equal(meta[slot, b].cpu().numpy().view(np.uint32), om)
-        checked += 1
+    wholecache.assert_whole(wholecache.quantize_dequantize(w), w)
+
+
+@pytest.mark.parametrize("inplace", [False, True])
+def test_full_size_llava_one_pass(inplace):
+    w = synthkv.WORKLOADS["llava-next-7b"].with_(kivi_group=0)
+    wholecache.assert_whole(wholecache.fake_quantize(w, inplace=inplace), w)
 
 
 # Enough (head, row) items that every workgroup stream of the resident kernel

@@ -8,15 +8,15 @@ patterns), the retained token lists, the retained rows, the packed codes and
 metadata, and the reconstruction with the retained rows written back.  Small
 shapes span several 256-token selection chunks with ragged tails; inputs with
 many equal norms exercise the tie rule; the one-pass simulated quantization is
-checked in place and out of place; the full InternVL3-8B-shaped cache at the
-paper's 2 % is checked on sampled slices and against the library's own
-quantize then dequantize."""
+checked in place and out of place; every slice of the full InternVL3-8B-shaped
+cache at the paper's 2 % is checked, for quantize then dequantize and for the
+one-pass form."""
 import numpy as np
 import pytest
 import torch
 
-import oracle
 import synthkv
+import wholecache
 from hgtest import compare_full
 from test_gpu_fakequant import check as check_fake
 from test_gpu_parity import _assert_exact, _special_values, small
@@ -85,6 +85,17 @@ def test_identical_keys():
     _assert_exact(rep, "identical")
 
 
+def test_identical_keys_many_workgroups_per_cu():
+    """All norms equal in every one of 2048 heads (several selection
+    workgroups per compute unit): no selection pass runs, and the scan's
+    shared totals must not overwrite the key bounds before every wavefront
+    has read them."""
+    w = retain_case(img_len=200, permille=100, n_protected=0, L=8, B=16, H=16, text=5, img_start=3)
+    K, V = synthkv.gen_kv(w)
+    K[:] = K[:, :, :, :1].clone()
+    _assert_exact(compare_full(w, K, V, np.zeros(w.L * w.H, np.uint8)), "identical-many")
+
+
 def test_special_values():
     """Large keys square to +inf (ties among infinities), subnormal and zero
     squares, signed zeros."""
@@ -140,7 +151,7 @@ def test_fake_quantize_one_tensor_in_place(k_in_place):
     fresh = lambda t: torch.full(t.shape, SENTINEL, dtype=torch.int16, device="cuda").view(torch.bfloat16)
     Ko = Kg if k_in_place else fresh(Kg)
     Vo = fresh(Vg) if k_in_place else Vg
-    hg.hg_fake_quantize(cfg, Kg, Vg, mask, Ko, Vo)
+    hg.hg_fake_quantize(cfg, Kg, Vg, mask, Ko, Vo, hg.alloc_fake_workspace(cfg, mask))
     torch.cuda.synchronize()
     Kb, Vb = synthkv.bf16_bits(K), synthkv.bf16_bits(V)
     oK, oV = oracle_roundtrip(w, Kb, Vb, mask, Kb if k_in_place else np.full_like(Kb, SENTINEL),
@@ -158,64 +169,17 @@ def test_fake_quantize_ties_in_place():
 # ---------------------------------------------------------------- full size
 
 def test_full_size_internvl_two_percent():
-    import paper_2609_35800_amd as hg
+    """The InternVL3-8B-shaped cache at the paper's 2 %: every slice's norms,
+    token list, retained rows, codes, metadata and reconstruction against the
+    oracle."""
     w = synthkv.WORKLOADS["internvl-8b"].with_(retain_permille=20)
-    mask = synthkv.protect_mask(w)
-    cfg = hg.make_config(**w.config_fields())
-    sizes = hg.hg_packed_sizes(cfg, mask)
-    k, s0, n, D = sizes["retain_count"], w.img_start, w.img_len, w.D
-    assert k == 67
-    K, V = synthkv.gen_kv(w, device="cuda")
-    packed = hg.alloc_packed(cfg, mask)
-    Ko = torch.full_like(K, 0)
-    Vo = torch.full_like(V, 0)
-    hg.hg_quantize(cfg, K, V, mask, packed)
-    hg.hg_dequantize(cfg, mask, packed, Ko, Vo)
-    torch.cuda.synchronize()
-    norms = packed["norm_k"].view(torch.float32).view(w.L, w.B, w.H, n)
-    idx = packed["ret_idx"].view(torch.int32).view(w.L, w.B, w.H, k)
-    retk = packed["ret_k"].view(torch.int16).view(-1, w.B, k, D)
-    retv = packed["ret_v"].view(torch.int16).view(-1, w.B, k, D)
-    ocfg = oracle.make_config(**w.config_fields())
-    rng = np.random.default_rng([w.seed, 7])
-    for _ in range(10):
-        l, b, h = int(rng.integers(w.L)), int(rng.integers(w.B)), int(rng.integers(w.H))
-        keys = synthkv.bf16_bits(K[l, b, h, s0:s0 + n])
-        want_norm = np.array([oracle.key_sqnorm(r) for r in keys], np.float32)
-        got_norm = norms[l, b, h].cpu().numpy()
-        assert np.array_equal(got_norm.view(np.uint32), want_norm.view(np.uint32))
-        want_idx = oracle.retain_select(want_norm, k)
-        assert np.array_equal(idx[l, b, h].cpu().numpy(), want_idx)
-        for X, (src, rec, ret) in enumerate(((K, Ko, retk), (V, Vo, retv))):
-            rows = synthkv.bf16_bits(src[l, b, h, s0:s0 + n])
-            prot, slot = oracle.route(ocfg, mask, X, l, h)
-            got = synthkv.bf16_bits(rec[l, b, h, s0:s0 + n])
-            if prot:
-                assert np.array_equal(got, rows)
-                continue
-            assert np.array_equal(ret[slot, b].cpu().numpy().view(np.uint16), rows[want_idx])
-            want = oracle.dequantize_slice(ocfg, X, *oracle.quantize_slice(ocfg, X, rows))
-            want[want_idx] = rows[want_idx]
-            assert np.array_equal(got, want)
-    # properties over every head: each list ascending and in range, and the
-    # retained rows restored bit-identical
-    assert bool((idx[..., 1:] > idx[..., :-1]).all()) and int(idx.min()) >= 0 and int(idx.max()) < n
-    gathered = torch.gather(Ko[:, :, :, s0:s0 + n], 3,
-                            idx.long().unsqueeze(-1).expand(-1, -1, -1, -1, D))
-    source = torch.gather(K[:, :, :, s0:s0 + n], 3, idx.long().unsqueeze(-1).expand(-1, -1, -1, -1, D))
-    assert torch.equal(gathered.view(torch.int16), source.view(torch.int16))
-    # the one-pass form writes exactly the same bytes, out of place (norms
-    # from its own pass) and in place (norms from a separate pass)
-    del packed
-    img = slice(s0, s0 + n)
-    Kf, Vf = torch.empty_like(K), torch.empty_like(V)
-    hg.hg_fake_quantize(cfg, K, V, mask, Kf, Vf)
-    torch.cuda.synchronize()
-    assert torch.equal(Kf[:, :, :, img].view(torch.int16), Ko[:, :, :, img].view(torch.int16))
-    assert torch.equal(Vf[:, :, :, img].view(torch.int16), Vo[:, :, :, img].view(torch.int16))
-    del Kf, Vf
-    hg.hg_fake_quantize(cfg, K, V, mask, K, V)
-    torch.cuda.synchronize()
-    assert torch.equal(K[:, :, :, img].view(torch.int16), Ko[:, :, :, img].view(torch.int16))
-    assert torch.equal(V[:, :, :, img].view(torch.int16), Vo[:, :, :, img].view(torch.int16))
-    torch.cuda.empty_cache()
+    import paper_2609_35800_amd as hg
+    sizes = hg.hg_packed_sizes(hg.make_config(**w.config_fields()), synthkv.protect_mask(w))
+    assert sizes["retain_count"] == 67  # round(0.02 * 3328)
+    wholecache.assert_whole(wholecache.quantize_dequantize(w), w)
+
+
+@pytest.mark.parametrize("inplace", [False, True])
+def test_full_size_internvl_two_percent_one_pass(inplace):
+    w = synthkv.WORKLOADS["internvl-8b"].with_(retain_permille=20)
+    wholecache.assert_whole(wholecache.fake_quantize(w, inplace=inplace), w)

@@ -28,17 +28,17 @@ SHAPES = [(28, 28, 4), (32, 32, 8), (32, 32, 32), (48, 40, 8), (28, 16, 8), (80,
 
 
 @pytest.mark.parametrize("shape", SHAPES)
-@pytest.mark.parametrize("fraction", [1 / 16, 1 / 12, 1 / 8, 1 / 4])
-def test_matches_oracle(shape, fraction):
+@pytest.mark.parametrize("den", [16, 12, 8, 4])
+def test_matches_oracle(shape, den):
     L, Hq, Hkv = shape
-    rng = np.random.default_rng(L * 1000 + Hq + int(1 / fraction))
+    rng = np.random.default_rng(L * 1000 + Hq + den)
     for trial in range(3):
         g = rng.gamma(1.5, 1e-3, size=(L, Hq))
         o = rng.gamma(2.0, 1e-2, size=(L, Hq))
         if trial == 1:  # exact ties: duplicate whole layers
             g[1] = g[0]
             o[1] = o[0]
-        K = hg.head_budget(L * Hkv, fraction)
+        K = hg.head_budget(L * Hkv, 1, den)
         got = hg.hg_select_heads(g, o, Hkv, K)
         want = oracle.select_heads(g, o, Hkv, K)
         assert got.sum() == K
@@ -51,7 +51,26 @@ def test_constant_scores_and_budget_edges():
     assert list(hg.hg_select_heads(g, o, 2, 3)) == [1, 1, 1, 0, 0, 0, 0, 0]
     assert hg.hg_select_heads(g, o, 2, 0).sum() == 0
     assert hg.hg_select_heads(g, o, 2, 100).sum() == 8
+    # the protected-head counts of the five workloads (1/8 of N_KV), and halves up
     assert [hg.head_budget(n) for n in (8, 112, 1024, 256, 640, 12, 4)] == [1, 14, 128, 32, 80, 2, 1]
+
+
+def test_head_budget_rounding_and_errors():
+    # exact integer rounding, halves up, no floating-point drift at large n
+    assert hg.head_budget(20, 1, 8) == 3      # 2.5 -> 3
+    assert hg.head_budget(12, 1, 16) == 1     # 0.75 -> 1
+    assert hg.head_budget(8, 1, 16) == 1      # 0.5 -> 1
+    assert hg.head_budget(7, 1, 16) == 0      # 0.4375 -> 0
+    assert hg.head_budget(8192, 1, 1) == 8192 and hg.head_budget(8192, 0, 5) == 0
+    assert hg.head_budget(8191, 1, 4) == 2048  # 2047.75
+    for n in range(1, 300):
+        for num, den in ((1, 16), (1, 12), (1, 8), (1, 4), (3, 8)):
+            want = (2 * n * num + den) // (2 * den)
+            assert hg.head_budget(n, num, den) == want == int(np.floor(n * num / den + 0.5))
+    for bad in ((0, 1, 8), (8, -1, 8), (8, 9, 8), (8, 1, 0)):
+        with pytest.raises(hg.HeadGuardError) as e:
+            hg.head_budget(*bad)
+        assert e.value.status == hg.HG_ERR_SHAPE
 
 
 def test_errors():
