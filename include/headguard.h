@@ -196,6 +196,22 @@ int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
                      const uint8_t* protect_mask, uint16_t* K_out, uint16_t* V_out,
                      void* workspace, uint64_t workspace_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid allocation): hg_fake_quantize
+ * with its token-retention workspace taken from a device array inside the
+ * library, HG_NOALLOC_SCRATCH_BYTES per GPU, held until the process ends,
+ * instead of a caller buffer.  Same arguments, results and errors as
+ * hg_fake_quantize otherwise; a call whose workspace would exceed the array
+ * (hg_sizes.fake_workspace in place, about 4n + 4k bytes per (l, b, h) out of
+ * place) returns HG_ERR_SHAPE before any device work.  Allocates nothing.
+ * Every call on one GPU shares that GPU's array: calls that overlap in time on
+ * one GPU (on other streams or host threads) race on it and must be
+ * serialized by the caller; nothing in it needs clearing between calls. */
+#define HG_NOALLOC_SCRATCH_BYTES (96u << 20)
+int hg_fake_quantize_noalloc(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
+                             const uint8_t* protect_mask, uint16_t* K_out, uint16_t* V_out,
+                             hipStream_t stream);
+
 /* Head budget (§3, "Selecting physical KV heads"): K = round(n_kv_heads *
  * num / den), halves rounded up, in exact integer arithmetic; the paper's
  * main budget is 1/8 of the physical KV heads, its sweeps 1/16 to 1/4.

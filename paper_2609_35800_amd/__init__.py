@@ -67,8 +67,9 @@ def _load():
     lib.hg_select_heads.argtypes = [P, P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, P]
     lib.hg_fake_quantize.argtypes = [C.POINTER(hg_config), P, P, P, P, P, P, C.c_uint64, P]
     lib.hg_head_budget.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_int32)]
+    lib.hg_fake_quantize_noalloc.argtypes = [C.POINTER(hg_config), P, P, P, P, P, P]
     for f in ("hg_packed_sizes", "hg_quantize", "hg_dequantize", "hg_select_heads",
-              "hg_fake_quantize", "hg_head_budget"):
+              "hg_fake_quantize", "hg_head_budget", "hg_fake_quantize_noalloc"):
         getattr(lib, f).restype = C.c_int
     lib.hg_status_string.argtypes = [C.c_int]
     lib.hg_status_string.restype = C.c_char_p
@@ -170,6 +171,19 @@ def hg_fake_quantize(cfg: hg_config, K: torch.Tensor, V: torch.Tensor, protect_m
     nbytes = workspace.numel() * workspace.element_size() if ws is not None else 0
     _check(_lib.hg_fake_quantize(C.byref(cfg), _ptr(K), _ptr(V), m.ctypes.data_as(C.c_void_p),
                                  _ptr(K_out), _ptr(V_out), ws, nbytes, _stream(stream)))
+
+
+def hg_fake_quantize_noalloc(cfg: hg_config, K: torch.Tensor, V: torch.Tensor, protect_mask,
+                             K_out: torch.Tensor, V_out: torch.Tensor, stream=None) -> None:
+    """hg_fake_quantize with the retention workspace taken from the library's
+    own device array (HG_NOALLOC_SCRATCH_BYTES per GPU): nothing is allocated;
+    overlapping calls on one GPU race on that array."""
+    m = _mask_arg(protect_mask)
+    _check(_lib.hg_fake_quantize_noalloc(C.byref(cfg), _ptr(K), _ptr(V), m.ctypes.data_as(C.c_void_p),
+                                         _ptr(K_out), _ptr(V_out), _stream(stream)))
+
+
+HG_NOALLOC_SCRATCH_BYTES = 96 << 20  # headguard.h
 
 
 # ------------------------------------------------------------ allocation helper

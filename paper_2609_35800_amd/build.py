@@ -14,7 +14,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libheadguard.so")
 SOURCES = ["api.hip", "quantize.hip", "dequantize.hip", "fakequant.hip", "kivi_seq.hip", "retain.hip",
-           "select.cpp"]
+           "noalloc.hip", "select.cpp"]
 ARCH = os.environ.get("HG_OFFLOAD_ARCH", "gfx950")
 
 FLAGS = [

@@ -346,13 +346,11 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
 
 namespace hg {
 
-// The one-pass simulated quantization with its retention workspace `ws` of
-// `ws_bytes` bytes of device memory (unused without token retention).
-// `caller_ws`: the workspace is the caller's buffer, checked like the other
-// arguments; otherwise it is library memory known to be device memory.
+// The one-pass simulated quantization.  `get_ws` supplies the token-retention
+// workspace once the call's host-side argument checks have passed and its
+// size is known (it is not called without retention).
 int fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, const uint8_t* mask,
-                  uint16_t* K_out, uint16_t* V_out, void* ws, uint64_t ws_bytes, bool caller_ws,
-                  hipStream_t stream) {
+                  uint16_t* K_out, uint16_t* V_out, const WorkspaceFn& get_ws, hipStream_t stream) {
   int s = check_config(cfg, mask);
   if (!s) s = check_grid(cfg);
   if (s) return s;
@@ -389,23 +387,27 @@ int fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, co
   const bool fused = retain && K_out != K && V_out != V;
   const FakeWorkspace lay = fake_workspace(z);
   const uint64_t ws_need = !retain ? 0 : fused ? lay.out_of_place : lay.in_place;
-  if (ws_need && caller_ws && !ws)
-    return fail(HG_ERR_NULL, "workspace is NULL but the call needs %llu bytes", (unsigned long long)ws_need);
-  if (ws_need > ws_bytes)
-    return fail(HG_ERR_SHAPE, "the call needs a %llu-byte workspace (%llu bytes available)",
-                (unsigned long long)ws_need, (unsigned long long)ws_bytes);
+  Workspace wsp;
   if (ws_need) {
-    if (!aligned(ws, 256)) return fail(HG_ERR_ALIGN, "workspace is not 256-byte aligned");
+    s = get_ws(ws_need, &wsp);
+    if (s) return s;
+    if (!wsp.ptr)
+      return fail(HG_ERR_NULL, "workspace is NULL but the call needs %llu bytes", (unsigned long long)ws_need);
+    if (ws_need > wsp.bytes)
+      return fail(HG_ERR_SHAPE, "the call needs a %llu-byte workspace (%llu bytes available)",
+                  (unsigned long long)ws_need, (unsigned long long)wsp.bytes);
+    if (!aligned(wsp.ptr, 256)) return fail(HG_ERR_ALIGN, "workspace is not 256-byte aligned");
     const void* ins[4] = {K, V, K_out, V_out};
     const char* names[4] = {"K", "V", "K_out", "V_out"};
     for (int i = 0; i < 4; ++i)
-      if (overlap(ws, ws_need, ins[i], need)) return fail(HG_ERR_POINTER, "workspace overlaps %s", names[i]);
+      if (overlap(wsp.ptr, ws_need, ins[i], need)) return fail(HG_ERR_POINTER, "workspace overlaps %s", names[i]);
   }
+  void* const ws = wsp.ptr;
   const Buf bufs[] = {{K, need, 16, "K"},
                       {V, need, 16, "V"},
                       {K_out, need, 16, "K_out"},
                       {V_out, need, 16, "V_out"},
-                      {ws, caller_ws ? ws_need : 0, 256, "workspace"}};
+                      {ws, wsp.caller ? ws_need : 0, 256, "workspace"}};
   s = check_device();
   if (s) return s;
   s = check_buffers(bufs, 5);
@@ -452,8 +454,13 @@ extern "C" {
 int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, const uint8_t* mask,
                      uint16_t* K_out, uint16_t* V_out, void* workspace, uint64_t workspace_bytes,
                      hipStream_t stream) {
-  return hg::fake_quantize(cfg, K, V, mask, K_out, V_out, workspace, workspace ? workspace_bytes : 0, true,
-                           stream);
+  const hg::WorkspaceFn caller = [&](uint64_t, hg::Workspace* ws) {
+    ws->ptr = workspace;
+    ws->bytes = workspace ? workspace_bytes : 0;
+    ws->caller = true;
+    return (int)HG_OK;
+  };
+  return hg::fake_quantize(cfg, K, V, mask, K_out, V_out, caller, stream);
 }
 
 int hg_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, const uint8_t* mask,

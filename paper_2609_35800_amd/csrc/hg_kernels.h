@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <functional>
+
 #include "headguard.h"
 
 namespace hg {
@@ -92,6 +94,21 @@ hipError_t launch_key_norms(const Params& p, int D, hipStream_t stream);
 enum class RowCopy { kGather, kScatter, kCacheToOut };
 hipError_t launch_retain_select(const Params& p, int D, RowCopy mode, hipStream_t stream);
 hipError_t launch_retain_rows(const Params& p, int D, RowCopy mode, hipStream_t stream);
+
+// Host side: the one-pass call (api.hip) with its token-retention workspace
+// supplied by `get_ws(need, &ws)` after the host-side argument checks, only
+// when the call needs one: the caller's buffer (checked like every other
+// argument) or library memory (`caller` false).  get_ws returns HG_OK or an
+// error status, with the detail recorded by set_error.
+struct Workspace {
+  void* ptr = nullptr;
+  uint64_t bytes = 0;
+  bool caller = true;
+};
+typedef std::function<int(uint64_t need, Workspace* ws)> WorkspaceFn;
+int fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, const uint8_t* mask,
+                  uint16_t* K_out, uint16_t* V_out, const WorkspaceFn& get_ws, hipStream_t stream);
+int set_error(int status, const char* msg);
 
 // Routing of one (tensor, slice): whether it is kept in BF16 and its slot in
 // the packed buffers (rank among kept heads if kept, else among quantized

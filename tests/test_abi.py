@@ -203,6 +203,22 @@ def test_fake_quantize_workspace_is_checked_before_device_work():
     assert hg.hg_packed_sizes(cfg0, mask)["fake_workspace"] == 0
 
 
+def test_no_alloc_one_pass_refuses_a_workspace_beyond_its_array():
+    """The allocation-free one-pass call checks its workspace need against the
+    library's array before any device work."""
+    f = _cfg(base=2, retain_permille=20, L=8, B=16, H=16, T=40000, img_start=0, img_len=40000, D=64)
+    cfg = hg.make_config(**f)
+    mask = np.zeros(128, np.uint8)
+    assert hg.hg_packed_sizes(cfg, mask)["fake_workspace"] > hg.HG_NOALLOC_SCRATCH_BYTES
+    base = 1 << 36  # never dereferenced
+    rc = hg.library().hg_fake_quantize_noalloc(C.byref(cfg), base, base + (1 << 34),
+                                               mask.ctypes.data_as(C.c_void_p), base, base + (1 << 34), None)
+    assert rc == hg.HG_ERR_SHAPE and "array holds" in hg.hg_last_error()
+    text = open(HEADER).read()
+    assert re.search(r"#define HG_NOALLOC_SCRATCH_BYTES \(96u << 20\)", text)
+    assert hg.HG_NOALLOC_SCRATCH_BYTES == 96 << 20
+
+
 def test_overlapping_outputs_are_refused_before_device_work():
     f = _cfg()
     cfg = hg.make_config(**f)
