@@ -71,6 +71,15 @@
  * kernels before it are enqueued and may write their outputs.  Calls are
  * thread-safe; the error detail is per thread.
  *
+ * KIVI keys over the whole sequence (kivi_group = 0): when a key slice is
+ * longer than one workgroup holds on chip, several co-resident workgroups
+ * hold it together and exchange partial ranges through the caller's
+ * workspace, waiting for one another (a bounded number of polls).  The
+ * kernel is sized to be resident on an otherwise idle device: a kernel
+ * running concurrently on another stream can delay it, and one that keeps
+ * compute units busy long enough makes waits run out (the workspace's first
+ * word then counts them and the codes of the slices affected are wrong).
+ *
  * Every buffer a call writes must be disjoint from every other buffer of the
  * call (HG_ERR_POINTER, checked on the host from the pointers and the sizes
  * hg_packed_sizes reports).  Preconditions not checked: inputs finite with
@@ -129,9 +138,13 @@ typedef struct {
 typedef struct {
   uint64_t codes_k, meta_k, side_k, codes_v, meta_v, side_v; /* bytes          */
   uint64_t norm_k, ret_idx, ret_k, ret_v;  /* bytes; 0 without token retention    */
+  uint64_t workspace;          /* bytes of hg_quantize's workspace: the exchange
+                                  area of KIVI keys over the whole sequence when
+                                  a slice spans several workgroups; else 0      */
   uint64_t fake_workspace;     /* bytes of hg_fake_quantize's workspace: the key
                                   norms, token lists and (in place) saved rows
-                                  of token retention; 0 without retention       */
+                                  of token retention, or the same exchange area
+                                  as `workspace`; else 0                        */
   int32_t n_protected;         /* heads with mask = 1                             */
   int32_t n_unprot_k, n_unprot_v; /* heads whose K / V are quantized              */
   int32_t retain_count;        /* k, retained tokens per (l, b, h)                */
@@ -140,6 +153,11 @@ typedef struct {
 typedef struct {
   void *codes_k, *meta_k, *side_k, *codes_v, *meta_v, *side_v; /* device */
   void *norm_k, *ret_idx, *ret_k, *ret_v;                      /* device */
+  void *workspace;  /* device, hg_sizes.workspace bytes, 256-byte aligned;
+                       scratch for hg_quantize (contents on entry do not
+                       matter; after the call its first 8 bytes count waits
+                       that ran out of polls, 0 normally); unused by
+                       hg_dequantize; may be NULL when its size is 0     */
 } hg_packed;
 
 /* Byte sizes of the packed buffers (the storage model of §5.4).  Pure
@@ -188,8 +206,10 @@ int hg_select_heads(const double* g, const double* o, int32_t L, int32_t Hq, int
  * retention it holds the key norms, the retained token lists and, in place,
  * the saved retained rows, and must be at least hg_sizes.fake_workspace
  * bytes (out of place it needs only the norms and lists, about 4n + 4k bytes
- * per (l, b, h)); its contents on entry do not matter and are overwritten.
- * Without retention it is not used and may be NULL.  Errors: HG_ERR_NULL if it
+ * per (l, b, h)); with KIVI keys over the whole sequence it is the exchange
+ * area described above (hg_sizes.fake_workspace = hg_sizes.workspace); its
+ * contents on entry do not matter and are overwritten.  When
+ * hg_sizes.fake_workspace is 0 it is not used and may be NULL.  Errors: HG_ERR_NULL if it
  * is NULL but needed, HG_ERR_SHAPE if workspace_bytes is too small,
  * HG_ERR_ALIGN, HG_ERR_POINTER (overlap, or not device memory). */
 int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,

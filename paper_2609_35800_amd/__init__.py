@@ -28,7 +28,8 @@ for _i, _n in enumerate(STATUS):
     globals()[_n] = _i
 HG_MAX_HEADS = 8192  # largest L*H the routing holds (headguard.h)
 BUFFERS = ("codes_k", "meta_k", "side_k", "codes_v", "meta_v", "side_v",
-           "norm_k", "ret_idx", "ret_k", "ret_v")
+           "norm_k", "ret_idx", "ret_k", "ret_v")  # the packed outputs
+PACKED = BUFFERS + ("workspace",)  # the fields of hg_packed
 
 
 class hg_config(C.Structure):
@@ -38,13 +39,14 @@ class hg_config(C.Structure):
 
 
 class hg_sizes(C.Structure):
-    _fields_ = [(n, C.c_uint64) for n in BUFFERS] + [("fake_workspace", C.c_uint64)] + [
+    _fields_ = [(n, C.c_uint64) for n in BUFFERS] + [("workspace", C.c_uint64),
+                                                     ("fake_workspace", C.c_uint64)] + [
         ("n_protected", C.c_int32), ("n_unprot_k", C.c_int32), ("n_unprot_v", C.c_int32),
         ("retain_count", C.c_int32)]
 
 
 class hg_packed(C.Structure):
-    _fields_ = [(n, C.c_void_p) for n in BUFFERS]
+    _fields_ = [(n, C.c_void_p) for n in PACKED]
 
 
 class HeadGuardError(RuntimeError):
@@ -138,7 +140,7 @@ def hg_packed_sizes(cfg: hg_config, protect_mask) -> Dict[str, int]:
 
 
 def _packed_struct(packed: Dict[str, torch.Tensor]) -> hg_packed:
-    return hg_packed(**{n: _ptr(packed.get(n)) for n in BUFFERS})
+    return hg_packed(**{n: _ptr(packed.get(n)) for n in PACKED})
 
 
 def hg_quantize(cfg: hg_config, K: torch.Tensor, V: torch.Tensor, protect_mask,
@@ -189,9 +191,10 @@ HG_NOALLOC_SCRATCH_BYTES = 96 << 20  # headguard.h
 # ------------------------------------------------------------ allocation helper
 
 def alloc_packed(cfg: hg_config, protect_mask, device="cuda") -> Dict[str, torch.Tensor]:
-    """Device buffers of the sizes hg_packed_sizes reports (uint8 tensors)."""
+    """Device buffers of the sizes hg_packed_sizes reports (uint8 tensors),
+    the quantize call's workspace included."""
     sz = hg_packed_sizes(cfg, protect_mask)
-    return {n: torch.empty(sz[n], dtype=torch.uint8, device=device) for n in BUFFERS}
+    return {n: torch.empty(sz[n], dtype=torch.uint8, device=device) for n in PACKED}
 
 
 def alloc_fake_workspace(cfg: hg_config, protect_mask, device="cuda") -> Optional[torch.Tensor]:

@@ -64,16 +64,19 @@ def build(verbose: bool = False, out: str = LIB, host_asan: bool = False) -> str
 
 
 def check_launch_stubs(lib: str) -> None:
-    """Fail the build if a kernel's host launch stub is left undefined (the
-    host pass can drop it when a kernel template does not instantiate there);
-    such a library would not load."""
+    """Fail the build if a kernel's host launch stub or handle, or another
+    symbol of the library's own namespace, is left undefined (the host pass
+    can drop a kernel template's handle when it is only used through a
+    pointer); such a library would not load."""
     nm = os.environ.get("NM", "nm")
     syms = subprocess.run([nm, "-D", "--undefined-only", lib], check=True, capture_output=True,
                           text=True).stdout
-    missing = [line.split()[-1] for line in syms.splitlines() if "__device_stub__" in line]
+    missing = [line.split()[-1] for line in syms.splitlines()
+               if "__device_stub__" in line or line.split()[-1].startswith("_ZN2hg")]
     if missing:
         os.remove(lib)
-        raise RuntimeError(f"{len(missing)} kernel launch stub(s) undefined, e.g. {missing[0]}")
+        raise RuntimeError(f"{len(missing)} kernel launch stub(s) or library symbol(s) undefined, "
+                           f"e.g. {missing[0]}")
 
 
 if __name__ == "__main__":

@@ -183,6 +183,13 @@ FakeWorkspace fake_workspace(const hg_sizes& z) {
   return w;
 }
 
+// Exchange workspace of KIVI-style keys over the whole sequence: needed when
+// a key slice is held by several workgroups and some key slice is quantized.
+uint64_t kivi_exchange_bytes(const hg_config* c, const Counts& k) {
+  if (c->base != HG_BASE_KIVI || c->kivi_group != 0 || k.n == 0 || k.uk == 0) return 0;
+  return hg::kivi_workspace_bytes(c->T, c->D);
+}
+
 void fill_params(hg::Params& p, const hg_config* c, const uint8_t* mask) {
   memset(&p, 0, sizeof p);
   p.L = c->L;
@@ -262,7 +269,8 @@ int hg_packed_sizes(const hg_config* cfg, const uint8_t* mask, hg_sizes* out) {
   out->ret_idx = LHB * k.k * 4;
   out->ret_k = (uint64_t)k.uk * B * k.k * D * 2;
   out->ret_v = (uint64_t)k.uv * B * k.k * D * 2;
-  out->fake_workspace = fake_workspace(*out).in_place;
+  out->workspace = kivi_exchange_bytes(cfg, k);
+  out->fake_workspace = cfg->retain_permille > 0 ? fake_workspace(*out).in_place : out->workspace;
   return ok();
 }
 
@@ -289,6 +297,7 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
       {pk->ret_idx, z.ret_idx, 16, "ret_idx"},
       {pk->ret_k, z.ret_k, 16, "ret_k"},
       {pk->ret_v, z.ret_v, 16, "ret_v"},
+      {pk->workspace, quantize ? z.workspace : 0, 256, "workspace"},  // dequantize does not use it
   };
   const int nb = (int)(sizeof bufs / sizeof bufs[0]);
   // Every buffer the call writes (quantize: the packed ones; dequantize: K_out,
@@ -333,7 +342,9 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
                     : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, stream);
   });
   if (e == hipSuccess && quantize && p.kivi_whole)
-    e = step([&] { return hg::launch_kivi_seq(p, cfg->D, cfg->bits, false, stream); });
+    e = step([&] {
+      return hg::launch_kivi_seq(p, cfg->D, cfg->bits, false, z.workspace ? pk->workspace : nullptr, stream);
+    });
   if (e == hipSuccess && p.k > 0 && quantize)
     e = step([&] { return hg::launch_retain_select(p, cfg->D, hg::RowCopy::kGather, stream); });
   if (e == hipSuccess && p.k > 0 && !quantize)
@@ -386,7 +397,8 @@ int fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, co
   const bool retain = need && z.retain_count > 0;
   const bool fused = retain && K_out != K && V_out != V;
   const FakeWorkspace lay = fake_workspace(z);
-  const uint64_t ws_need = !retain ? 0 : fused ? lay.out_of_place : lay.in_place;
+  // retention (AKVQ) or the exchange of whole-sequence KIVI key ranges
+  const uint64_t ws_need = retain ? (fused ? lay.out_of_place : lay.in_place) : need ? z.workspace : 0;
   Workspace wsp;
   if (ws_need) {
     s = get_ws(ws_need, &wsp);
@@ -437,7 +449,7 @@ int fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, co
   if (e == hipSuccess)
     e = step([&] { return hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, fused, stream); });
   if (e == hipSuccess && p.kivi_whole)
-    e = step([&] { return hg::launch_kivi_seq(p, cfg->D, cfg->bits, true, stream); });
+    e = step([&] { return hg::launch_kivi_seq(p, cfg->D, cfg->bits, true, ws, stream); });
   if (e == hipSuccess && fused) {
     e = step([&] { return hg::launch_retain_select(p, cfg->D, hg::RowCopy::kCacheToOut, stream); });
   } else if (e == hipSuccess && retain) {

@@ -120,8 +120,7 @@ __device__ __forceinline__ void fake_tokens(const uint16_t* rows, uint16_t* out,
       // rotation for AKVQ keys, then BF16.
 #pragma unroll
       for (int e = 0; e < E; ++e) {
-        const uint32_t code = code_bits(x[e], g) - kMagicBits;
-        x[e] = __builtin_fmaf((float)code, S, g.m);
+        x[e] = __builtin_fmaf(__builtin_rintf(code_scaled(x[e], g)), S, g.m);
       }
       if constexpr (ROTATE) fwht_quad<E, G>(x, j, fwht_scale<D>());
 
@@ -202,7 +201,7 @@ __device__ __forceinline__ void fake_kivi_keys(const uint16_t* rows, uint16_t* o
       float y[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        y[e] = __builtin_fmaf((float)(code_bits(x[k][e], g[e]) - kMagicBits), S[e], g[e].m);
+        y[e] = __builtin_fmaf(__builtin_rintf(code_scaled(x[k][e], g[e])), S[e], g[e].m);
       const u32x4 v = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
                        pack_bf16x2_hw(y[6], y[7])};
       if (t < n) store_nt((u32x4*)(out + (size_t)t * D + 8 * c8), v);

@@ -176,6 +176,11 @@ __device__ __forceinline__ uint32_t code_bits(float v, const GroupScale& g) {
   return __float_as_uint(t + 0x1.8p23f);
 }
 
+// The scaled value of one element, t = (v - m) * inv (two roundings, no
+// contraction), whose rint is its code (see code_bits: 0 <= t < L + 1/2).
+// The one-pass reconstruction takes rint(t) directly (v_rndne_f32).
+__device__ __forceinline__ float code_scaled(float v, const GroupScale& g) { return (v - g.m) * g.inv; }
+
 // ------------------------------------------------- Walsh-Hadamard transform
 
 // fp32(1/sqrt(D)) for the supported power-of-two head dims: 1/8 and 1/16

@@ -82,9 +82,15 @@ hipError_t launch_quantize(const Params& p, int base, int D, int bits, bool norm
 hipError_t launch_dequantize(const Params& p, int base, int D, int bits, hipStream_t stream);
 hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, bool norms, hipStream_t stream);
 // KIVI keys over the whole sequence: a persistent grid over the quantized key
-// slices (a 64-channel part of a slice per workgroup, held on chip, when
-// T <= 3072; else a range pass and a code pass per slice).
-hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, hipStream_t stream);
+// slices; each slice is held on chip by a group of workgroups (each a run of
+// its rows, every channel) that combine their partial ranges through the
+// exchange workspace `ws` (kivi_workspace_bytes; unused with one workgroup
+// per slice), or, for longer slices, a range pass and a code pass per slice.
+hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, void* ws, hipStream_t stream);
+// Workgroups per slice of the resident kernel (0: the two-pass kernel), and
+// the exchange workspace bytes a call with T rows per slice needs (0: none).
+int kivi_partners(int T, int D);
+uint64_t kivi_workspace_bytes(int T, int D);
 // Token retention: squared key norms of every image token (p.norm); the k
 // largest per (l, b, h) into p.ret_idx; their rows gathered from p.cache into
 // p.ret, written back from p.ret into p.out, or copied from p.cache straight

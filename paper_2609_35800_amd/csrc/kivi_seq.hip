@@ -7,32 +7,43 @@
 // slice, so a slice must be fully read before any of its codes is formed.
 // Two kernels:
 //
-// Resident (T <= kResRows): a persistent grid, one 1024-thread workgroup per
-// compute unit.  A workgroup takes one 64-channel part of a key slice (l, b, h)
-// and holds all T rows of that part on chip — 9 row slots in LDS, filled by
-// buffer loads that write LDS directly, and 15 in registers, 128 rows per
-// slot — so each slice is read from HBM exactly once:
-//  1. per-channel min / max over the resident rows (each lane holds 8
-//     channels of one row per slot), reduced across the wavefront's rows by
-//     shuffles and across the 16 wavefronts through LDS; 64 lanes form the
-//     part's group scales and write its metadata words;
-//  2. codes (or, for the one-pass simulated quantization, the BF16
-//     reconstruction) of the image rows from the resident copy; as the slots
-//     are consumed, the loads of the workgroup's next slice are issued into
-//     them, so the next slice streams in while this one is coded.
-// The parts of one slice go to workgroups whose indices differ by multiples
-// of 8 (the dispatcher places those on the same XCD), so a slice's parts are
-// processed at the same time.
+// Partitioned resident kernel (T at most 8 workgroups' capacity): a
+// persistent grid of 1024-thread workgroups, one per compute unit.  A group of
+// P workgroups takes one key slice (l, b, h) at a time; workgroup q of the
+// group holds rows [q R, (q + 1) R) of the slice, every channel, on chip (9
+// row slots in LDS filled by buffer loads that write LDS directly, 15 in
+// registers), so each slice is read from HBM exactly once:
+//  1. per-channel min / max over the workgroup's rows, reduced across the
+//     rows a wavefront holds by shuffles and across wavefronts by LDS
+//     atomics;
+//  2. with P > 1, the group's partial ranges are combined through a caller
+//     workspace: each workgroup publishes its 2D partial values as 64-bit
+//     words tagged with the slice's sequence number in the group (relaxed
+//     device-scope atomics; a tagged word carries its own value, so no fence
+//     is needed) and waits, a bounded number of polls, for its partners'
+//     words of the same tag; two buffers alternate between consecutive
+//     slices;
+//  3. codes (or, for the one-pass simulated quantization, the BF16
+//     reconstruction) of the workgroup's image rows: whole packed rows, so
+//     every stored line is complete; as the row slots are consumed, the
+//     loads of the workgroup's rows of the next slice are issued into them.
+// The grid never exceeds the number of workgroups the device holds at once,
+// so every partner of a group is resident; a wait that runs out of polls
+// (only if another kernel held the device's resources) ends anyway and is
+// counted in the workspace's first word.  (Two 512-thread workgroups per
+// compute unit, each holding half as many rows, measured 1 % slower.)
 //
-// Two-pass (longer slices): a persistent grid of kSeqBlocksPerCU workgroups
-// of kSeqThreads threads per compute unit walks the key slices; per slice a
-// range pass over all T rows, the wavefronts' partial ranges combined through
-// LDS, then a second pass over the image rows for the codes.  The grid is
-// sized so that the slices in flight at once stay within the 256 MB Infinity
-// Cache, which then serves much of the second read.
+// Two-pass kernel (longer slices): a persistent grid of kSeqBlocksPerCU
+// workgroups of kSeqThreads threads per compute unit walks the key slices;
+// per slice a range pass over all T rows, the wavefronts' partial ranges
+// combined through LDS, then a second pass over the image rows for the codes.
+// The grid is sized so that the slices in flight at once stay within the
+// 256 MB Infinity Cache, which then serves much of the second read.
 //
 // Values, protected slices and the rest of the cache are handled by the
 // regular kernels of the same call.
+
+#include <stdlib.h>
 
 #include <algorithm>
 
@@ -136,18 +147,18 @@ __device__ __forceinline__ void kivi_seq_slice(const Params& p, uint32_t s, cons
       const int t = t0 + u * STEP;
       const float x[8] = {bf16_lo(v[u].x), bf16_hi(v[u].x), bf16_lo(v[u].y), bf16_hi(v[u].y),
                           bf16_lo(v[u].z), bf16_hi(v[u].z), bf16_lo(v[u].w), bf16_hi(v[u].w)};
-      uint32_t cb[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) cb[e] = code_bits(x[e], g[e]);
       if constexpr (FAKE) {
         float y[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf((float)(cb[e] - kMagicBits), S[e], g[e].m);
+        for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf(__builtin_rintf(code_scaled(x[e], g[e])), S[e], g[e].m);
         const u32x4 o = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
                          pack_bf16x2_hw(y[6], y[7])};
         if (t < p.n) store_nt((u32x4*)(out + (size_t)t * D + 8 * c8), o);
       } else {
-        const Packed<8, BITS> pk = pack_code_bits<8, BITS>(cb);
+        uint32_t cq[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cq[e] = code_bits(x[e], g[e]);
+        const Packed<8, BITS> pk = pack_code_bits<8, BITS>(cq);
         if (t < p.n) store_packed<8, BITS>(codes + (size_t)t * ROW + c8 * BITS, pk);
       }
     }
@@ -165,18 +176,20 @@ __global__ __launch_bounds__(kSeqThreads) void kivi_seq_kernel(const Params p) {
   }
 }
 
-// ------------------------------------------------------ resident variant
+// ------------------------------------------------- partitioned resident kernel
 
-constexpr int kResThreads = 1024;
-constexpr int kResWaves = kResThreads / 64;
-constexpr int kResPart = 64;                                  // channels per workgroup part
-constexpr int kResLanesPerRow = kResPart / 8;                 // 8 channels per lane
-constexpr int kResRowsPerWave = 64 / kResLanesPerRow;         // rows per load instruction
-constexpr int kResRowsPerSlot = kResWaves * kResRowsPerWave;  // 128
-constexpr int kResLdsSlots = 9;
-constexpr int kResRegSlots = 15;
-constexpr int kResSlots = kResLdsSlots + kResRegSlots;
-constexpr int kResRows = kResSlots * kResRowsPerSlot;         // 3072
+constexpr int kPartThreads = 1024;
+constexpr int kPartWaves = kPartThreads / 64;
+constexpr int kPartLdsSlots = 9;
+constexpr int kPartRegSlots = 15;
+constexpr int kPartSlots = kPartLdsSlots + kPartRegSlots;
+constexpr int kMaxPartners = 8;
+// Exchange area (u64 words): a header (word 0 counts waits that ran out of
+// polls), then [group][2 buffers][partner][2D] tagged words for at most
+// kExMaxWgs workgroups.
+constexpr int kExHeader = 64;
+constexpr int kExMaxWgs = 1024;
+constexpr uint32_t kSpinLimit = 1u << 20;
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
@@ -185,10 +198,9 @@ typedef __attribute__((address_space(3))) void* lds_ptr;
 constexpr int kWaitVmem0 = 0x0F70;
 constexpr int kWaitLds0 = 0xC07F;
 
-// Work item i of the resident kernel: the i-th (unprotected key head, batch
-// row) pair, heads in row-major (l, h) order.  Its slab in the packed key
-// buffers is i itself (slot u = i / B is the head's rank among quantized key
-// heads).  Scalar work.
+// Work item i: the i-th (unprotected key head, batch row) pair, heads in
+// row-major (l, h) order.  Its slab in the packed key buffers is i itself
+// (slot u = i / B is the head's rank among quantized key heads).  Scalar work.
 struct ResItem {
   uint32_t s;  // slice (l*B + b)*H + h
   bool valid;
@@ -228,17 +240,19 @@ __device__ __forceinline__ ResItem res_item(const Params& p, uint32_t item, uint
 }
 
 // Buffer resource over `bytes` bytes at `base` (gfx9 raw buffer, no swizzle):
-// a store whose offset is at or past `bytes` is dropped by the hardware.
+// an access whose offset is at or past `bytes` is dropped by the hardware.
 constexpr uint32_t kRawBufferWord3 = 0x00020000u;
 constexpr int kNonTemporal = 2;  // buffer instruction cache policy: streaming (nt)
+constexpr uint32_t kDropped = 0x80000000u;  // an offset past every resource of this kernel
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t out_rsrc(void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(base, 0, bytes, kRawBufferWord3);
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, 0, bytes, kRawBufferWord3);
 }
 
-// 16-byte load at byte `off` of a buffer resource, into registers or, for
-// the whole wavefront, into 64 consecutive 16-byte LDS slots at `dst` (lane i
-// at dst + 16 i).
+// 16-byte streaming load at byte `off` of a buffer resource, into registers
+// or, for the whole wavefront, into 64 consecutive 16-byte LDS slots at `dst`
+// (lane i at dst + 16 i).  (Device functions: called from the kernel's
+// lambdas, the builtins would leave the kernel uninstantiated on the host.)
 __device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal);
 }
@@ -246,86 +260,119 @@ __device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t r, lds_
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, off, 0, 0, kNonTemporal);
 }
 
-// Store of one lane's 8 codes (BITS bytes) at byte `off` of the resource,
-// with the default (write-back) cache policy, which measured faster than
-// streaming stores for these small pieces (the parts of a packed code row are
-// written by different workgroups, so every store covers part of a line).
+// Stores the packed codes of a lane quad's 32 consecutive channels: each lane
+// holds the BITS bytes of its 8 channels in the low bits of `piece`; the
+// quad's first lane gathers the other three (quad_perm broadcasts, executed
+// by every lane) and writes the 4*BITS contiguous bytes at byte `off`.
 template <int BITS>
-__device__ __forceinline__ void store_codes8(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t w) {
+__device__ __forceinline__ void store_quad_codes(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t piece,
+                                                 bool leader) {
+  const uint32_t p1 = (uint32_t)__builtin_amdgcn_mov_dpp((int)piece, 0x55, 0xF, 0xF, false);  // [1,1,1,1]
+  const uint32_t p2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)piece, 0xAA, 0xF, 0xF, false);  // [2,2,2,2]
+  const uint32_t p3 = (uint32_t)__builtin_amdgcn_mov_dpp((int)piece, 0xFF, 0xF, 0xF, false);  // [3,3,3,3]
+  if (!leader) return;
   if constexpr (BITS == 2) {
-    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)w, r, off, 0, 0);
-  } else if constexpr (BITS == 4) {
-    __builtin_amdgcn_raw_buffer_store_b32(w, r, off, 0, 0);
+    const u32x2 w = {piece | (p1 << 16), p2 | (p3 << 16)};
+    __builtin_amdgcn_raw_buffer_store_b64(w, r, off, 0, kNonTemporal);
+  } else if constexpr (BITS == 3) {
+    const u32x3 w = {piece | (p1 << 24), (p1 >> 8) | (p2 << 16), (p2 >> 16) | (p3 << 8)};
+    __builtin_amdgcn_raw_buffer_store_b96(w, r, off, 0, kNonTemporal);
   } else {
-    static_assert(BITS == 3, "bits");
-    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)w, r, off, 0, 0);
-    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(w >> 8), r, off + 1, 0, 0);
-    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(w >> 16), r, off + 2, 0, 0);
+    static_assert(BITS == 4, "bits");
+    const u32x4 w = {piece, p1, p2, p3};
+    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, kNonTemporal);
   }
 }
 
+// Waits for a partner's tagged word of sequence tag `gen` (bounded polls).
+__device__ __forceinline__ uint64_t wait_tagged(uint64_t* w, uint32_t gen, uint32_t& timeouts) {
+  uint64_t v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (uint32_t spin = 0; (uint32_t)(v >> 32) != gen; ++spin) {
+    if (spin == kSpinLimit) {
+      ++timeouts;
+      break;
+    }
+    __builtin_amdgcn_s_sleep(2);
+    v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint64_t tagged(float v, uint32_t gen) {
+  return ((uint64_t)gen << 32) | __float_as_uint(v);
+}
+
 template <int D, int BITS, bool FAKE>
-__global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, uint32_t n_items,
-                                                               uint32_t streams) {
-  constexpr int PARTS = D / kResPart;
+__global__ __launch_bounds__(kPartThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void kivi_part_kernel(const Params p, uint32_t n_items, uint32_t groups, uint32_t parts, uint32_t rows_per_part,
+                      uint64_t* __restrict__ ex) {
   constexpr int LEVELS = (1 << BITS) - 1;
   constexpr int ROW = D * BITS / 8;
-  __shared__ u32x4 rows_lds[kResLdsSlots][kResThreads];
-  __shared__ float part_rng[2][kResWaves][kResPart];
-  __shared__ uint32_t g_meta[kResPart];
-  __shared__ float g_inv[kResPart];
+  constexpr int LR = D / 8;                  // lanes per row (8 channels each)
+  constexpr int RPW = 64 / LR;               // rows per wavefront per slot
+  constexpr int RS = kPartWaves * RPW;       // rows per slot
+  __shared__ u32x4 rows_lds[kPartLdsSlots][kPartThreads];
+  __shared__ float red[2 * D];               // per-channel min | max of the workgroup's rows
+  __shared__ __attribute__((aligned(16))) uint32_t g_meta[D];
+  __shared__ float g_inv[D];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int c = lane % kResLanesPerRow;
-  const int r = lane / kResLanesPerRow;
-  const int row0 = wave * kResRowsPerWave + r;  // row of slot 0 held by this lane
-  // workgroup -> (stream, part); the parts of a stream are 8 workgroups apart
+  const int c = lane % LR;
+  const int rw = lane / LR;
+  // workgroup -> (group, partner); a group's partners are 8 workgroups apart
   const uint32_t bx = blockIdx.x;
-  const int part = (int)((bx / 8u) % PARTS);
-  const uint32_t stream = (bx / (8u * PARTS)) * 8u + bx % 8u;
-  const int ch = part * kResPart + 8 * c;       // first of this lane's 8 channels
+  const uint32_t q = (bx / 8u) % parts;
+  const uint32_t g = (bx / (8u * parts)) * 8u + bx % 8u;
   const int T = p.T;
+  const int t_lo = (int)(q * rows_per_part);
+  const int t_hi = min(t_lo + (int)rows_per_part, T);  // t_hi > t_lo (host)
+  const int ch = 8 * c;
 
-  uint32_t item = stream;
+  if (tid < D) {
+    red[tid] = __builtin_inff();
+    red[D + tid] = -__builtin_inff();
+  }
+  __syncthreads();
+
+  uint32_t item = g;
   ResItem cur = res_item(p, item, n_items);
-  if (!cur.valid) return;
+  if (!cur.valid) return;  // every partner of the group takes the same items
 
-  // Row of a slot for this lane: `rowb` is row0, made opaque to the compiler
-  // once per slice so that the 24 slots' row offsets are formed where they
-  // are used instead of being hoisted out of the slice loop (which keeps them
-  // all live and spills the resident rows).
+  // First slice row of a slot for this lane (relative to t_lo): made opaque
+  // once per slice so that the slots' row offsets are formed where they are
+  // used (hoisted, they would all stay live and spill the resident rows).
+  const int row0 = wave * RPW + rw;
   int rowb = row0;
-  // Loads go through a buffer resource over the slice (wave-uniform), with a
-  // 32-bit per-lane byte offset: rows past T repeat row T-1.
-  auto slice_rsrc = [&](uint32_t s) {
-    return __builtin_amdgcn_make_buffer_rsrc((void*)(p.cache[0] + (size_t)s * T * D), 0,
-                                             (uint32_t)T * D * 2, kRawBufferWord3);
-  };
+  auto slice_rsrc = [&](uint32_t s) { return make_rsrc(p.cache[0] + (size_t)s * T * D, (uint32_t)T * D * 2); };
   auto src_off = [&](int slot) {
-    return (uint32_t)min(slot * kResRowsPerSlot + rowb, T - 1) * (D * 2) + (uint32_t)ch * 2;
+    return (uint32_t)min(t_lo + slot * RS + rowb, t_hi - 1) * (D * 2) + (uint32_t)ch * 2;
   };
   auto load_reg = [&](__amdgpu_buffer_rsrc_t r, int slot) { return buffer_load16(r, src_off(slot)); };
   auto load_lds = [&](__amdgpu_buffer_rsrc_t r, int j) {
     buffer_load16_lds(r, (lds_ptr)&rows_lds[j][wave * 64], src_off(j));
   };
 
-  u32x4 v[kResRegSlots];
+  u32x4 v[kPartRegSlots];
   float mn[8], mx[8];
+  // The odd channels (high halves) enter the range as the raw 32-bit words:
+  // finite BF16 high halves with any low bits order exactly as the BF16
+  // values (ties only between equal high halves), so the minimum and maximum
+  // words carry the exact BF16 extremes, recovered by masking once per slice.
   auto range8 = [&](const u32x4 w) {
-    const float x[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
-                        bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
+    const float x[8] = {bf16_lo(w.x), __uint_as_float(w.x), bf16_lo(w.y), __uint_as_float(w.y),
+                        bf16_lo(w.z), __uint_as_float(w.z), bf16_lo(w.w), __uint_as_float(w.w)};
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       mn[e] = fminf(mn[e], x[e]);
       mx[e] = fmaxf(mx[e], x[e]);
     }
   };
-  // Per-channel range over all T rows of the slice (slot rows past T repeat
-  // row T-1): the register slots (the compiler waits for their loads), then,
-  // after every vector memory operation has completed (the fence keeps the
-  // LDS reads behind the wait), the LDS slots.
+  // Per-channel range over the workgroup's rows (slot rows past t_hi repeat
+  // row t_hi - 1): the register slots (the compiler waits for their loads),
+  // then, after every vector memory operation has completed (the scheduling
+  // barrier keeps the LDS reads behind the wait), the LDS slots.
   auto range_pass = [&]() {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -333,120 +380,140 @@ __global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, u
       mx[e] = -__builtin_inff();
     }
 #pragma unroll
-    for (int k = 0; k < kResRegSlots; ++k) range8(v[k]);
+    for (int k = 0; k < kPartRegSlots; ++k) range8(v[k]);
     __builtin_amdgcn_s_waitcnt(kWaitVmem0);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int j = 0; j < kResLdsSlots; ++j) range8(rows_lds[j][tid]);
+    for (int j = 0; j < kPartLdsSlots; ++j) range8(rows_lds[j][tid]);
   };
 
-  // prologue: the first slice's loads and its range pass
   {
     const __amdgpu_buffer_rsrc_t r = slice_rsrc(cur.s);
 #pragma unroll
-    for (int j = 0; j < kResLdsSlots; ++j) load_lds(r, j);
+    for (int j = 0; j < kPartLdsSlots; ++j) load_lds(r, j);
 #pragma unroll
-    for (int k = 0; k < kResRegSlots; ++k) v[k] = load_reg(r, kResLdsSlots + k);
+    for (int k = 0; k < kPartRegSlots; ++k) v[k] = load_reg(r, kPartLdsSlots + k);
   }
   range_pass();
 
+  uint32_t seq = 0;
   for (;;) {
-    const ResItem nxt = res_item(p, item + streams, n_items);
+    const ResItem nxt = res_item(p, item + groups, n_items);
 
-    // scales: the wavefront's rows by shuffles, the 16 wavefronts through LDS
+    // 1. the workgroup's range: rows of the wavefront by shuffles, the
+    //    wavefronts by LDS atomics
+#pragma unroll
+    for (int e = 1; e < 8; e += 2) {
+      mn[e] = __uint_as_float(__float_as_uint(mn[e]) & 0xFFFF0000u);
+      mx[e] = __uint_as_float(__float_as_uint(mx[e]) & 0xFFFF0000u);
+    }
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
 #pragma unroll
-      for (int off = kResLanesPerRow; off < 64; off *= 2) {
+      for (int off = LR; off < 64; off *= 2) {
         mn[e] = fminf(mn[e], __shfl_xor(mn[e], off));
         mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], off));
       }
     }
-    if (r == 0) {
+    if (rw == 0) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        part_rng[0][wave][8 * c + e] = mn[e];
-        part_rng[1][wave][8 * c + e] = mx[e];
+        atomicMin(&red[ch + e], mn[e]);
+        atomicMax(&red[D + ch + e], mx[e]);
       }
     }
     __syncthreads();
+    // 2. the slice's range from the partners' partial ranges, and its scales
     const size_t slab = (size_t)item;  // [slot][B] with slot = item / B
-    if (tid < kResPart) {
-      float a = part_rng[0][0][tid], b = part_rng[1][0][tid];
-#pragma unroll
-      for (int w = 1; w < kResWaves; ++w) {
-        a = fminf(a, part_rng[0][w][tid]);
-        b = fmaxf(b, part_rng[1][w][tid]);
+    if (tid < D) {
+      float a = red[tid], b = red[D + tid];
+      red[tid] = __builtin_inff();  // reset for the next slice (several barriers away)
+      red[D + tid] = -__builtin_inff();
+      if (parts > 1) {
+        const uint32_t gen = seq + 1;
+        uint64_t* buf = ex + kExHeader + ((size_t)g * 2u + (seq & 1u)) * parts * 2u * D;
+        uint64_t* mine = buf + (size_t)q * 2u * D;
+        __hip_atomic_store(mine + tid, tagged(a, gen), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(mine + D + tid, tagged(b, gen), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        uint32_t timeouts = 0;
+        for (uint32_t r = 0; r < parts; ++r) {
+          if (r == q) continue;
+          uint64_t* theirs = buf + (size_t)r * 2u * D;
+          a = fminf(a, __uint_as_float((uint32_t)wait_tagged(theirs + tid, gen, timeouts)));
+          b = fmaxf(b, __uint_as_float((uint32_t)wait_tagged(theirs + D + tid, gen, timeouts)));
+        }
+        if (timeouts) __hip_atomic_fetch_add(ex, (uint64_t)timeouts, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
-      const GroupScale g = group_scale<LEVELS>(a, b);
-      g_meta[tid] = g.meta;
-      g_inv[tid] = g.inv;
-      if (!FAKE) __builtin_nontemporal_store(g.meta, p.meta[0] + slab * D + part * kResPart + tid);
+      const GroupScale gs = group_scale<LEVELS>(a, b);
+      g_meta[tid] = gs.meta;
+      g_inv[tid] = gs.inv;
+      if (!FAKE && q == 0) __builtin_nontemporal_store(gs.meta, p.meta[0] + slab * D + tid);
     }
     __syncthreads();
-    GroupScale g[8];  // .meta unused below
-    float S[8];
+    ++seq;
+    GroupScale gsc[8];  // .meta unused below; one-pass: .m read in emit
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const uint32_t w = g_meta[8 * c + e];
-      g[e].meta = 0;
-      g[e].m = bf16_as_float(w >> 16);
-      g[e].inv = g_inv[8 * c + e];
-      S[e] = FAKE ? bf16_as_float(w & 0xFFFFu) : 0.0f;
+      gsc[e].meta = 0;
+      gsc[e].m = FAKE ? 0.0f : bf16_as_float(g_meta[ch + e] >> 16);
+      gsc[e].inv = g_inv[ch + e];
     }
 
-    // Codes (or the reconstruction) of the image rows, through buffer
-    // resources over this slice's outputs: a text row, or a slot row past T,
-    // has an offset outside the resource and its store is dropped, so the
-    // code pass has no branches.
+    // 3. codes (or the reconstruction) of the workgroup's image rows through a
+    //    resource over this slice's outputs; a row outside the image span, or
+    //    a slot row past t_hi (the next partner's), gets an offset outside it
     rowb = row0;
     asm volatile("" : "+v"(rowb));
-    // (the resource is wave-uniform, the slice's image rows; the lane's
-    // channels are part of its offset)
     const __amdgpu_buffer_rsrc_t res =
-        FAKE ? out_rsrc(p.out[0] + ((size_t)cur.s * T + p.s0) * D, (uint32_t)p.n * D * 2)
-             : out_rsrc(p.codes[0] + slab * p.n * ROW, (uint32_t)p.n * ROW);
-    // Byte offset of a slot row's piece: rows before the span wrap to huge
-    // offsets and rows at or past its end (slot rows past T included, as
-    // s0 + n <= T) land at or past n rows; both fall outside the resource.
+        FAKE ? make_rsrc(p.out[0] + ((size_t)cur.s * T + p.s0) * D, (uint32_t)p.n * D * 2)
+             : make_rsrc(p.codes[0] + slab * p.n * ROW, (uint32_t)p.n * ROW);
     constexpr uint32_t kStride = FAKE ? D * 2 : ROW;
-    const uint32_t lane_off = (FAKE ? (uint32_t)ch * 2 : (uint32_t)(ch / 8) * BITS) - (uint32_t)p.s0 * kStride;
+    const uint32_t lane_off = FAKE ? (uint32_t)ch * 2 : (uint32_t)c * BITS;
+    const bool leader = (c & 3) == 0;
     auto emit = [&](u32x4 w, int slot) {
       asm volatile("" : "+v"(w));  // convert here, not reuse the range pass's values
-      const uint32_t off = (uint32_t)(slot * kResRowsPerSlot + rowb) * kStride + lane_off;
+      const int r = t_lo + slot * RS + rowb;
+      const uint32_t off = r < t_hi ? (uint32_t)(r - p.s0) * kStride + lane_off : kDropped;
       const float x[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
                           bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
-      uint32_t cb[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) cb[e] = code_bits(x[e], g[e]);
       if constexpr (FAKE) {
+        // the metadata words (min and scale) are read back from LDS here
+        // (held in registers with the rest, they would spill)
+        const u32x4 m0 = *(const u32x4*)&g_meta[ch], m1 = *(const u32x4*)&g_meta[ch + 4];
+        const uint32_t mw[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
         float y[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf((float)(cb[e] - kMagicBits), S[e], g[e].m);
+        for (int e = 0; e < 8; ++e) {
+          GroupScale ge;
+          ge.m = bf16_as_float(mw[e] >> 16);
+          ge.inv = gsc[e].inv;
+          y[e] = __builtin_fmaf(__builtin_rintf(code_scaled(x[e], ge)), bf16_as_float(mw[e] & 0xFFFFu), ge.m);
+        }
         const u32x4 o = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
                          pack_bf16x2_hw(y[6], y[7])};
         __builtin_amdgcn_raw_buffer_store_b128(o, res, off, 0, kNonTemporal);
       } else {
-        store_codes8<BITS>(res, off, pack_code_bits<8, BITS>(cb).w[0]);
+        uint32_t cb[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cb[e] = code_bits(x[e], gsc[e]);
+        store_quad_codes<BITS>(res, off, pack_code_bits<8, BITS>(cb).w[0], leader);
       }
     };
     // The register slots come first, each refilled as soon as it is coded
-    // (scheduling barriers keep each refill after the slot's use: hoisted
-    // refills would need a second copy of the rows), so the next slice's
-    // loads start at once.  The LDS slots are then all read before any of
-    // them is refilled: the compiler cannot tell the slots apart, and an LDS
-    // read issued after a pending direct-to-LDS load makes it wait for that
-    // load.
+    // (scheduling barriers keep each refill after the slot's use), so the
+    // next slice's loads start at once.  The LDS slots are then all read
+    // before any of them is refilled: an LDS read issued after a pending
+    // direct-to-LDS load would wait for that load.
     auto code_pass = [&](bool refill) {
       const __amdgpu_buffer_rsrc_t r = slice_rsrc(nxt.s);
 #pragma unroll
-      for (int k = 0; k < kResRegSlots; ++k) {
-        emit(v[k], kResLdsSlots + k);
+      for (int k = 0; k < kPartRegSlots; ++k) {
+        emit(v[k], kPartLdsSlots + k);
         __builtin_amdgcn_sched_barrier(0);
-        if (refill) v[k] = load_reg(r, kResLdsSlots + k);
+        if (refill) v[k] = load_reg(r, kPartLdsSlots + k);
       }
 #pragma unroll
-      for (int j = 0; j < kResLdsSlots; ++j) {
+      for (int j = 0; j < kPartLdsSlots; ++j) {
         emit(rows_lds[j][tid], j);
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -454,7 +521,7 @@ __global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, u
         __builtin_amdgcn_s_waitcnt(kWaitLds0);  // every slot read before it is refilled
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int j = 0; j < kResLdsSlots; ++j) load_lds(r, j);
+        for (int j = 0; j < kPartLdsSlots; ++j) load_lds(r, j);
       }
     };
     if (!nxt.valid) {
@@ -464,33 +531,95 @@ __global__ __launch_bounds__(kResThreads) void kivi_res_kernel(const Params p, u
     code_pass(true);
     range_pass();
     cur = nxt;
-    item += streams;
+    item += groups;
   }
 }
 
-template <int D, int BITS>
-static hipError_t launch_k(const Params& p, bool fake, hipStream_t stream) {
-  int dev = 0, cus = 0;
+// Zeroes the exchange words a launch uses (a kernel rather than a memset, so
+// the call can be captured in a graph).
+__global__ void zero_words_kernel(uint64_t* w, uint32_t n) {
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) w[i] = 0;
+}
+
+// ---------------------------------------------------------------- host side
+
+int kivi_part_capacity(int D) { return kPartSlots * kPartWaves * (512 / D); }
+
+int kivi_partners(int T, int D) {
+  const int cap = kivi_part_capacity(D);
+  const int parts = (T + cap - 1) / cap;
+  if (parts > kMaxPartners || (uint64_t)T * D * 2 >= (1ull << 31)) return 0;  // two-pass kernel
+  return parts;
+}
+
+uint64_t kivi_workspace_bytes(int T, int D) {
+  return kivi_partners(T, D) > 1 ? ((uint64_t)kExHeader + (uint64_t)kExMaxWgs * 2 * 2 * D) * 8 : 0;
+}
+
+// Compute units the persistent grids are sized for: the device's, or fewer
+// with HG_TEST_CUS=n in the environment (a test hook: results must not
+// depend on the grid).
+static hipError_t grid_cus(int* cus) {
+  int dev = 0;
   hipError_t e = hipGetDevice(&dev);
-  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
-  const uint32_t slices = (uint32_t)p.L * p.B * p.H;
-  if (p.T <= kResRows) {
-    // one workgroup per compute unit, in whole groups of 8 * PARTS (a stream's parts 8 apart)
-    constexpr uint32_t PARTS = D / kResPart;
-    const uint32_t unit = 8u * PARTS;
-    const uint32_t n_items = (uint32_t)p.n_unprot_k * (uint32_t)p.B;
-    const uint32_t want = (n_items + 7u) / 8u * unit;  // no more streams than items (rounded up)
-    const uint32_t blocks = std::max(unit, std::min((uint32_t)std::max(cus, 1) / unit * unit, want));
-    const uint32_t streams = blocks / PARTS;
-    if (fake)
-      hipLaunchKernelGGL((kivi_res_kernel<D, BITS, true>), dim3(blocks), dim3(kResThreads), 0, stream, p,
-                         n_items, streams);
-    else
-      hipLaunchKernelGGL((kivi_res_kernel<D, BITS, false>), dim3(blocks), dim3(kResThreads), 0, stream, p,
-                         n_items, streams);
-    return hipGetLastError();
+  const char* s = getenv("HG_TEST_CUS");
+  if (s && *s) *cus = std::max(1, std::min(*cus, atoi(s)));
+  return hipSuccess;
+}
+
+template <int D, int BITS, bool FAKE>
+static hipError_t launch_part(const Params& p, int parts, uint64_t* ex, int cus, bool* launched,
+                              hipStream_t stream) {
+  *launched = false;
+  int per_cu = 0;
+  hipError_t e =
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kivi_part_kernel<D, BITS, FAKE>, kPartThreads, 0);
+  if (e != hipSuccess) return e;
+  const uint32_t n_items = (uint32_t)p.n_unprot_k * (uint32_t)p.B;
+  if (n_items == 0) {  // every key head kept in BF16: nothing to quantize here
+    *launched = true;
+    return hipSuccess;
   }
+  const uint32_t resident = (uint32_t)std::max(per_cu, 0) * (uint32_t)cus;  // workgroups held at once
+  uint32_t cap = resident / (uint32_t)parts;
+  if (parts > 1) cap = std::min(cap, (uint32_t)(kExMaxWgs / parts));
+  cap = cap / 8u * 8u;
+  if (cap == 0) return hipSuccess;  // too few resident workgroups: the two-pass kernel instead
+  const uint32_t groups = std::min((n_items + 7u) / 8u * 8u, cap);
+  const uint32_t rows_per_part = (uint32_t)((p.T + parts - 1) / parts);
+  if (parts > 1) {
+    const uint32_t words = (uint32_t)(kExHeader + (uint64_t)groups * 2 * parts * 2 * D);
+    hipLaunchKernelGGL(zero_words_kernel, dim3(std::min<uint32_t>((words + 255) / 256, 1024)), dim3(256), 0,
+                       stream, ex, words);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((kivi_part_kernel<D, BITS, FAKE>), dim3(groups * (uint32_t)parts), dim3(kPartThreads), 0,
+                     stream, p, n_items, groups, (uint32_t)parts, rows_per_part, ex);
+  *launched = true;
+  return hipGetLastError();
+}
+
+template <int D, int BITS>
+static hipError_t launch_k(const Params& p, bool fake, void* ws, hipStream_t stream) {
+  int cus = 0;
+  hipError_t e = grid_cus(&cus);
+  if (e != hipSuccess) return e;
+  const int parts = kivi_partners(p.T, D);
+  if (parts > 0 && (parts == 1 || ws)) {
+    bool launched = false;
+    e = fake ? launch_part<D, BITS, true>(p, parts, (uint64_t*)ws, cus, &launched, stream)
+             : launch_part<D, BITS, false>(p, parts, (uint64_t*)ws, cus, &launched, stream);
+    if (e != hipSuccess || launched) return e;
+  }
+  if (ws) {  // the two-pass kernel waits for nothing: the workspace's count of timed-out waits is 0
+    hipLaunchKernelGGL(zero_words_kernel, dim3(1), dim3(64), 0, stream, (uint64_t*)ws, (uint32_t)kExHeader);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const uint32_t slices = (uint32_t)p.L * p.B * p.H;
   const uint32_t blocks = std::min<uint32_t>(slices, (uint32_t)std::max(cus, 1) * kSeqBlocksPerCU);
   if (fake)
     hipLaunchKernelGGL((kivi_seq_kernel<D, BITS, true>), dim3(blocks), dim3(kSeqThreads), 0, stream, p);
@@ -500,20 +629,20 @@ static hipError_t launch_k(const Params& p, bool fake, hipStream_t stream) {
 }
 
 template <int D>
-static hipError_t launch_k_bits(const Params& p, int bits, bool fake, hipStream_t stream) {
+static hipError_t launch_k_bits(const Params& p, int bits, bool fake, void* ws, hipStream_t stream) {
   switch (bits) {
-    case 2: return launch_k<D, 2>(p, fake, stream);
-    case 3: return launch_k<D, 3>(p, fake, stream);
-    case 4: return launch_k<D, 4>(p, fake, stream);
+    case 2: return launch_k<D, 2>(p, fake, ws, stream);
+    case 3: return launch_k<D, 3>(p, fake, ws, stream);
+    case 4: return launch_k<D, 4>(p, fake, ws, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, hipStream_t stream) {
+hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, void* ws, hipStream_t stream) {
   switch (D) {
-    case 64: return launch_k_bits<64>(p, bits, fake, stream);
-    case 128: return launch_k_bits<128>(p, bits, fake, stream);
-    case 256: return launch_k_bits<256>(p, bits, fake, stream);
+    case 64: return launch_k_bits<64>(p, bits, fake, ws, stream);
+    case 128: return launch_k_bits<128>(p, bits, fake, ws, stream);
+    case 256: return launch_k_bits<256>(p, bits, fake, ws, stream);
     default: return hipErrorInvalidValue;
   }
 }

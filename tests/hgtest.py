@@ -30,7 +30,7 @@ def alloc_with_canary(sizes, device="cuda"):
     """Packed buffers with PAD canary bytes after each; returns (views, raw)."""
     import paper_2609_35800_amd as hg
     views, raw = {}, {}
-    for n in hg.BUFFERS:
+    for n in hg.PACKED:
         t = torch.full((sizes[n] + PAD,), CANARY, dtype=torch.uint8, device=device)
         raw[n] = t
         views[n] = t[: sizes[n]]
@@ -57,7 +57,16 @@ def gpu_run(w: synthkv.Workload, K: torch.Tensor, V: torch.Tensor, mask: np.ndar
     hg.hg_dequantize(cfg, mask, packed, Ko, Vo, stream=stream)
     torch.cuda.synchronize()
     out = {n: packed[n].cpu().numpy() for n in hg.BUFFERS}
+    out["_exchange_timeouts"] = exchange_timeouts(packed.get("workspace"))
     return out, synthkv.bf16_bits(Ko), synthkv.bf16_bits(Vo), canaries_intact(raw)
+
+
+def exchange_timeouts(ws) -> int:
+    """Waits that ran out of polls, counted in a KIVI exchange workspace's
+    first 8 bytes (0 when the call used no workspace)."""
+    if ws is None or ws.numel() < 8:
+        return 0
+    return int(ws[:8].cpu().numpy().view(np.uint64)[0])
 
 
 def oracle_run(w: synthkv.Workload, Kb: np.ndarray, Vb: np.ndarray, mask: np.ndarray,
@@ -76,7 +85,7 @@ def compare_full(w, K, V, mask, stream=None):
     Kb, Vb = synthkv.bf16_bits(K), synthkv.bf16_bits(V)
     g_pk, g_K, g_V, canary_ok = gpu_run(w, K, V, mask, stream=stream)
     o_pk, o_K, o_V = oracle_run(w, Kb, Vb, mask)
-    rep = {"canaries": canary_ok}
+    rep = {"canaries": canary_ok, "exchange_timeouts": g_pk.pop("_exchange_timeouts")}
     for n in o_pk:
         assert g_pk[n].size == o_pk[n].size, n
         rep[n + "_mismatch"] = int(np.count_nonzero(g_pk[n] != o_pk[n]))

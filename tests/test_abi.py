@@ -69,15 +69,48 @@ def test_sizes_match_oracle(seed):
              base=int(rng.integers(0, 3)), keys_only=int(rng.integers(0, 2)))
     if f["base"] == 2:
         f["retain_permille"] = int(rng.choice([0, 20, 100, 1000]))
+    if f["base"] == 1:
+        f["kivi_group"] = int(rng.choice([32, 0]))
+        f["T"] = T = int(rng.choice([T, 769, 3008, 6144]))  # one or several workgroups per slice
+        f["img_len"] = min(f["img_len"], T - f["img_start"])
     mask = (rng.random(L * H) < 0.2).astype(np.uint8)
     got = hg.hg_packed_sizes(hg.make_config(**f), mask)
     want = oracle.sizes(oracle.make_config(**f), mask)
     assert {n: got[n] for n in want} == want
+    assert got["workspace"] == kivi_exchange_bytes(f, want)
     # the one-pass call's workspace: norms, lists and both tensors' saved rows,
-    # each part rounded up to 256 bytes; none without retention
+    # each part rounded up to 256 bytes, with retention; else the exchange area
     up = lambda b: -(-b // 256) * 256  # noqa: E731
     parts = ("norm_k", "ret_idx", "ret_k", "ret_v")
-    assert got["fake_workspace"] == (sum(up(want[n]) for n in parts) if want["retain_count"] else 0)
+    assert got["fake_workspace"] == (sum(up(want[n]) for n in parts) if want["retain_count"]
+                                     else got["workspace"])
+
+
+def kivi_exchange_bytes(f, sizes):
+    """Closed form of hg_quantize's workspace: KIVI keys over the whole
+    sequence, some key slice quantized, and a slice longer than one
+    workgroup's 24 slots of 16 * 512/D rows (at most 8 workgroups per slice):
+    a 64-word header plus 1024 workgroups x 2 buffers x 2D tagged words."""
+    if f["base"] != 1 or f["kivi_group"] != 0 or f["img_len"] == 0 or sizes["n_unprot_k"] == 0:
+        return 0
+    cap = 24 * 8192 // f["D"]
+    parts = -(-f["T"] // cap)
+    if parts < 2 or parts > 8:
+        return 0
+    return (64 + 1024 * 2 * 2 * f["D"]) * 8
+
+
+def test_workspace_of_whole_sequence_kivi_keys():
+    mask = np.zeros(8, np.uint8)
+    ws = lambda D: (64 + 4096 * D) * 8  # noqa: E731
+    for T, D, want in ((3008, 128, ws(128)), (1536, 128, 0), (1537, 128, ws(128)), (12288, 128, ws(128)),
+                       (12289, 128, 0), (3008, 64, 0), (3073, 64, ws(64)), (3008, 256, ws(256)),
+                       (6144, 256, ws(256)), (6145, 256, 0)):
+        f = _cfg(base=1, kivi_group=0, T=T, D=D, img_start=0, img_len=T)
+        got = hg.hg_packed_sizes(hg.make_config(**f), mask)
+        assert got["workspace"] == want == got["fake_workspace"], (T, D, got["workspace"], want)
+    f = _cfg(base=1, kivi_group=0, T=3008, img_start=0, img_len=3008)
+    assert hg.hg_packed_sizes(hg.make_config(**f), np.ones(8, np.uint8))["workspace"] == 0  # no key quantized
 
 
 def test_storage_model_bits_per_element():

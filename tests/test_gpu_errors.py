@@ -25,7 +25,7 @@ def _setup(w):
     cfg = hg.make_config(**w.config_fields())
     K, V = synthkv.gen_kv(w, device="cuda")
     packed = {n: torch.full((sz,), FILL, dtype=torch.uint8, device="cuda")
-              for n, sz in hg.hg_packed_sizes(cfg, mask).items() if n in hg.BUFFERS}
+              for n, sz in hg.hg_packed_sizes(cfg, mask).items() if n in hg.PACKED}
     Ko = torch.full(K.shape, 0x7FBF, dtype=torch.int16, device="cuda").view(torch.bfloat16)
     Vo = Ko.clone()
     return hg, mask, cfg, K, V, packed, Ko, Vo

@@ -9,7 +9,7 @@ import torch
 
 import oracle
 import synthkv
-from hgtest import bf16_ulp_diff
+from hgtest import bf16_ulp_diff, exchange_timeouts
 from test_gpu_parity import _special_values, small
 
 pytestmark = pytest.mark.gpu
@@ -37,6 +37,8 @@ def run_fake(w, K, V, mask, inplace):
         Vo = torch.full(Vg.shape, SENTINEL, dtype=torch.int16, device="cuda").view(torch.bfloat16)
         hg.hg_fake_quantize(cfg, Kg, Vg, mask, Ko, Vo, ws)
     torch.cuda.synchronize()
+    if w.base == "kivi" and w.kivi_group == 0:
+        assert exchange_timeouts(ws) == 0, "exchange waits ran out of polls"
     return synthkv.bf16_bits(Ko), synthkv.bf16_bits(Vo)
 
 

@@ -4,11 +4,14 @@ against the oracle: codes, metadata, side store and reconstruction
 bit-exact for quantize / dequantize and for the one-pass simulated
 quantization; every slice of the full LLaVA-NeXT-7B-shaped cache.
 
-Slices of up to 3072 rows go through the resident kernel (each workgroup
-holds a 64-channel part of a slice on chip and refills its row slots with
-its next slice while coding); longer slices through the two-pass kernel.
-Both are covered, including several slices per workgroup stream and the
-boundary at 3072 / 3073 rows."""
+Slices of up to 8 workgroups' capacity (24 slots of 8192/D rows: 3072,
+1536 and 768 rows at head_dim 64, 128 and 256) go through the partitioned
+resident kernel: P workgroups each hold a run of a slice's rows on chip and
+combine their partial ranges through the call's workspace; longer slices go
+through the two-pass kernel.  Covered: one to eight workgroups per slice and
+the capacity boundaries, several slices per group (with the grid shrunk
+through the HG_TEST_CUS hook), identical bytes for different grid sizes, and
+no exchange wait running out of polls."""
 import numpy as np
 import pytest
 import torch
@@ -60,49 +63,77 @@ def test_full_size_llava_one_pass(inplace):
     wholecache.assert_whole(wholecache.fake_quantize(w, inplace=inplace), w)
 
 
-# Enough (head, row) items that every workgroup stream of the resident kernel
-# takes several slices (streams: 256 / 128 / 64 at head_dim 64 / 128 / 256),
-# so each slot's refill with the next slice is exercised.
-STREAM_CASES = [small("kivi", D, bits, ko, img_len=150, img_start=20, text=30, L=2, B=20, H=8,
-                      n_protected=2).with_(kivi_group=0, name=f"kiviseq-streams-D{D}-b{bits}-ko{ko}")
-                for D in (64, 128, 256) for bits in (2, 3) for ko in (0, 1)]
+def capacity(D):
+    """Rows one workgroup of the partitioned kernel holds."""
+    return 24 * 8192 // D
+
+
+# Enough (head, row) items that every group takes several slices once the
+# grid is shrunk to 32 compute units' worth (32 workgroups: 32, 16 and 8
+# groups of 1, 2 and 4 workgroups), so each slot's refill with the next
+# slice and the alternation of the exchange buffers are exercised.
+STREAM_CASES = [small("kivi", D, bits, ko, img_len=T - 50, img_start=20, text=30, L=2, B=6, H=8,
+                      n_protected=2).with_(kivi_group=0, name=f"kiviseq-streams-D{D}-T{T}-b{bits}-ko{ko}")
+                for D in (64, 128, 256) for T in (200, capacity(D) + 300, 3 * capacity(D) + 7)
+                for bits in (2, 3) for ko in (0, 1)]
 
 
 @pytest.mark.parametrize("w", STREAM_CASES, ids=lambda w: w.name)
-def test_resident_streams(w):
+def test_resident_streams(w, monkeypatch):
+    monkeypatch.setenv("HG_TEST_CUS", "32")
     K, V = synthkv.gen_kv(w)
     _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), w.name)
 
 
-@pytest.mark.parametrize("w", STREAM_CASES[2:4], ids=lambda w: w.name)
+@pytest.mark.parametrize("w", STREAM_CASES[2:4] + STREAM_CASES[8:10], ids=lambda w: w.name)
 @pytest.mark.parametrize("inplace", [False, True])
-def test_resident_streams_fake(w, inplace):
+def test_resident_streams_fake(w, inplace, monkeypatch):
+    monkeypatch.setenv("HG_TEST_CUS", "32")
     K, V = synthkv.gen_kv(w)
     check_fake(w, K, V, synthkv.protect_mask(w), inplace)
 
 
-# Slices at the resident capacity (3072 rows: every row slot filled), one row
-# past it (the two-pass kernel), and longer; image spans at the start, in the
-# middle and at the end of the slice.
-BOUNDARY = [(3072, 3000, 40), (3073, 3000, 40), (3072, 3072, 0), (3072, 100, 2972),
-            (3200, 3100, 0), (4000, 1000, 1500)]
+@pytest.mark.parametrize("cus", ["", "256", "64", "24", "16", "8", "1"])
+def test_grid_size_does_not_change_the_bytes(cus, monkeypatch):
+    """The same cache (two workgroups per slice) under persistent grids sized
+    for 256 down to 1 compute units (fewer than 16 are too few workgroups for
+    a multiple of 8 groups: the two-pass kernel takes over), and once more with
+    the full grid: every run equals the oracle."""
+    w = small("kivi", 128, 2, 0, img_len=3000, img_start=5, text=3, L=2, B=6, H=5,
+              n_protected=2).with_(kivi_group=0)
+    monkeypatch.setenv("HG_TEST_CUS", cus)
+    K, V = synthkv.gen_kv(w)
+    _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), f"cus{cus or 'all'}")
 
 
-@pytest.mark.parametrize("D", [128, 256])
-@pytest.mark.parametrize("T,img_len,img_start", BOUNDARY, ids=lambda v: str(v))
+# Slices at each workgroup count's capacity and one row past it (one to eight
+# workgroups per slice; past eight, the two-pass kernel), spans at the
+# start, in the middle and at the end of the slice.
+def _boundary_cases():
+    out = []
+    for D in (64, 128, 256):
+        c = capacity(D)
+        for T in (c, c + 1, 2 * c + 1, 3 * c - 5, 8 * c, 8 * c + 1):
+            for img_start, img_len in ((0, T), (T // 3, T // 2), (T - 40, 40)):
+                out.append((D, T, img_len, img_start))
+    return out
+
+
+@pytest.mark.parametrize("D,T,img_len,img_start", _boundary_cases(), ids=lambda v: str(v))
 def test_capacity_boundary(D, T, img_len, img_start):
     w = small("kivi", D, 3, 0, img_len=img_len, img_start=img_start, text=T - img_len - img_start,
               L=1, B=2, H=2, n_protected=1).with_(kivi_group=0)
     assert w.T == T
     K, V = synthkv.gen_kv(w)
     K[0, :, :, T - 1, 5] = -4000.0  # an extreme in the last row of every slice
-    _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), f"T{T}-n{img_len}-s{img_start}")
+    K[0, :, :, 0, 9] = 5000.0       # and in the first
+    _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), f"D{D}-T{T}-n{img_len}-s{img_start}")
 
 
-@pytest.mark.parametrize("T,img_len,img_start", BOUNDARY[:2], ids=lambda v: str(v))
+@pytest.mark.parametrize("T", [1536, 1537, 3008, 12288, 12289])
 @pytest.mark.parametrize("inplace", [False, True])
-def test_capacity_boundary_fake(T, img_len, img_start, inplace):
-    w = small("kivi", 128, 2, 1, img_len=img_len, img_start=img_start, text=T - img_len - img_start,
+def test_capacity_boundary_fake(T, inplace):
+    w = small("kivi", 128, 2, 1, img_len=T - 60, img_start=20, text=40,
               L=1, B=2, H=2, n_protected=1).with_(kivi_group=0)
     K, V = synthkv.gen_kv(w)
     check_fake(w, K, V, synthkv.protect_mask(w), inplace)

@@ -21,6 +21,7 @@ pytestmark = pytest.mark.gpu
 def _assert_exact(rep, tag):
     bad = {k: v for k, v in rep.items() if k.endswith("_mismatch") and v}
     assert rep["canaries"], f"{tag}: canary bytes overwritten"
+    assert rep.get("exchange_timeouts", 0) == 0, f"{tag}: exchange waits ran out of polls"
     assert not bad, f"{tag}: packed mismatches {bad}"
     assert rep["K_ulp"] <= 1 and rep["V_ulp"] <= 1, f"{tag}: dequant ulp {rep}"
     # the reconstruction rule is exact on both sides: report any ulp drift

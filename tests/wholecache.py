@@ -26,7 +26,7 @@ import torch
 
 import oracle
 import synthkv
-from hgtest import PAD, alloc_with_canary, canaries_intact
+from hgtest import PAD, alloc_with_canary, canaries_intact, exchange_timeouts
 
 SENTINEL = 0x7FBF
 # oracle threads: the host's cores, at most 16 (a GPU machine's CPU share)
@@ -155,6 +155,8 @@ def quantize_dequantize(w: synthkv.Workload, mask=None) -> Report:
         check_layer(w, ocfg, rows[l], gpu, obytes, g_rec, (oK[0], oV[0]), rep, l, packed=True)
         rep.layers += 1
     rep.canaries = canaries_intact(raw)
+    if exchange_timeouts(packed.get("workspace")):
+        rep.failures.append("KIVI exchange waits ran out of polls")
     del K, V, Ko, Vo, packed, raw
     torch.cuda.empty_cache()
     return rep
@@ -178,9 +180,12 @@ def fake_quantize(w: synthkv.Workload, inplace: bool, mask=None) -> Report:
         Vo = torch.full(V.shape, SENTINEL, dtype=torch.int16, device="cuda").view(torch.bfloat16)
     hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo, ws)
     torch.cuda.synchronize()
+    rep_timeouts = exchange_timeouts(ws) if (w.base == "kivi" and w.kivi_group == 0) else 0
     del ws
     chans = synthkv.outlier_channels(w)
     rep = Report(expected=2 * w.L * w.B * w.H)
+    if rep_timeouts:
+        rep.failures.append("KIVI exchange waits ran out of polls")
     for l in range(w.L):
         if inplace:
             Kb = synthkv.bf16_bits(synthkv.gen_layer(w, 0, l, "cuda", chans))[None]
