@@ -28,6 +28,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 QUANT_KERNEL = "quantize_kernel"
+DEQUANT_KERNEL = "dequantize_kernel"
 FAKE_KERNEL = "fake_quantize_kernel"
 _CSRC = "paper_2609_35800_amd/csrc/"
 # the device sources that decide what each timed call reads and writes; a
@@ -35,9 +36,15 @@ _CSRC = "paper_2609_35800_amd/csrc/"
 KERNEL_SOURCES = {
     QUANT_KERNEL: tuple(_CSRC + f for f in ("quantize.hip", "kivi_seq.hip", "retain.hip",
                                               "hg_device.h", "hg_kernels.h")),
+    DEQUANT_KERNEL: tuple(_CSRC + f for f in ("dequantize.hip", "retain.hip", "hg_device.h", "hg_kernels.h")),
     FAKE_KERNEL: tuple(_CSRC + f for f in ("fakequant.hip", "kivi_seq.hip", "retain.hip",
                                              "hg_device.h", "hg_kernels.h")),
 }
+# The table of the benchmark's measured results: the five workloads, the 72B-shaped
+# one at each bit width (name, bits).
+TABLE_WORKLOADS = (("tiny", None), ("qwen2.5-vl-7b", None), ("llava-next-7b", None), ("internvl-8b", None),
+                   ("72b-long", 2), ("72b-long", 3), ("72b-long", 4))
+BASELINE_TABLE_HEADER = "## 4. Measured results"
 
 
 def parse():
@@ -59,6 +66,11 @@ def parse():
                          "that scales the counters now always runs")
     ap.add_argument("--quant-only", action="store_true",
                     help="time only the quantize launches (for profiling that kernel)")
+    ap.add_argument("--table", metavar="JSON",
+                    help="measure every workload of BASELINE.md's results table (quantize and "
+                         "dequantize median times, oracle on the host cores) into JSON")
+    ap.add_argument("--fill-baseline", metavar="JSON",
+                    help="(no GPU) write the rows of a --table run into BASELINE.md's section 4")
     ap.add_argument("--op", default="step", choices=["step", "fakequant"],
                     help="step: quantize+pack then dequantize (the default line); "
                          "fakequant: the one-pass simulated quantization alone")
@@ -110,10 +122,9 @@ def variant_name(w) -> str:
     return f"{name}_b{w.bits}"
 
 
-def traffic_from_profile(w, kernel: str = QUANT_KERNEL):
-    """HBM bytes per call (all kernels of the timed call) measured by the
-    rocprofv3 FETCH_SIZE and WRITE_SIZE counters, if a committed measurement
-    of this workload variant exists and was taken on the current sources."""
+def traffic_record(w, kernel: str = QUANT_KERNEL):
+    """The committed rocprofv3 FETCH_SIZE / WRITE_SIZE record of this workload
+    variant's call, if one exists and was taken on the current sources."""
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{variant_name(w)}.json")
     if not os.path.exists(path):
         return None
@@ -121,7 +132,15 @@ def traffic_from_profile(w, kernel: str = QUANT_KERNEL):
         rec = json.load(f)
     if rec.get("kernel_source_hash") != kernel_source_hash(kernel):
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec
+
+
+def traffic_from_profile(w, kernel: str = QUANT_KERNEL):
+    """HBM bytes per call (all kernels of the timed call) measured by the
+    rocprofv3 FETCH_SIZE and WRITE_SIZE counters, if a committed measurement
+    of this workload variant exists and was taken on the current sources."""
+    rec = traffic_record(w, kernel)
+    return rec.get("hbm_bytes_per_launch") if rec else None
 
 
 def algorithmic_bytes(w, sizes) -> dict:
@@ -295,13 +314,112 @@ def bench_fakequant(args, hg, w, cfg, mask, K, V):
     }), flush=True)
 
 
+def measure_table(args) -> None:
+    """The benchmark's measured-results table: for each workload, the median
+    quantize and dequantize call times over `steps` calls (HIP events on the
+    launch stream, inputs resident in HBM), the GB/s and image tokens/s they
+    give, the committed counter ratios, and the oracle on the host cores
+    (one thread and all of them, quantize + dequantize)."""
+    import torch
+    import paper_2609_35800_amd as hg
+    import synthkv
+    stream = torch.cuda.current_stream()
+    rows = []
+    for name, bits in TABLE_WORKLOADS:
+        w = synthkv.WORKLOADS[name]
+        if bits is not None:
+            w = w.with_(bits=bits)
+        mask = synthkv.protect_mask(w)
+        cfg = hg.make_config(**w.config_fields())
+        sizes = hg.hg_packed_sizes(cfg, mask)
+        ab = algorithmic_bytes(w, sizes)
+        K, V = synthkv.gen_kv(w, device="cuda")
+        packed = hg.alloc_packed(cfg, mask)
+        Ko, Vo = torch.empty_like(K), torch.empty_like(V)
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+        for _ in range(args.warmup):
+            hg.hg_quantize(cfg, K, V, mask, packed, stream=stream)
+            hg.hg_dequantize(cfg, mask, packed, Ko, Vo, stream=stream)
+        for e0, e1, e2 in ev:
+            e0.record(stream)
+            hg.hg_quantize(cfg, K, V, mask, packed, stream=stream)
+            e1.record(stream)
+            hg.hg_dequantize(cfg, mask, packed, Ko, Vo, stream=stream)
+            e2.record(stream)
+        torch.cuda.synchronize()
+        q_ms = float(np.median([a.elapsed_time(b) for a, b, _ in ev]))
+        d_ms = float(np.median([b.elapsed_time(c) for _, b, c in ev]))
+        cb_n = cpu_baseline(w, K, V, mask, args.cpu_seconds / 2)
+        cb_1 = cpu_baseline(w, K, V, mask, args.cpu_seconds / 4, threads=1)
+        label = w.name + (f", {w.bits}-bit" if bits is not None else "")
+        for call, ms, nbytes, kernel in (("hg_quantize", q_ms, ab["quant"], QUANT_KERNEL),
+                                         ("hg_dequantize", d_ms, ab["dequant"], DEQUANT_KERNEL)):
+            rec = traffic_record(w, kernel)
+            rows.append({
+                "config": label, "workload": w.name, "bits": w.bits, "call": call,
+                "median_ms": round(ms, 4), "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                "pct_of_peak": round(100 * nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 1),
+                "bytes": nbytes, "traffic_ratio": rec.get("ratio_to_algorithmic") if rec else None,
+                "image_tokens_per_s": round(w.B * w.img_len / (ms * 1e-3), 1),
+                "oracle_1_thread_GBps": cb_1["value"], "oracle_n_thread_GBps": cb_n["value"],
+                "oracle_threads": cb_n["cores"], "oracle_sample": cb_n["sample"],
+                "parity_test": (f"tests/test_gpu_workloads.py::test_72b_long_bit_sweep[{w.bits}]"
+                                if name == "72b-long" else f"tests/test_gpu_workloads.py::test_workload[{name}]"),
+            })
+        print(json.dumps(rows[-2]), flush=True)
+        del K, V, Ko, Vo, packed
+        torch.cuda.empty_cache()
+    out = {"rows": rows, "steps": args.steps, "warmup": args.warmup, "cpu_model": cpu_model(),
+           "host_cores": os.cpu_count(), "date": time.strftime("%Y-%m-%d")}
+    with open(args.table, "w") as f:
+        json.dump(out, f, indent=1)
+
+
+def fill_baseline(path: str) -> None:
+    """Writes the rows of a --table run as the table of the benchmark's section
+    4 (everything from its header to the next section is replaced)."""
+    with open(path) as f:
+        t = json.load(f)
+    fmt = lambda v, spec: "—" if v is None else format(v, spec)  # noqa: E731
+    lines = [BASELINE_TABLE_HEADER, "",
+             f"Written by `python bench.py --fill-baseline` from a `python bench.py --table` run on one MI355X "
+             f"({t['date']}; median of {t['steps']} calls after {t['warmup']} warm-up steps, HIP events on the "
+             "launch stream, inputs resident in HBM; bytes are the algorithmic bytes of `bench.py`). Counter "
+             "ratios come from the committed rocprofv3 records under `profiles/` when they were taken on the "
+             "current kernel sources. The oracle columns time the CPU oracle (quantize + dequantize, same "
+             f"byte count) on the box's host ({t['cpu_model']}): one thread, and one per core "
+             f"(N = {t['rows'][0]['oracle_threads']}). Parity: every slice compared with the oracle, bit for "
+             "bit, by the GPU test named.", "",
+             "| Config | Call | Median time | GB/s | % of 8 TB/s | rocprof bytes ÷ algorithmic bytes | "
+             "Image tokens/s | Oracle 1-thread | Oracle N-thread | Parity |",
+             "|---|---|---|---|---|---|---|---|---|---|"]
+    for r in t["rows"]:
+        lines.append(f"| {r['config']} | `{r['call']}` | {r['median_ms'] * 1e3:.1f} µs | {r['GBps']:,.0f} | "
+                     f"{r['pct_of_peak']:.1f} | {fmt(r['traffic_ratio'], '.4f')} | "
+                     f"{r['image_tokens_per_s']:.3g} | {r['oracle_1_thread_GBps']:.3f} GB/s | "
+                     f"{r['oracle_n_thread_GBps']:.2f} GB/s | bit-exact, `{r['parity_test']}` |")
+    base = os.path.join(ROOT, "BASELINE.md")
+    with open(base) as f:
+        text = f.read()
+    i = text.index(BASELINE_TABLE_HEADER)
+    j = text.find("\n## ", i + len(BASELINE_TABLE_HEADER))
+    text = text[:i] + "\n".join(lines) + "\n" + (text[j:] if j >= 0 else "")
+    with open(base, "w") as f:
+        f.write(text)
+
+
 def main():
     args = parse()
+    if args.fill_baseline:
+        return fill_baseline(args.fill_baseline)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
               "(the quantizer's slices are independent; sharding is by KV head, layer or "
               "batch row with no communication).", file=sys.stderr)
         sys.exit(2)
+
+    if args.table:
+        return measure_table(args)
 
     import torch
     import paper_2609_35800_amd as hg

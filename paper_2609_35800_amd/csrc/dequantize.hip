@@ -156,8 +156,9 @@ static hipError_t launch_d(const Params& p, Tensors which, hipStream_t stream) {
   const uint64_t blocks = which == Tensors::kBoth ? 2 * per_tensor : per_tensor;
   if (blocks > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
   pd.blocks_k = which == Tensors::kValues ? 0u : (uint32_t)per_tensor;
+  constexpr int kWaves = BASE == HG_BASE_MINMAX ? kDequantizeWavesMinMax : kDequantizeWaves;
   hipLaunchKernelGGL((dequantize_kernel<BASE, D, BITS>), dim3((uint32_t)blocks), dim3(kThreads),
-                     occupancy_lds(kDequantizeWaves), stream, pd);
+                     occupancy_lds(kWaves), stream, pd);
   return hipGetLastError();
 }
 
