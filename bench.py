@@ -393,7 +393,12 @@ def fill_baseline(path: str) -> None:
              "| Config | Call | Median time | GB/s | % of 8 TB/s | rocprof bytes ÷ algorithmic bytes | "
              "Image tokens/s | Oracle 1-thread | Oracle N-thread | Parity |",
              "|---|---|---|---|---|---|---|---|---|---|"]
+    import synthkv
     for r in t["rows"]:
+        # counter ratios from the records committed now (taken on the current sources)
+        w = synthkv.WORKLOADS[r["workload"]].with_(bits=r["bits"])
+        rec = traffic_record(w, QUANT_KERNEL if r["call"] == "hg_quantize" else DEQUANT_KERNEL)
+        r["traffic_ratio"] = rec.get("ratio_to_algorithmic") if rec else None
         lines.append(f"| {r['config']} | `{r['call']}` | {r['median_ms'] * 1e3:.1f} µs | {r['GBps']:,.0f} | "
                      f"{r['pct_of_peak']:.1f} | {fmt(r['traffic_ratio'], '.4f')} | "
                      f"{r['image_tokens_per_s']:.3g} | {r['oracle_1_thread_GBps']:.3f} GB/s | "
