@@ -40,11 +40,12 @@ KERNEL_SOURCES = {
     FAKE_KERNEL: tuple(_CSRC + f for f in ("fakequant.hip", "kivi_seq.hip", "retain.hip",
                                              "hg_device.h", "hg_kernels.h")),
 }
-# The table of the benchmark's measured results: the five workloads, the 72B-shaped
-# one at each bit width (name, bits).
+# The measured-results table: the five workloads, the 72B-shaped one at each bit
+# width (name, bits).
 TABLE_WORKLOADS = (("tiny", None), ("qwen2.5-vl-7b", None), ("llava-next-7b", None), ("internvl-8b", None),
                    ("72b-long", 2), ("72b-long", 3), ("72b-long", 4))
-BASELINE_TABLE_HEADER = "## 4. Measured results"
+RESULTS_DOC = "BASELINE.md"  # the document whose results section --fill-baseline writes
+RESULTS_HEADER = "## 4. Measured results"
 
 
 def parse():
@@ -67,10 +68,11 @@ def parse():
     ap.add_argument("--quant-only", action="store_true",
                     help="time only the quantize launches (for profiling that kernel)")
     ap.add_argument("--table", metavar="JSON",
-                    help="measure every workload of BASELINE.md's results table (quantize and "
+                    help="measure every workload of the measured-results table (quantize and "
                          "dequantize median times, oracle on the host cores) into JSON")
     ap.add_argument("--fill-baseline", metavar="JSON",
-                    help="(no GPU) write the rows of a --table run into BASELINE.md's section 4")
+                    help="(no GPU) write the rows of a --table run as the results document's "
+                         "measured-results section")
     ap.add_argument("--op", default="step", choices=["step", "fakequant"],
                     help="step: quantize+pack then dequantize (the default line); "
                          "fakequant: the one-pass simulated quantization alone")
@@ -315,7 +317,7 @@ def bench_fakequant(args, hg, w, cfg, mask, K, V):
 
 
 def measure_table(args) -> None:
-    """The benchmark's measured-results table: for each workload, the median
+    """The measured-results table: for each workload, the median
     quantize and dequantize call times over `steps` calls (HIP events on the
     launch stream, inputs resident in HBM), the GB/s and image tokens/s they
     give, the committed counter ratios, and the oracle on the host cores
@@ -376,12 +378,13 @@ def measure_table(args) -> None:
 
 
 def fill_baseline(path: str) -> None:
-    """Writes the rows of a --table run as the table of the benchmark's section
-    4 (everything from its header to the next section is replaced)."""
+    """Writes the rows of a --table run as the results document's
+    measured-results section (everything from its header to the next section
+    is replaced)."""
     with open(path) as f:
         t = json.load(f)
     fmt = lambda v, spec: "—" if v is None else format(v, spec)  # noqa: E731
-    lines = [BASELINE_TABLE_HEADER, "",
+    lines = [RESULTS_HEADER, "",
              f"Written by `python bench.py --fill-baseline` from a `python bench.py --table` run on one MI355X "
              f"({t['date']}; median of {t['steps']} calls after {t['warmup']} warm-up steps, HIP events on the "
              "launch stream, inputs resident in HBM; bytes are the algorithmic bytes of `bench.py`). Counter "
@@ -403,11 +406,11 @@ def fill_baseline(path: str) -> None:
                      f"{r['pct_of_peak']:.1f} | {fmt(r['traffic_ratio'], '.4f')} | "
                      f"{r['image_tokens_per_s']:.3g} | {r['oracle_1_thread_GBps']:.3f} GB/s | "
                      f"{r['oracle_n_thread_GBps']:.2f} GB/s | bit-exact, `{r['parity_test']}` |")
-    base = os.path.join(ROOT, "BASELINE.md")
+    base = os.path.join(ROOT, RESULTS_DOC)
     with open(base) as f:
         text = f.read()
-    i = text.index(BASELINE_TABLE_HEADER)
-    j = text.find("\n## ", i + len(BASELINE_TABLE_HEADER))
+    i = text.index(RESULTS_HEADER)
+    j = text.find("\n## ", i + len(RESULTS_HEADER))
     text = text[:i] + "\n".join(lines) + "\n" + (text[j:] if j >= 0 else "")
     with open(base, "w") as f:
         f.write(text)
