@@ -1,9 +1,10 @@
 """hg_fake_quantize_noalloc (the one-pass call for callers that cannot
-allocate device memory; its retention workspace is the library's own device
-array) against hg_fake_quantize with a caller workspace: the same bytes, on
-two calls in a row, the second on a smaller cache, in place and out of place,
-with and without token retention.  A cache whose workspace would exceed the
-array is refused before any device work."""
+allocate device memory; its workspace is the library's own device array)
+against hg_fake_quantize with a caller workspace: the same bytes, on two calls
+in a row, the second on a smaller cache, in place and out of place, with and
+without token retention, and with whole-sequence KIVI keys (whose workgroups
+exchange partial ranges through the workspace).  A cache whose workspace
+would exceed the array is refused before any device work."""
 import ctypes as C
 
 import numpy as np
@@ -46,6 +47,28 @@ def _one_pass(hg, w, mask, inplace, noalloc):
         hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo, hg.alloc_fake_workspace(cfg, mask))
     torch.cuda.synchronize()
     return Ko.view(torch.int16).clone(), Vo.view(torch.int16).clone()
+
+
+def _kivi_whole(big):
+    # the workgroups holding a slice exchange their partial ranges through the
+    # workspace (4 MiB at head_dim 128)
+    if big:
+        return synthkv.WORKLOADS["llava-next-7b"].with_(kivi_group=0, L=8)
+    w = small("kivi", D=128, bits=2, img_len=1700, img_start=5, text=11, L=2, B=2, H=4, n_protected=1)
+    return w.with_(kivi_group=0, name="small-kivi-whole")
+
+
+@pytest.mark.parametrize("inplace", [False, True])
+def test_whole_sequence_kivi_keys_on_two_calls(inplace):
+    import paper_2609_35800_amd as hg
+    for w in (_kivi_whole(True), _kivi_whole(False)):
+        mask = synthkv.protect_mask(w)
+        need = hg.hg_packed_sizes(hg.make_config(**w.config_fields()), mask)["fake_workspace"]
+        assert 0 < need <= hg.HG_NOALLOC_SCRATCH_BYTES
+        gK, gV = _one_pass(hg, w, mask, inplace, noalloc=True)
+        wK, wV = _one_pass(hg, w, mask, inplace, noalloc=False)
+        assert torch.equal(gK, wK), w.name
+        assert torch.equal(gV, wV), w.name
 
 
 @pytest.mark.parametrize("permille", [20, 0])
