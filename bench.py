@@ -32,14 +32,16 @@ DEQUANT_KERNEL = "dequantize_kernel"
 FAKE_KERNEL = "fake_quantize_kernel"
 _CSRC = "paper_2609_35800_amd/csrc/"
 # the device sources that decide what each timed call reads and writes; a
-# counter measurement is reported only while their text is unchanged
+# counter measurement is reported only while their text is unchanged.  The
+# whole-sequence KIVI key kernels and the token-retention kernels count only
+# for the workloads whose calls launch them.
 KERNEL_SOURCES = {
-    QUANT_KERNEL: tuple(_CSRC + f for f in ("quantize.hip", "kivi_seq.hip", "retain.hip",
-                                              "hg_device.h", "hg_kernels.h")),
-    DEQUANT_KERNEL: tuple(_CSRC + f for f in ("dequantize.hip", "retain.hip", "hg_device.h", "hg_kernels.h")),
-    FAKE_KERNEL: tuple(_CSRC + f for f in ("fakequant.hip", "kivi_seq.hip", "retain.hip",
-                                             "hg_device.h", "hg_kernels.h")),
+    QUANT_KERNEL: tuple(_CSRC + f for f in ("quantize.hip", "hg_device.h", "hg_kernels.h")),
+    DEQUANT_KERNEL: tuple(_CSRC + f for f in ("dequantize.hip", "hg_device.h", "hg_kernels.h")),
+    FAKE_KERNEL: tuple(_CSRC + f for f in ("fakequant.hip", "hg_device.h", "hg_kernels.h")),
 }
+KIVI_WHOLE_SOURCE = _CSRC + "kivi_seq.hip"
+RETAIN_SOURCE = _CSRC + "retain.hip"
 # The measured-results table: the five workloads, the 72B-shaped one at each bit
 # width (name, bits).
 TABLE_WORKLOADS = (("tiny", None), ("qwen2.5-vl-7b", None), ("llava-next-7b", None), ("internvl-8b", None),
@@ -103,11 +105,24 @@ def _code_only(text: str) -> str:
     return "\n".join(line.rstrip() for line in "".join(out).splitlines() if line.strip())
 
 
-def kernel_source_hash(kernel: str = QUANT_KERNEL) -> str:
+def kernel_sources(kernel: str, w=None) -> tuple:
+    """Device sources of a call on workload w (without w: every source the
+    call can launch)."""
+    srcs = list(KERNEL_SOURCES[kernel])
+    kivi_whole = w is None or (w.base == "kivi" and w.kivi_group == 0)
+    if kernel in (QUANT_KERNEL, FAKE_KERNEL) and kivi_whole:
+        srcs.append(KIVI_WHOLE_SOURCE)
+    if w is None or w.retain_permille:
+        srcs.append(RETAIN_SOURCE)
+    return tuple(srcs)
+
+
+def kernel_source_hash(kernel: str = QUANT_KERNEL, w=None) -> str:
     """Hash of the code (comments and blank lines removed) of the device
-    sources of a call; a traffic record is reported only while it matches."""
+    sources of a call on workload w; a traffic record is reported only while
+    it matches."""
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES[kernel]:
+    for p in kernel_sources(kernel, w):
         with open(os.path.join(ROOT, p), encoding="utf-8") as f:
             h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
@@ -132,7 +147,7 @@ def traffic_record(w, kernel: str = QUANT_KERNEL):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("kernel_source_hash") != kernel_source_hash(kernel):
+    if rec.get("kernel_source_hash") != kernel_source_hash(kernel, w):
         return None
     return rec
 

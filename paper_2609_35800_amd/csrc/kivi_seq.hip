@@ -17,12 +17,12 @@
 //     rows a wavefront holds by shuffles and across wavefronts by LDS
 //     atomics;
 //  2. with P > 1, the group's partial ranges are combined through a caller
-//     workspace: each workgroup publishes its 2D partial values as 64-bit
-//     words tagged with the slice's sequence number in the group (relaxed
-//     device-scope atomics; a tagged word carries its own value, so no fence
-//     is needed) and waits, a bounded number of polls, for its partners'
-//     words of the same tag; two buffers alternate between consecutive
-//     slices;
+//     workspace: each workgroup publishes its range of each channel as one
+//     64-bit word, the BF16 minimum and maximum tagged with the slice's
+//     sequence number in the group (relaxed device-scope atomics; a tagged
+//     word carries its own values, so no fence is needed), and polls each
+//     partner's word of the channel, a bounded number of times, until it
+//     carries that tag; two buffers alternate between consecutive slices;
 //  3. codes (or, for the one-pass simulated quantization, the BF16
 //     reconstruction) of the workgroup's image rows: whole packed rows, so
 //     every stored line is complete; as the row slots are consumed, the
@@ -185,7 +185,7 @@ constexpr int kPartRegSlots = 15;
 constexpr int kPartSlots = kPartLdsSlots + kPartRegSlots;
 constexpr int kMaxPartners = 8;
 // Exchange area (u64 words): a header (word 0 counts waits that ran out of
-// polls), then [group][2 buffers][partner][2D] tagged words for at most
+// polls), then [group][2 buffers][partner][D] tagged words for at most
 // kExMaxWgs workgroups.
 constexpr int kExHeader = 64;
 constexpr int kExMaxWgs = 1024;
@@ -284,22 +284,32 @@ __device__ __forceinline__ void store_quad_codes(__amdgpu_buffer_rsrc_t r, uint3
   }
 }
 
-// Waits for a partner's tagged word of sequence tag `gen` (bounded polls).
-__device__ __forceinline__ uint64_t wait_tagged(uint64_t* w, uint32_t gen, uint32_t& timeouts) {
+// A channel's range in one 64-bit exchange word: the sequence tag in the high
+// half, then the maximum's and the minimum's BF16 bits (both are BF16 values:
+// the range is taken over BF16 inputs, odd channels masked to their high
+// halves), so one relaxed 64-bit store publishes the whole range and a reader
+// that sees the tag sees the values with it.
+__device__ __forceinline__ uint64_t tagged_range(float lo, float hi, uint32_t gen) {
+  return ((uint64_t)gen << 32) | (__float_as_uint(hi) & 0xFFFF0000u) | (__float_as_uint(lo) >> 16);
+}
+
+// Folds partner r's range of one channel into [a, b]: `w` is the partner's
+// word of the channel, loaded again, with a short sleep, until it carries
+// tag `gen` or kSpinLimit polls have passed (then counted).  One word per
+// partner and round trip: the minimum and the maximum arrive together.
+__device__ __forceinline__ void fold_partner(const uint64_t* w, uint32_t gen, float& a, float& b,
+                                             uint32_t& timeouts) {
   uint64_t v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   for (uint32_t spin = 0; (uint32_t)(v >> 32) != gen; ++spin) {
     if (spin == kSpinLimit) {
       ++timeouts;
-      break;
+      return;
     }
     __builtin_amdgcn_s_sleep(2);
     v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  return v;
-}
-
-__device__ __forceinline__ uint64_t tagged(float v, uint32_t gen) {
-  return ((uint64_t)gen << 32) | __float_as_uint(v);
+  a = fminf(a, __uint_as_float((uint32_t)v << 16));
+  b = fmaxf(b, __uint_as_float((uint32_t)v & 0xFFFF0000u));
 }
 
 template <int D, int BITS, bool FAKE>
@@ -431,17 +441,12 @@ void kivi_part_kernel(const Params p, uint32_t n_items, uint32_t groups, uint32_
       red[D + tid] = -__builtin_inff();
       if (parts > 1) {
         const uint32_t gen = seq + 1;
-        uint64_t* buf = ex + kExHeader + ((size_t)g * 2u + (seq & 1u)) * parts * 2u * D;
-        uint64_t* mine = buf + (size_t)q * 2u * D;
-        __hip_atomic_store(mine + tid, tagged(a, gen), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(mine + D + tid, tagged(b, gen), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        uint64_t* buf = ex + kExHeader + ((size_t)g * 2u + (seq & 1u)) * parts * D;
+        __hip_atomic_store(buf + (size_t)q * D + tid, tagged_range(a, b, gen), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
         uint32_t timeouts = 0;
-        for (uint32_t r = 0; r < parts; ++r) {
-          if (r == q) continue;
-          uint64_t* theirs = buf + (size_t)r * 2u * D;
-          a = fminf(a, __uint_as_float((uint32_t)wait_tagged(theirs + tid, gen, timeouts)));
-          b = fmaxf(b, __uint_as_float((uint32_t)wait_tagged(theirs + D + tid, gen, timeouts)));
-        }
+        for (uint32_t r = 0; r < parts; ++r)
+          if (r != q) fold_partner(buf + (size_t)r * D + tid, gen, a, b, timeouts);
         if (timeouts) __hip_atomic_fetch_add(ex, (uint64_t)timeouts, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       const GroupScale gs = group_scale<LEVELS>(a, b);
@@ -553,7 +558,7 @@ int kivi_partners(int T, int D) {
 }
 
 uint64_t kivi_workspace_bytes(int T, int D) {
-  return kivi_partners(T, D) > 1 ? ((uint64_t)kExHeader + (uint64_t)kExMaxWgs * 2 * 2 * D) * 8 : 0;
+  return kivi_partners(T, D) > 1 ? ((uint64_t)kExHeader + (uint64_t)kExMaxWgs * 2 * D) * 8 : 0;
 }
 
 // Compute units the persistent grids are sized for: the device's, or fewer
@@ -590,7 +595,7 @@ static hipError_t launch_part(const Params& p, int parts, uint64_t* ex, int cus,
   const uint32_t groups = std::min((n_items + 7u) / 8u * 8u, cap);
   const uint32_t rows_per_part = (uint32_t)((p.T + parts - 1) / parts);
   if (parts > 1) {
-    const uint32_t words = (uint32_t)(kExHeader + (uint64_t)groups * 2 * parts * 2 * D);
+    const uint32_t words = (uint32_t)(kExHeader + (uint64_t)groups * 2 * parts * D);
     hipLaunchKernelGGL(zero_words_kernel, dim3(std::min<uint32_t>((words + 255) / 256, 1024)), dim3(256), 0,
                        stream, ex, words);
     e = hipGetLastError();

@@ -90,19 +90,20 @@ def kivi_exchange_bytes(f, sizes):
     """Closed form of hg_quantize's workspace: KIVI keys over the whole
     sequence, some key slice quantized, and a slice longer than one
     workgroup's 24 slots of 16 * 512/D rows (at most 8 workgroups per slice):
-    a 64-word header plus 1024 workgroups x 2 buffers x 2D tagged words."""
+    a 64-word header plus 1024 workgroups x 2 buffers x D tagged words (one
+    per channel)."""
     if f["base"] != 1 or f["kivi_group"] != 0 or f["img_len"] == 0 or sizes["n_unprot_k"] == 0:
         return 0
     cap = 24 * 8192 // f["D"]
     parts = -(-f["T"] // cap)
     if parts < 2 or parts > 8:
         return 0
-    return (64 + 1024 * 2 * 2 * f["D"]) * 8
+    return (64 + 1024 * 2 * f["D"]) * 8
 
 
 def test_workspace_of_whole_sequence_kivi_keys():
     mask = np.zeros(8, np.uint8)
-    ws = lambda D: (64 + 4096 * D) * 8  # noqa: E731
+    ws = lambda D: (64 + 2048 * D) * 8  # noqa: E731
     for T, D, want in ((3008, 128, ws(128)), (1536, 128, 0), (1537, 128, ws(128)), (12288, 128, ws(128)),
                        (12289, 128, 0), (3008, 64, 0), (3073, 64, ws(64)), (3008, 256, ws(256)),
                        (6144, 256, ws(256)), (6145, 256, 0)):
