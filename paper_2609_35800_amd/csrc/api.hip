@@ -336,15 +336,22 @@ static int run(bool quantize, const hg_config* cfg, const uint16_t* K, const uin
   p.k = z.retain_count;
   p.out[0] = quantize ? nullptr : (uint16_t*)K;
   p.out[1] = quantize ? nullptr : (uint16_t*)V;
+  // whole-sequence KIVI keys: the first kernel of the call clears the key
+  // kernel's exchange words (one launch fewer)
+  void* kivi_ws = z.workspace ? pk->workspace : nullptr;
+  if (quantize && p.kivi_whole && kivi_ws) {
+    const hipError_t pe = hg::kivi_seq_clear_words(p, cfg->D, cfg->bits, false, kivi_ws, &p.clear_words);
+    if (pe != hipSuccess) return fail(HG_ERR_HIP, "KIVI key kernel plan failed: %s", hipGetErrorString(pe));
+    p.clear = (uint64_t*)kivi_ws;
+  }
   LaunchSteps step;
   hipError_t e = step([&] {
     return quantize ? hg::launch_quantize(p, cfg->base, cfg->D, cfg->bits, retain, stream)
                     : hg::launch_dequantize(p, cfg->base, cfg->D, cfg->bits, stream);
   });
+  p.clear_words = 0;
   if (e == hipSuccess && quantize && p.kivi_whole)
-    e = step([&] {
-      return hg::launch_kivi_seq(p, cfg->D, cfg->bits, false, z.workspace ? pk->workspace : nullptr, stream);
-    });
+    e = step([&] { return hg::launch_kivi_seq(p, cfg->D, cfg->bits, false, kivi_ws, true, stream); });
   if (e == hipSuccess && p.k > 0 && quantize)
     e = step([&] { return hg::launch_retain_select(p, cfg->D, hg::RowCopy::kGather, stream); });
   if (e == hipSuccess && p.k > 0 && !quantize)
@@ -446,10 +453,15 @@ int fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V, co
     if (e == hipSuccess)
       e = step([&] { return hg::launch_retain_select(p, cfg->D, hg::RowCopy::kGather, stream); });
   }
+  if (e == hipSuccess && p.kivi_whole && ws) {  // the one-pass kernel clears the key kernel's exchange words
+    e = hg::kivi_seq_clear_words(p, cfg->D, cfg->bits, true, ws, &p.clear_words);
+    p.clear = (uint64_t*)ws;
+  }
   if (e == hipSuccess)
     e = step([&] { return hg::launch_fake_quantize(p, cfg->base, cfg->D, cfg->bits, fused, stream); });
+  p.clear_words = 0;
   if (e == hipSuccess && p.kivi_whole)
-    e = step([&] { return hg::launch_kivi_seq(p, cfg->D, cfg->bits, true, ws, stream); });
+    e = step([&] { return hg::launch_kivi_seq(p, cfg->D, cfg->bits, true, ws, true, stream); });
   if (e == hipSuccess && fused) {
     e = step([&] { return hg::launch_retain_select(p, cfg->D, hg::RowCopy::kCacheToOut, stream); });
   } else if (e == hipSuccess && retain) {

@@ -214,6 +214,7 @@ __device__ __forceinline__ void fake_kivi_keys(const uint16_t* rows, uint16_t* o
 template <int BASE, int D, int BITS, bool NORM>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWaves)))
 void fake_quantize_kernel(const Params p) {
+  clear_words_share(p);
   const Slice sl = decode_block(p, blockIdx.x);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);

@@ -77,6 +77,10 @@ struct Params {
   int32_t* ret_idx;          // [L][B][H][k] retained tokens, ascending
   uint16_t* ret[2];          // [slot][B][k][D] retained rows of K, V
   int32_t k;                 // retained tokens per (l, b, h)
+  // words the first workgroups of this launch set to zero (the exchange area
+  // of the whole-sequence KIVI key kernel that follows in the same call)
+  uint64_t* clear;
+  uint32_t clear_words;
   Route route;
 };
 
@@ -93,7 +97,10 @@ hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, bool
 // its rows, every channel) that combine their partial ranges through the
 // exchange workspace `ws` (kivi_workspace_bytes; unused with one workgroup
 // per slice), or, for longer slices, a range pass and a code pass per slice.
-hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, void* ws, hipStream_t stream);
+// `cleared`: the words kivi_seq_clear_words gives were set to zero by an
+// earlier launch of the call (else the launch clears them itself).
+hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, void* ws, bool cleared, hipStream_t stream);
+hipError_t kivi_seq_clear_words(const Params& p, int D, int bits, bool fake, void* ws, uint32_t* words);
 // Workgroups per slice of the resident kernel (0: the two-pass kernel), and
 // the exchange workspace bytes a call with T rows per slice needs (0: none).
 int kivi_partners(int T, int D);
@@ -152,6 +159,15 @@ __device__ __forceinline__ SliceRoute route_slice(const Params& p, int X, uint32
     r.slot = i - rank;
   }
   return r;
+}
+
+// The first kClearBlocks workgroups of a launch set the p.clear_words words
+// at p.clear to zero (a share each), before anything else.
+constexpr uint32_t kClearBlocks = 64;
+__device__ __forceinline__ void clear_words_share(const Params& p) {
+  if (p.clear_words == 0 || blockIdx.x >= kClearBlocks) return;
+  const uint32_t nb = min(gridDim.x, kClearBlocks);
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < p.clear_words; i += nb * blockDim.x) p.clear[i] = 0;
 }
 
 // Block decoding: tensor, slice, token tile and routing of a workgroup.

@@ -574,82 +574,115 @@ static hipError_t grid_cus(int* cus) {
   return hipSuccess;
 }
 
-template <int D, int BITS, bool FAKE>
-static hipError_t launch_part(const Params& p, int parts, uint64_t* ex, int cus, bool* launched,
-                              hipStream_t stream) {
-  *launched = false;
-  int per_cu = 0;
-  hipError_t e =
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kivi_part_kernel<D, BITS, FAKE>, kPartThreads, 0);
-  if (e != hipSuccess) return e;
-  const uint32_t n_items = (uint32_t)p.n_unprot_k * (uint32_t)p.B;
-  if (n_items == 0) {  // every key head kept in BF16: nothing to quantize here
-    *launched = true;
-    return hipSuccess;
-  }
-  const uint32_t resident = (uint32_t)std::max(per_cu, 0) * (uint32_t)cus;  // workgroups held at once
-  uint32_t cap = resident / (uint32_t)parts;
-  if (parts > 1) cap = std::min(cap, (uint32_t)(kExMaxWgs / parts));
-  cap = cap / 8u * 8u;
-  if (cap == 0) return hipSuccess;  // too few resident workgroups: the two-pass kernel instead
-  const uint32_t groups = std::min((n_items + 7u) / 8u * 8u, cap);
-  const uint32_t rows_per_part = (uint32_t)((p.T + parts - 1) / parts);
-  if (parts > 1) {
-    const uint32_t words = (uint32_t)(kExHeader + (uint64_t)groups * 2 * parts * D);
-    hipLaunchKernelGGL(zero_words_kernel, dim3(std::min<uint32_t>((words + 255) / 256, 1024)), dim3(256), 0,
-                       stream, ex, words);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL((kivi_part_kernel<D, BITS, FAKE>), dim3(groups * (uint32_t)parts), dim3(kPartThreads), 0,
-                     stream, p, n_items, groups, (uint32_t)parts, rows_per_part, ex);
-  *launched = true;
-  return hipGetLastError();
-}
+// Launch plan of one call's key kernels: the resident kernel when every
+// workgroup of its grid can be resident at once (and, with several per slice,
+// an exchange workspace is given), else the two-pass kernel; and the leading
+// workspace words to clear before it (the exchange words the resident grid
+// uses, or the header alone, whose first word then reads 0: the two-pass
+// kernel waits for nothing).
+struct KiviPlan {
+  bool resident = false;
+  int parts = 0;
+  uint32_t n_items = 0, groups = 0, rows_per_part = 0;
+  uint32_t clear_words = 0;
+};
 
-template <int D, int BITS>
-static hipError_t launch_k(const Params& p, bool fake, void* ws, hipStream_t stream) {
+template <int D, int BITS, bool FAKE>
+static hipError_t plan_k(const Params& p, bool has_ws, KiviPlan* pl) {
+  *pl = KiviPlan();
+  pl->n_items = (uint32_t)p.n_unprot_k * (uint32_t)p.B;
+  if (pl->n_items == 0) return hipSuccess;  // every key head kept in BF16: nothing to quantize here
   int cus = 0;
   hipError_t e = grid_cus(&cus);
   if (e != hipSuccess) return e;
   const int parts = kivi_partners(p.T, D);
-  if (parts > 0 && (parts == 1 || ws)) {
-    bool launched = false;
-    e = fake ? launch_part<D, BITS, true>(p, parts, (uint64_t*)ws, cus, &launched, stream)
-             : launch_part<D, BITS, false>(p, parts, (uint64_t*)ws, cus, &launched, stream);
-    if (e != hipSuccess || launched) return e;
+  if (parts > 0 && (parts == 1 || has_ws)) {
+    int per_cu = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kivi_part_kernel<D, BITS, FAKE>, kPartThreads, 0);
+    if (e != hipSuccess) return e;
+    const uint32_t resident = (uint32_t)std::max(per_cu, 0) * (uint32_t)cus;  // workgroups held at once
+    uint32_t cap = resident / (uint32_t)parts;
+    if (parts > 1) cap = std::min(cap, (uint32_t)(kExMaxWgs / parts));
+    cap = cap / 8u * 8u;
+    if (cap > 0) {
+      pl->resident = true;
+      pl->parts = parts;
+      pl->groups = std::min((pl->n_items + 7u) / 8u * 8u, cap);
+      pl->rows_per_part = (uint32_t)((p.T + parts - 1) / parts);
+      if (parts > 1) pl->clear_words = (uint32_t)(kExHeader + (uint64_t)pl->groups * 2 * parts * D);
+      return hipSuccess;
+    }
   }
-  if (ws) {  // the two-pass kernel waits for nothing: the workspace's count of timed-out waits is 0
-    hipLaunchKernelGGL(zero_words_kernel, dim3(1), dim3(64), 0, stream, (uint64_t*)ws, (uint32_t)kExHeader);
+  if (has_ws) pl->clear_words = (uint32_t)kExHeader;
+  return hipSuccess;
+}
+
+template <int D, int BITS, bool FAKE>
+static hipError_t launch_k(const Params& p, void* ws, bool cleared, hipStream_t stream) {
+  KiviPlan pl;
+  hipError_t e = plan_k<D, BITS, FAKE>(p, ws != nullptr, &pl);
+  if (e != hipSuccess || pl.n_items == 0) return e;
+  if (pl.clear_words > 0 && !cleared) {
+    hipLaunchKernelGGL(zero_words_kernel, dim3(std::min<uint32_t>((pl.clear_words + 255) / 256, 1024)), dim3(256),
+                       0, stream, (uint64_t*)ws, pl.clear_words);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  if (pl.resident) {
+    hipLaunchKernelGGL((kivi_part_kernel<D, BITS, FAKE>), dim3(pl.groups * (uint32_t)pl.parts), dim3(kPartThreads),
+                       0, stream, p, pl.n_items, pl.groups, (uint32_t)pl.parts, pl.rows_per_part, (uint64_t*)ws);
+    return hipGetLastError();
+  }
+  int cus = 0;
+  e = grid_cus(&cus);
+  if (e != hipSuccess) return e;
   const uint32_t slices = (uint32_t)p.L * p.B * p.H;
   const uint32_t blocks = std::min<uint32_t>(slices, (uint32_t)std::max(cus, 1) * kSeqBlocksPerCU);
-  if (fake)
-    hipLaunchKernelGGL((kivi_seq_kernel<D, BITS, true>), dim3(blocks), dim3(kSeqThreads), 0, stream, p);
-  else
-    hipLaunchKernelGGL((kivi_seq_kernel<D, BITS, false>), dim3(blocks), dim3(kSeqThreads), 0, stream, p);
+  hipLaunchKernelGGL((kivi_seq_kernel<D, BITS, FAKE>), dim3(blocks), dim3(kSeqThreads), 0, stream, p);
   return hipGetLastError();
 }
 
-template <int D>
-static hipError_t launch_k_bits(const Params& p, int bits, bool fake, void* ws, hipStream_t stream) {
+template <int D, int BITS, bool FAKE>
+static hipError_t plan_words(const Params& p, void* ws, uint32_t* clear_words) {
+  KiviPlan pl;
+  const hipError_t e = plan_k<D, BITS, FAKE>(p, ws != nullptr, &pl);
+  *clear_words = pl.clear_words;
+  return e;
+}
+
+// With clear_words: only the number of workspace words the launch needs
+// cleared; else the launch.
+template <int D, bool FAKE>
+static hipError_t kivi_d(const Params& p, int bits, void* ws, bool cleared, uint32_t* clear_words,
+                         hipStream_t stream) {
   switch (bits) {
-    case 2: return launch_k<D, 2>(p, fake, ws, stream);
-    case 3: return launch_k<D, 3>(p, fake, ws, stream);
-    case 4: return launch_k<D, 4>(p, fake, ws, stream);
+    case 2: return clear_words ? plan_words<D, 2, FAKE>(p, ws, clear_words) : launch_k<D, 2, FAKE>(p, ws, cleared, stream);
+    case 3: return clear_words ? plan_words<D, 3, FAKE>(p, ws, clear_words) : launch_k<D, 3, FAKE>(p, ws, cleared, stream);
+    case 4: return clear_words ? plan_words<D, 4, FAKE>(p, ws, clear_words) : launch_k<D, 4, FAKE>(p, ws, cleared, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, void* ws, hipStream_t stream) {
+static hipError_t kivi_dispatch(const Params& p, int D, int bits, bool fake, void* ws, bool cleared,
+                                uint32_t* clear_words, hipStream_t stream) {
   switch (D) {
-    case 64: return launch_k_bits<64>(p, bits, fake, ws, stream);
-    case 128: return launch_k_bits<128>(p, bits, fake, ws, stream);
-    case 256: return launch_k_bits<256>(p, bits, fake, ws, stream);
+    case 64: return fake ? kivi_d<64, true>(p, bits, ws, cleared, clear_words, stream)
+                         : kivi_d<64, false>(p, bits, ws, cleared, clear_words, stream);
+    case 128: return fake ? kivi_d<128, true>(p, bits, ws, cleared, clear_words, stream)
+                          : kivi_d<128, false>(p, bits, ws, cleared, clear_words, stream);
+    case 256: return fake ? kivi_d<256, true>(p, bits, ws, cleared, clear_words, stream)
+                          : kivi_d<256, false>(p, bits, ws, cleared, clear_words, stream);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t kivi_seq_clear_words(const Params& p, int D, int bits, bool fake, void* ws, uint32_t* words) {
+  *words = 0;
+  return kivi_dispatch(p, D, bits, fake, ws, false, words, nullptr);
+}
+
+hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, void* ws, bool cleared, hipStream_t stream) {
+  return kivi_dispatch(p, D, bits, fake, ws, cleared, nullptr, stream);
 }
 
 }  // namespace hg

@@ -230,6 +230,7 @@ __device__ __forceinline__ void quantize_kivi_keys(const uint16_t* __restrict__ 
 
 template <int BASE, int D, int BITS, bool NORM>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWaves))) void quantize_kernel(const Params p) {
+  clear_words_share(p);
   const Slice sl = decode_block(p, blockIdx.x);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
