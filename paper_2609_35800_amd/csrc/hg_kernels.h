@@ -35,9 +35,9 @@ constexpr int kDequantizeWaves = 6;
 // The min-max dequantize instantiation (per-token groups only: min-max keys
 // and values, AKVQ-style values): 4 (kernel time 1095 -> 1053 us on the
 // LLaVA-1.5-shaped cache, 872 -> 854 on the 72B-shaped one, 711 -> 698 at
-// head_dim 256, 363 -> 351 for InternVL-shaped values; 5 % slower on the
-// small Qwen-shaped cache); the KIVI-style and AKVQ-style key
-// instantiations keep 6 (4: 6 % slower).
+// head_dim 256, 363 -> 351 for InternVL-shaped values) when a launch writes
+// at least 1 GiB of rows; smaller launches keep 6 (dequantize.hip).  The
+// KIVI-style and AKVQ-style key instantiations keep 6 (4: 6 % slower).
 constexpr int kDequantizeWavesMinMax = 4;
 // The one-pass kernels: 4 (0.3-1 % faster than uncapped or 6 on the Qwen-,
 // 72B- and LLaVA-NeXT-shaped caches, InternVL-shaped unchanged).
