@@ -42,12 +42,15 @@ def canaries_intact(raw) -> bool:
 
 
 def gpu_run(w: synthkv.Workload, K: torch.Tensor, V: torch.Tensor, mask: np.ndarray,
-            stream=None, sentinel: int = 0x7FBF):
-    """Quantize + dequantize on the GPU; returns host copies of everything."""
+            stream=None, sentinel: int = 0x7FBF, prefill=None):
+    """Quantize + dequantize on the GPU; returns host copies of everything.
+    prefill(packed), if given, writes the output buffers before the call."""
     import paper_2609_35800_amd as hg
     cfg = hg.make_config(**w.config_fields())
     sizes = hg.hg_packed_sizes(cfg, mask)
     packed, raw = alloc_with_canary(sizes)
+    if prefill is not None:
+        prefill(packed)
     Kg, Vg = K.cuda().contiguous(), V.cuda().contiguous()
     Ko = torch.full(Kg.shape, sentinel, dtype=torch.int16, device="cuda").view(torch.bfloat16)
     Vo = torch.full(Vg.shape, sentinel, dtype=torch.int16, device="cuda").view(torch.bfloat16)
@@ -80,10 +83,10 @@ def oracle_run(w: synthkv.Workload, Kb: np.ndarray, Vb: np.ndarray, mask: np.nda
     return as_bytes, Ko, Vo
 
 
-def compare_full(w, K, V, mask, stream=None):
+def compare_full(w, K, V, mask, stream=None, prefill=None):
     """Element-by-element parity of every output; returns a report dict."""
     Kb, Vb = synthkv.bf16_bits(K), synthkv.bf16_bits(V)
-    g_pk, g_K, g_V, canary_ok = gpu_run(w, K, V, mask, stream=stream)
+    g_pk, g_K, g_V, canary_ok = gpu_run(w, K, V, mask, stream=stream, prefill=prefill)
     o_pk, o_K, o_V = oracle_run(w, Kb, Vb, mask)
     rep = {"canaries": canary_ok, "exchange_timeouts": g_pk.pop("_exchange_timeouts")}
     for n in o_pk:

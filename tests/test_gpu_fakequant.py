@@ -24,11 +24,13 @@ def oracle_roundtrip(w, Kb, Vb, mask, init_K, init_V):
     return Ko, Vo
 
 
-def run_fake(w, K, V, mask, inplace):
+def run_fake(w, K, V, mask, inplace, prefill_ws=None):
     import paper_2609_35800_amd as hg
     cfg = hg.make_config(**w.config_fields())
     Kg, Vg = K.cuda().contiguous(), V.cuda().contiguous()
     ws = hg.alloc_fake_workspace(cfg, mask)
+    if prefill_ws is not None and ws is not None:
+        prefill_ws(ws)
     if inplace:
         hg.hg_fake_quantize(cfg, Kg, Vg, mask, Kg, Vg, ws)
         Ko, Vo = Kg, Vg
@@ -42,9 +44,9 @@ def run_fake(w, K, V, mask, inplace):
     return synthkv.bf16_bits(Ko), synthkv.bf16_bits(Vo)
 
 
-def check(w, K, V, mask, inplace):
+def check(w, K, V, mask, inplace, prefill_ws=None):
     Kb, Vb = synthkv.bf16_bits(K), synthkv.bf16_bits(V)
-    gK, gV = run_fake(w, K, V, mask, inplace)
+    gK, gV = run_fake(w, K, V, mask, inplace, prefill_ws)
     initK = Kb if inplace else np.full_like(Kb, SENTINEL)
     initV = Vb if inplace else np.full_like(Vb, SENTINEL)
     oK, oV = oracle_roundtrip(w, Kb, Vb, mask, initK, initV)

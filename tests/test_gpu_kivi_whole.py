@@ -151,3 +151,39 @@ def test_degenerate_masks(which, keys_only):
     if which == "last":
         mask[-1] = 0
     _assert_exact(compare_full(w, K, V, mask), f"mask-{which}-ko{keys_only}")
+
+
+def _stale_words(ws):
+    """Every 64-bit word of an exchange workspace set to what a partner would
+    fold in if the words were not cleared before the key kernel: a small
+    sequence tag (1 to 8, the first slices' tags) above the BF16 bits of the
+    range [-1000, 1000]."""
+    n = ws.numel() // 8
+    tags = (np.arange(n, dtype=np.uint64) % np.uint64(8)) + np.uint64(1)
+    words = (tags << np.uint64(32)) | (np.uint64(0x447A) << np.uint64(16)) | np.uint64(0xC47A)
+    ws[: n * 8].copy_(torch.from_numpy(words.view(np.uint8)).to(ws.device))
+
+
+# Two workgroups per slice (head_dim 128), 2-bit, keys and values quantized.
+STALE_CASE = next(w for w in STREAM_CASES
+                  if w.D == 128 and w.T == capacity(128) + 300 and w.bits == 2 and not w.keys_only)
+
+
+# Resident kernel with several slices per group (32 and 256 compute units'
+# grids) and the two-pass fallback (8), every call on a workspace holding
+# stale tagged words: the call must clear them before the key kernel reads.
+@pytest.mark.parametrize("cus", ["32", "", "8"])
+def test_stale_exchange_words(cus, monkeypatch):
+    monkeypatch.setenv("HG_TEST_CUS", cus)
+    w = STALE_CASE
+    K, V = synthkv.gen_kv(w)
+    prefill = lambda pk: _stale_words(pk["workspace"])  # noqa: E731
+    _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w), prefill=prefill), f"stale-cus{cus or 'all'}")
+
+
+@pytest.mark.parametrize("inplace", [False, True])
+def test_stale_exchange_words_fake(inplace, monkeypatch):
+    monkeypatch.setenv("HG_TEST_CUS", "32")
+    w = STALE_CASE
+    K, V = synthkv.gen_kv(w)
+    check_fake(w, K, V, synthkv.protect_mask(w), inplace, prefill_ws=_stale_words)
