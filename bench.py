@@ -183,13 +183,18 @@ def algorithmic_bytes(w, sizes) -> dict:
 
 
 def fake_quantize_bytes(w, sizes) -> int:
-    """Bytes the one-pass call must move: every image row of K and V read once
-    and written once, plus the text rows of quantized key slices that
-    KIVI-style keys over the whole sequence read for the range (retention
-    extras not counted)."""
+    """Bytes the out-of-place one-pass call must move: every image row of K
+    and V read once and written once, plus the text rows of quantized key
+    slices that KIVI-style keys over the whole sequence read for the range;
+    with token retention also the key norms written and read back by the
+    selection, the token lists written, and the retained rows read from the
+    input again and written over their simulated reconstruction (the
+    selection needs every norm, so it follows the pass that writes them)."""
     ab = algorithmic_bytes(w, sizes)
     img = 2 * w.L * w.B * w.H * w.img_len * w.D * 2
-    return img + ab["read"]
+    rows = sizes.get("ret_k", 0) + sizes.get("ret_v", 0)
+    retain = 2 * sizes.get("norm_k", 0) + sizes.get("ret_idx", 0) + 2 * rows
+    return img + ab["read"] + retain
 
 
 def cpu_model() -> str:
