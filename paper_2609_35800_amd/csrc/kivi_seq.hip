@@ -22,7 +22,9 @@
 //     sequence number in the group (relaxed device-scope atomics; a tagged
 //     word carries its own values, so no fence is needed), and polls each
 //     partner's word of the channel, a bounded number of times, until it
-//     carries that tag; two buffers alternate between consecutive slices;
+//     carries that tag; two buffers alternate between consecutive slices,
+//     and the words start at zero (cleared by the call's first kernel, the
+//     values' quantize or one-pass launch, or else by a kernel of their own);
 //  3. codes (or, for the one-pass simulated quantization, the BF16
 //     reconstruction) of the workgroup's image rows: whole packed rows, so
 //     every stored line is complete; as the row slots are consumed, the
