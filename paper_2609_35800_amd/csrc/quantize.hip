@@ -268,12 +268,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
   }
 }
 
+// Wavefronts per SIMD of a quantize launch: fewer as the codes' share of the
+// traffic grows (36, 52 and 68 bytes written per 256 read at head_dim 128).
+// At 4 bits, 4 instead of 6 measured 2-3 % faster on every cache shaped like
+// the workloads (72B-shaped 996 -> 972 us, Qwen-shaped 138.3 -> 133.7); at 3
+// bits, 5 gained 0.5-0.7 %; 2 bits keep kQuantizeWaves.  Launches whose
+// registers already allow fewer (KIVI-style key groups at 4) are unaffected.
+template <int BITS>
+constexpr int kQuantizeWavesOf = BITS == 4 ? 4 : BITS == 3 ? 5 : kQuantizeWaves;
+
 // Dynamic LDS of a quantize launch: the occupancy cap's reservation, less
 // the static stage of the staged-load path.
-template <int D>
+template <int D, int BITS>
 constexpr size_t quantize_lds() {
   constexpr size_t stage = kStagedLoads<D> ? (kThreads / 64) * (64 / kTokenLanes<D>) * (D / 8) * 16 : 0;
-  return occupancy_lds(kQuantizeWaves) - stage;
+  static_assert(occupancy_lds(kQuantizeWavesOf<BITS>) > stage, "the stage fits the reservation");
+  return occupancy_lds(kQuantizeWavesOf<BITS>) - stage;
 }
 
 // The workgroup tiles of a launch: kBlockTokens tokens each.
@@ -285,16 +295,17 @@ static hipError_t launch_q(const Params& p, Tensors which, bool norms, hipStream
   const uint64_t blocks = which == Tensors::kBoth ? 2 * per_tensor : per_tensor;
   if (blocks > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
   pq.blocks_k = which == Tensors::kValues ? 0u : (uint32_t)per_tensor;
+  constexpr size_t kLds = quantize_lds<D, BITS>();
   if constexpr (BASE == HG_BASE_AKVQ) {
     if (norms) {
       hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, true>), dim3((uint32_t)blocks), dim3(kThreads),
-                         quantize_lds<D>(), stream, pq);
+                         kLds, stream, pq);
       return hipGetLastError();
     }
   }
   if (norms) return hipErrorInvalidValue;  // key norms belong to the AKVQ base
   hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, false>), dim3((uint32_t)blocks), dim3(kThreads),
-                     quantize_lds<D>(), stream, pq);
+                     kLds, stream, pq);
   return hipGetLastError();
 }
 
