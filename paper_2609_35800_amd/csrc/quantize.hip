@@ -268,22 +268,32 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWa
   }
 }
 
-// Wavefronts per SIMD of a quantize launch: fewer as the codes' share of the
-// traffic grows (36, 52 and 68 bytes written per 256 read at head_dim 128).
-// At 4 bits, 4 instead of 6 measured 2-3 % faster on every cache shaped like
-// the workloads (72B-shaped 996 -> 972 us, Qwen-shaped 138.3 -> 133.7); at 3
-// bits, 5 gained 0.5-0.7 %; 2 bits keep kQuantizeWaves.  Launches whose
-// registers already allow fewer (KIVI-style key groups at 4) are unaffected.
-template <int BITS>
-constexpr int kQuantizeWavesOf = BITS == 4 ? 4 : BITS == 3 ? 5 : kQuantizeWaves;
+// Wavefronts per SIMD of a quantize launch (each measured against 6 on the
+// caches shaped like the workloads):
+//  - 4 for 4-bit codes, whose stores are twice the 2-bit share of the traffic
+//    (68 bytes per 256 read): 2-3 % faster everywhere (72B-shaped 996 -> 972
+//    us, Qwen-shaped 138.3 -> 133.7);
+//  - 4 at head_dim 256 (staged loads; its registers allow 5): Gemma-shaped
+//    705 -> 694 us;
+//  - 4 for the rotated AKVQ-style keys: InternVL-shaped 384 -> 381 us (3
+//    bits: 395 -> 385); with the key norms of token retention, 4 measured
+//    slower (399 -> 407), so those keep the rule by width;
+//  - 5 for 3-bit codes: 0.5-0.7 %;
+//  - else kQuantizeWaves.
+// Launches whose registers already allow fewer (KIVI-style key groups at 4)
+// are unaffected.
+template <int BASE, int D, int BITS, bool NORM>
+constexpr int kQuantizeWavesOf =
+    BITS == 4 || D == 256 || (BASE == HG_BASE_AKVQ && !NORM) ? 4 : BITS == 3 ? 5 : kQuantizeWaves;
 
 // Dynamic LDS of a quantize launch: the occupancy cap's reservation, less
 // the static stage of the staged-load path.
-template <int D, int BITS>
+template <int BASE, int D, int BITS, bool NORM>
 constexpr size_t quantize_lds() {
   constexpr size_t stage = kStagedLoads<D> ? (kThreads / 64) * (64 / kTokenLanes<D>) * (D / 8) * 16 : 0;
-  static_assert(occupancy_lds(kQuantizeWavesOf<BITS>) > stage, "the stage fits the reservation");
-  return occupancy_lds(kQuantizeWavesOf<BITS>) - stage;
+  constexpr int waves = kQuantizeWavesOf<BASE, D, BITS, NORM>;
+  static_assert(occupancy_lds(waves) > stage, "the stage fits the reservation");
+  return occupancy_lds(waves) - stage;
 }
 
 // The workgroup tiles of a launch: kBlockTokens tokens each.
@@ -295,15 +305,16 @@ static hipError_t launch_q(const Params& p, Tensors which, bool norms, hipStream
   const uint64_t blocks = which == Tensors::kBoth ? 2 * per_tensor : per_tensor;
   if (blocks > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
   pq.blocks_k = which == Tensors::kValues ? 0u : (uint32_t)per_tensor;
-  constexpr size_t kLds = quantize_lds<D, BITS>();
   if constexpr (BASE == HG_BASE_AKVQ) {
     if (norms) {
+      constexpr size_t kLdsNorm = quantize_lds<BASE, D, BITS, true>();
       hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, true>), dim3((uint32_t)blocks), dim3(kThreads),
-                         kLds, stream, pq);
+                         kLdsNorm, stream, pq);
       return hipGetLastError();
     }
   }
   if (norms) return hipErrorInvalidValue;  // key norms belong to the AKVQ base
+  constexpr size_t kLds = quantize_lds<BASE, D, BITS, false>();
   hipLaunchKernelGGL((quantize_kernel<BASE, D, BITS, false>), dim3((uint32_t)blocks), dim3(kThreads),
                      kLds, stream, pq);
   return hipGetLastError();
