@@ -30,7 +30,7 @@ constexpr size_t occupancy_lds(int waves) { return waves > 0 ? kLdsPerCU / (wave
 // registers allow, the memory system is oversubscribed (6 measured faster
 // than 8, 5 and 4 over the workloads at 2 bits; quantize kernels whose
 // registers already allow fewer, such as KIVI key groups at 4, are not
-// affected).  Quantize lowers it for 3- and 4-bit codes (quantize.hip).
+// affected).  Quantize lowers it for some launches (kQuantizeWavesOf).
 constexpr int kQuantizeWaves = 6;
 constexpr int kDequantizeWaves = 6;
 // The min-max dequantize instantiation (per-token groups only: min-max keys
