@@ -190,18 +190,16 @@ static hipError_t launch_d_dim(const Params& p, int D, int bits, Tensors which, 
   }
 }
 
-// AKVQ-style values are dequantized per token exactly as min-max ones, so
-// they run as a launch of the min-max instantiation, with its shorter tiles.
+// KIVI-style and AKVQ-style values are dequantized per token exactly as
+// min-max ones, so they run as a second launch of the min-max instantiation,
+// with its shorter tiles and occupancy rule (the KIVI-style values in it:
+// LLaVA-NeXT-shaped dequantize 1252 -> 1239 us at 2 bits, 1359 -> 1305 at 4).
 hipError_t launch_dequantize(const Params& p, int base, int D, int bits, hipStream_t stream) {
-  switch (base) {
-    case HG_BASE_MINMAX: return launch_d_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kBoth, stream);
-    case HG_BASE_KIVI: return launch_d_dim<HG_BASE_KIVI>(p, D, bits, Tensors::kBoth, stream);
-    case HG_BASE_AKVQ: {
-      const hipError_t e = launch_d_dim<HG_BASE_AKVQ>(p, D, bits, Tensors::kKeys, stream);
-      return e != hipSuccess ? e : launch_d_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kValues, stream);
-    }
-    default: return hipErrorInvalidValue;
-  }
+  if (base == HG_BASE_MINMAX) return launch_d_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kBoth, stream);
+  if (base != HG_BASE_KIVI && base != HG_BASE_AKVQ) return hipErrorInvalidValue;
+  const hipError_t e = base == HG_BASE_KIVI ? launch_d_dim<HG_BASE_KIVI>(p, D, bits, Tensors::kKeys, stream)
+                                            : launch_d_dim<HG_BASE_AKVQ>(p, D, bits, Tensors::kKeys, stream);
+  return e != hipSuccess ? e : launch_d_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kValues, stream);
 }
 
 }  // namespace hg
