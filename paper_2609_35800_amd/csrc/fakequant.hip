@@ -215,7 +215,7 @@ template <int BASE, int D, int BITS, bool NORM>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWaves)))
 void fake_quantize_kernel(const Params p) {
   clear_words_share(p);
-  const Slice sl = decode_block(p, blockIdx.x);
+  const Slice sl = decode_launch_block(p, blockIdx.x);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   constexpr int kTokens = kFakeTokens<BASE, D>;
@@ -261,9 +261,13 @@ static hipError_t launch_f(const Params& p, Tensors which, bool norms, hipStream
   Params pf = p;
   pf.tiles = (p.n + kTile - 1) / kTile;
   const uint64_t per_tensor = (uint64_t)p.L * p.B * p.H * (uint64_t)pf.tiles;
-  const uint64_t blocks = which == Tensors::kBoth ? 2 * per_tensor : per_tensor;
+  const bool kept = which == Tensors::kKeptKeysAndValues;
+  const uint64_t blocks_k = which == Tensors::kValues ? 0
+                            : kept ? (uint64_t)(p.L * p.H - p.n_unprot_k) * p.B * pf.tiles : per_tensor;
+  const uint64_t blocks = which == Tensors::kKeys ? per_tensor : blocks_k + per_tensor;
   if (blocks > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
-  pf.blocks_k = which == Tensors::kValues ? 0u : (uint32_t)per_tensor;
+  pf.blocks_k = (uint32_t)blocks_k;
+  pf.kept_keys = kept;
   if constexpr (BASE == HG_BASE_AKVQ) {
     if (norms) {
       hipLaunchKernelGGL((fake_quantize_kernel<BASE, D, BITS, true>), dim3((uint32_t)blocks), dim3(kThreads), fake_lds<D>(),
@@ -300,10 +304,16 @@ static hipError_t launch_f_dim(const Params& p, int D, int bits, Tensors which, 
 // Value tiles of the KIVI-style and AKVQ-style bases run as a launch of the
 // min-max instantiation, which needs fewer registers than their key paths
 // (as in launch_quantize); with KIVI keys over the whole sequence the whole
-// launch does.
+// launch does, its key blocks listing the protected key slices alone (out of
+// place they are copied; in place they need nothing, and the launch takes the
+// values only).
 hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, bool norms, hipStream_t stream) {
-  if (base == HG_BASE_MINMAX || (base == HG_BASE_KIVI && p.kivi_whole))
-    return launch_f_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kBoth, norms, stream);
+  if (base == HG_BASE_KIVI && p.kivi_whole) {
+    const bool in_place = p.out[0] == p.cache[0];
+    return launch_f_dim<HG_BASE_MINMAX>(p, D, bits, in_place ? Tensors::kValues : Tensors::kKeptKeysAndValues,
+                                        norms, stream);
+  }
+  if (base == HG_BASE_MINMAX) return launch_f_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kBoth, norms, stream);
   if (base != HG_BASE_KIVI && base != HG_BASE_AKVQ) return hipErrorInvalidValue;
   hipError_t e = base == HG_BASE_KIVI ? launch_f_dim<HG_BASE_KIVI>(p, D, bits, Tensors::kKeys, norms, stream)
                                       : launch_f_dim<HG_BASE_AKVQ>(p, D, bits, Tensors::kKeys, norms, stream);

@@ -82,11 +82,17 @@ struct Params {
   // of the whole-sequence KIVI key kernel that follows in the same call)
   uint64_t* clear;
   uint32_t clear_words;
+  // 1: blocks [0, blocks_k) take only the protected key slices (k-th
+  // protected head, batch row, tile), so a launch that has nothing to do for
+  // the other key slices starts no workgroup for them
+  int32_t kept_keys = 0;
   Route route;
 };
 
 // Tensors a launch covers: K and V, or one of them.
-enum class Tensors { kBoth, kKeys, kValues };
+// kKeptKeysAndValues: the protected key slices, listed compactly (see
+// decode_launch_block), then every value slice.
+enum class Tensors { kBoth, kKeys, kValues, kKeptKeysAndValues };
 
 // Dispatch over (base, D, bits); return hipSuccess or the launch error.
 // With `norms`, the quantize kernel also writes the squared key norms (AKVQ).
@@ -191,6 +197,46 @@ __device__ __forceinline__ Slice decode_block(const Params& p, uint32_t bid) {
   r.b = sr.b;
   r.kept = sr.kept;
   r.slot = sr.slot;
+  return r;
+}
+
+// (l*H + h) of the k-th protected head (k < the number of protected heads):
+// the word holding it is the last one with at most k protected heads before
+// it (prefix[w], non-decreasing in w), so the number of words with
+// prefix[w] <= k, minus one; the lanes test 64 words at a time.
+__device__ __forceinline__ uint32_t kth_protected_head(const Params& p, uint32_t k) {
+  const uint32_t words = ((uint32_t)p.L * p.H + 31u) / 32u;
+  const uint32_t lane = threadIdx.x & 63u;
+  uint32_t count = 0;
+#pragma unroll
+  for (uint32_t w0 = 0; w0 < (uint32_t)kMaskWords; w0 += 64u) {
+    if (w0 >= words) break;
+    const uint32_t w = min(w0 + lane, words - 1u);
+    const bool le = w0 + lane < words && p.route.prefix[w] <= k;
+    count += (uint32_t)__popcll(__ballot(le));
+  }
+  const uint32_t lo = count - 1u;
+  uint32_t ones = p.route.mask[lo];
+  for (uint32_t j = k - p.route.prefix[lo]; j > 0; --j) ones &= ones - 1u;
+  return 32u * lo + (uint32_t)__builtin_ctz(ones);
+}
+
+// A block of a launch: with kept_keys, blocks [0, blocks_k) are the protected
+// key slices in (protected head, batch row, tile) order, and the rest are
+// value slices as in decode_block.
+__device__ __forceinline__ Slice decode_launch_block(const Params& p, uint32_t bid) {
+  if (!p.kept_keys || bid >= p.blocks_k) return decode_block(p, bid);
+  Slice r;
+  r.X = 0;
+  r.tile = (int)(bid % (uint32_t)p.tiles);
+  const uint32_t q = bid / (uint32_t)p.tiles;
+  r.b = (int)(q % (uint32_t)p.B);
+  const uint32_t k = q / (uint32_t)p.B;
+  const uint32_t i = kth_protected_head(p, k);
+  const uint32_t l = i / (uint32_t)p.H, h = i % (uint32_t)p.H;
+  r.s = (l * (uint32_t)p.B + (uint32_t)r.b) * (uint32_t)p.H + h;
+  r.kept = true;
+  r.slot = k;
   return r;
 }
 

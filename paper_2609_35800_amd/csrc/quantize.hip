@@ -231,7 +231,7 @@ __device__ __forceinline__ void quantize_kivi_keys(const uint16_t* __restrict__ 
 template <int BASE, int D, int BITS, bool NORM>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWaves))) void quantize_kernel(const Params p) {
   clear_words_share(p);
-  const Slice sl = decode_block(p, blockIdx.x);
+  const Slice sl = decode_launch_block(p, blockIdx.x);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int t_first = sl.tile * kBlockTokens + wave * kWaveTokens;
@@ -302,9 +302,13 @@ static hipError_t launch_q(const Params& p, Tensors which, bool norms, hipStream
   Params pq = p;
   pq.tiles = (p.n + kBlockTokens - 1) / kBlockTokens;
   const uint64_t per_tensor = (uint64_t)p.L * p.B * p.H * (uint64_t)pq.tiles;
-  const uint64_t blocks = which == Tensors::kBoth ? 2 * per_tensor : per_tensor;
+  const bool kept = which == Tensors::kKeptKeysAndValues;
+  const uint64_t blocks_k = which == Tensors::kValues ? 0
+                            : kept ? (uint64_t)(p.L * p.H - p.n_unprot_k) * p.B * pq.tiles : per_tensor;
+  const uint64_t blocks = which == Tensors::kKeys ? per_tensor : blocks_k + per_tensor;
   if (blocks > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
-  pq.blocks_k = which == Tensors::kValues ? 0u : (uint32_t)per_tensor;
+  pq.blocks_k = (uint32_t)blocks_k;
+  pq.kept_keys = kept;
   if constexpr (BASE == HG_BASE_AKVQ) {
     if (norms) {
       constexpr size_t kLdsNorm = quantize_lds<BASE, D, BITS, true>();
@@ -346,10 +350,14 @@ static hipError_t launch_q_dim(const Params& p, int D, int bits, Tensors which, 
 // and the key paths (KIVI groups, rotation) need more than the per-token
 // path, which would leave the value tiles with fewer waves per SIMD.  With
 // KIVI keys over the whole sequence this launch only copies protected keys
-// and quantizes values, so all of it runs as the min-max instantiation.
+// and quantizes values, so all of it runs as the min-max instantiation, its
+// key blocks listing the protected key slices alone (with every key slice
+// listed, the 7/8 that exit at once cost 36 us on the LLaVA-NeXT-shaped
+// cache).
 hipError_t launch_quantize(const Params& p, int base, int D, int bits, bool norms, hipStream_t stream) {
-  if (base == HG_BASE_MINMAX || (base == HG_BASE_KIVI && p.kivi_whole))
-    return launch_q_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kBoth, norms, stream);
+  if (base == HG_BASE_KIVI && p.kivi_whole)
+    return launch_q_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kKeptKeysAndValues, norms, stream);
+  if (base == HG_BASE_MINMAX) return launch_q_dim<HG_BASE_MINMAX>(p, D, bits, Tensors::kBoth, norms, stream);
   if (base != HG_BASE_KIVI && base != HG_BASE_AKVQ) return hipErrorInvalidValue;
   hipError_t e = base == HG_BASE_KIVI ? launch_q_dim<HG_BASE_KIVI>(p, D, bits, Tensors::kKeys, norms, stream)
                                       : launch_q_dim<HG_BASE_AKVQ>(p, D, bits, Tensors::kKeys, norms, stream);
