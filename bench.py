@@ -42,10 +42,49 @@ KERNEL_SOURCES = {
 }
 KIVI_WHOLE_SOURCE = _CSRC + "kivi_seq.hip"
 RETAIN_SOURCE = _CSRC + "retain.hip"
-# The measured-results table: the five workloads, the 72B-shaped one at each bit
-# width (name, bits).
-TABLE_WORKLOADS = (("tiny", None), ("qwen2.5-vl-7b", None), ("llava-next-7b", None), ("internvl-8b", None),
-                   ("72b-long", 2), ("72b-long", 3), ("72b-long", 4))
+# The measured-results table: the five workloads (the 72B-shaped one at each
+# bit width), the whole-sequence KIVI keys and the 2 % token retention, each as
+# a quantize + dequantize step, and the one-pass mode on three of them:
+# (workload, option overrides, op).
+TABLE_ROWS = (
+    ("tiny", {}, "step"), ("qwen2.5-vl-7b", {}, "step"), ("llava-next-7b", {}, "step"),
+    ("internvl-8b", {}, "step"), ("72b-long", {"bits": 2}, "step"), ("72b-long", {"bits": 3}, "step"),
+    ("72b-long", {"bits": 4}, "step"), ("llava-next-7b", {"kivi_group": 0}, "step"),
+    ("internvl-8b", {"retain_permille": 20}, "step"),
+    ("qwen2.5-vl-7b", {}, "fakequant"), ("llava-next-7b", {"kivi_group": 0}, "fakequant"),
+    ("internvl-8b", {"retain_permille": 20}, "fakequant"),
+)
+
+
+def table_label(name: str, over: dict, op: str) -> str:
+    parts = [name]
+    if "bits" in over:
+        parts.append(f"{over['bits']}-bit")
+    if over.get("kivi_group") == 0:
+        parts.append("whole-sequence keys")
+    if over.get("retain_permille"):
+        parts.append(f"{over['retain_permille'] / 10:g} % retention")
+    if op == "fakequant":
+        parts.append("one-pass")
+    return ", ".join(parts)
+
+
+def table_parity_test(name: str, over: dict, op: str) -> str:
+    """The full-size GPU test that compares every slice of the row's call
+    with the oracle."""
+    if over.get("kivi_group") == 0:
+        return ("tests/test_gpu_kivi_whole.py::test_full_size_llava_one_pass[False]" if op == "fakequant"
+                else "tests/test_gpu_kivi_whole.py::test_full_size_llava")
+    if over.get("retain_permille"):
+        return ("tests/test_gpu_retain.py::test_full_size_internvl_two_percent_one_pass[False]" if op == "fakequant"
+                else "tests/test_gpu_retain.py::test_full_size_internvl_two_percent")
+    if op == "fakequant":
+        return f"tests/test_gpu_workloads.py::test_one_pass_out_of_place[{name}]"
+    if name == "72b-long":
+        return f"tests/test_gpu_workloads.py::test_72b_long_bit_sweep[{over['bits']}]"
+    return f"tests/test_gpu_workloads.py::test_workload[{name}]"
+
+
 RESULTS_DOC = "BASELINE.md"  # the document whose results section --fill-baseline writes
 RESULTS_HEADER = "## 4. Measured results"
 
@@ -227,19 +266,19 @@ def cpu_baseline(w, K, V, mask, budget_s: float, threads: int = 0):
         t0 = time.perf_counter()
         pk = oracle.quantize(cfg, Kb, Vb, m, threads=threads)
         oracle.dequantize(cfg, m, pk, Ko, Vo, threads=threads)
-        return time.perf_counter() - t0, pk
+        return time.perf_counter() - t0
 
     sub, cfg, m, Kb, Vb = prepare(1)
-    dt1, _ = one_pass(cfg, m, Kb, Vb, np.zeros_like(Kb), np.zeros_like(Vb))
+    dt1 = one_pass(cfg, m, Kb, Vb, np.zeros_like(Kb), np.zeros_like(Vb))
     nl = int(max(1, min(w.L, budget_s / max(dt1, 1e-6))))
     sub, cfg, m, Kb, Vb = prepare(nl)
     Ko, Vo = np.zeros_like(Kb), np.zeros_like(Vb)
     total, passes = 0.0, 0
     while passes == 0 or total < budget_s:
-        dt, pk = one_pass(cfg, m, Kb, Vb, Ko, Vo)
+        dt = one_pass(cfg, m, Kb, Vb, Ko, Vo)
         total += dt
         passes += 1
-    ab = algorithmic_bytes(sub, {n: int(v.nbytes) for n, v in pk.items()})
+    ab = algorithmic_bytes(sub, oracle.sizes(cfg, m))
     per_pass = total / passes
     return {"value": round((ab["quant"] + ab["dequant"]) / per_pass / 1e9, 4), "unit": "GB/s",
             "cores": threads, "kind": "oracle", "cpu_model": cpu_model(),
@@ -337,59 +376,74 @@ def bench_fakequant(args, hg, w, cfg, mask, K, V):
 
 
 def measure_table(args) -> None:
-    """The measured-results table: for each workload, the median
-    quantize and dequantize call times over `steps` calls (HIP events on the
-    launch stream, inputs resident in HBM), the GB/s and image tokens/s they
-    give, the committed counter ratios, and the oracle on the host cores
-    (one thread and all of them, quantize + dequantize)."""
+    """The measured-results table: for each row, the median quantize and
+    dequantize call times (or the one-pass call's, out of place) over `steps`
+    calls (HIP events on the launch stream, inputs resident in HBM), the GB/s
+    and image tokens/s they give, the committed counter ratios, and the oracle
+    on the host cores (one thread and all of them, quantize + dequantize, which
+    is also what the one-pass mode computes)."""
     import torch
     import paper_2609_35800_amd as hg
     import synthkv
     stream = torch.cuda.current_stream()
-    rows = []
-    for name, bits in TABLE_WORKLOADS:
-        w = synthkv.WORKLOADS[name]
-        if bits is not None:
-            w = w.with_(bits=bits)
+    rows, oracle_runs = [], {}
+    for name, over, op in TABLE_ROWS:
+        w = synthkv.WORKLOADS[name].with_(**over)
         mask = synthkv.protect_mask(w)
         cfg = hg.make_config(**w.config_fields())
         sizes = hg.hg_packed_sizes(cfg, mask)
-        ab = algorithmic_bytes(w, sizes)
         K, V = synthkv.gen_kv(w, device="cuda")
-        packed = hg.alloc_packed(cfg, mask)
         Ko, Vo = torch.empty_like(K), torch.empty_like(V)
+        if op == "fakequant":  # out of place, as bench_fakequant
+            ws = hg.alloc_fake_workspace(cfg, mask)
+            run = lambda: hg.hg_fake_quantize(cfg, K, V, mask, Ko, Vo, ws, stream=stream)  # noqa: E731
+            calls = (("hg_fake_quantize", fake_quantize_bytes(w, sizes), FAKE_KERNEL),)
+        else:
+            ab = algorithmic_bytes(w, sizes)
+            packed = hg.alloc_packed(cfg, mask)
+            q = lambda: hg.hg_quantize(cfg, K, V, mask, packed, stream=stream)  # noqa: E731
+            d = lambda: hg.hg_dequantize(cfg, mask, packed, Ko, Vo, stream=stream)  # noqa: E731
+            calls = (("hg_quantize", ab["quant"], QUANT_KERNEL), ("hg_dequantize", ab["dequant"], DEQUANT_KERNEL))
         ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
         for _ in range(args.warmup):
-            hg.hg_quantize(cfg, K, V, mask, packed, stream=stream)
-            hg.hg_dequantize(cfg, mask, packed, Ko, Vo, stream=stream)
+            if op == "fakequant":
+                run()
+            else:
+                q()
+                d()
         for e0, e1, e2 in ev:
             e0.record(stream)
-            hg.hg_quantize(cfg, K, V, mask, packed, stream=stream)
+            if op == "fakequant":
+                run()
+            else:
+                q()
             e1.record(stream)
-            hg.hg_dequantize(cfg, mask, packed, Ko, Vo, stream=stream)
+            if op != "fakequant":
+                d()
             e2.record(stream)
         torch.cuda.synchronize()
-        q_ms = float(np.median([a.elapsed_time(b) for a, b, _ in ev]))
-        d_ms = float(np.median([b.elapsed_time(c) for _, b, c in ev]))
-        cb_n = cpu_baseline(w, K, V, mask, args.cpu_seconds / 2)
-        cb_1 = cpu_baseline(w, K, V, mask, args.cpu_seconds / 4, threads=1)
-        label = w.name + (f", {w.bits}-bit" if bits is not None else "")
-        for call, ms, nbytes, kernel in (("hg_quantize", q_ms, ab["quant"], QUANT_KERNEL),
-                                         ("hg_dequantize", d_ms, ab["dequant"], DEQUANT_KERNEL)):
+        times = [float(np.median([a.elapsed_time(b) for a, b, _ in ev])),
+                 float(np.median([b.elapsed_time(c) for _, b, c in ev]))]
+        key = (name, tuple(sorted(over.items())))
+        if key not in oracle_runs:  # the one-pass rows reuse their step row's oracle timing
+            oracle_runs[key] = (cpu_baseline(w, K, V, mask, args.cpu_seconds / 2),
+                                cpu_baseline(w, K, V, mask, args.cpu_seconds / 4, threads=1))
+        cb_n, cb_1 = oracle_runs[key]
+        label = table_label(name, over, op)
+        for (call, nbytes, kernel), ms in zip(calls, times):
             rec = traffic_record(w, kernel)
             rows.append({
-                "config": label, "workload": w.name, "bits": w.bits, "call": call,
+                "config": label, "workload": w.name, "bits": w.bits, "overrides": over, "op": op, "call": call,
                 "median_ms": round(ms, 4), "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
                 "pct_of_peak": round(100 * nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 1),
                 "bytes": nbytes, "traffic_ratio": rec.get("ratio_to_algorithmic") if rec else None,
                 "image_tokens_per_s": round(w.B * w.img_len / (ms * 1e-3), 1),
                 "oracle_1_thread_GBps": cb_1["value"], "oracle_n_thread_GBps": cb_n["value"],
                 "oracle_threads": cb_n["cores"], "oracle_sample": cb_n["sample"],
-                "parity_test": (f"tests/test_gpu_workloads.py::test_72b_long_bit_sweep[{w.bits}]"
-                                if name == "72b-long" else f"tests/test_gpu_workloads.py::test_workload[{name}]"),
+                "parity_test": table_parity_test(name, over, op),
             })
-        print(json.dumps(rows[-2]), flush=True)
-        del K, V, Ko, Vo, packed
+            print(json.dumps(rows[-1]), flush=True)
+        del K, V, Ko, Vo
         torch.cuda.empty_cache()
     out = {"rows": rows, "steps": args.steps, "warmup": args.warmup, "cpu_model": cpu_model(),
            "host_cores": os.cpu_count(), "date": time.strftime("%Y-%m-%d")}
@@ -409,18 +463,20 @@ def fill_baseline(path: str) -> None:
              f"({t['date']}; median of {t['steps']} calls after {t['warmup']} warm-up steps, HIP events on the "
              "launch stream, inputs resident in HBM; bytes are the algorithmic bytes of `bench.py`). Counter "
              "ratios come from the committed rocprofv3 records under `profiles/` when they were taken on the "
-             "current kernel sources. The oracle columns time the CPU oracle (quantize + dequantize, same "
-             f"byte count) on the box's host ({t['cpu_model']}): one thread, and one per core "
+             "current kernel sources. The oracle columns time the CPU oracle (quantize + dequantize, the "
+             "step's byte count; for the one-pass rows too, since that mode computes the dequantize of the "
+             f"quantize) on the box's host ({t['cpu_model']}): one thread, and one per core "
              f"(N = {t['rows'][0]['oracle_threads']}). Parity: every slice compared with the oracle, bit for "
              "bit, by the GPU test named.", "",
              "| Config | Call | Median time | GB/s | % of 8 TB/s | rocprof bytes ÷ algorithmic bytes | "
              "Image tokens/s | Oracle 1-thread | Oracle N-thread | Parity |",
              "|---|---|---|---|---|---|---|---|---|---|"]
     import synthkv
+    kernels = {"hg_quantize": QUANT_KERNEL, "hg_dequantize": DEQUANT_KERNEL, "hg_fake_quantize": FAKE_KERNEL}
     for r in t["rows"]:
         # counter ratios from the records committed now (taken on the current sources)
-        w = synthkv.WORKLOADS[r["workload"]].with_(bits=r["bits"])
-        rec = traffic_record(w, QUANT_KERNEL if r["call"] == "hg_quantize" else DEQUANT_KERNEL)
+        w = synthkv.WORKLOADS[r["workload"]].with_(**r.get("overrides", {"bits": r["bits"]}))
+        rec = traffic_record(w, kernels[r["call"]])
         r["traffic_ratio"] = rec.get("ratio_to_algorithmic") if rec else None
         lines.append(f"| {r['config']} | `{r['call']}` | {r['median_ms'] * 1e3:.1f} µs | {r['GBps']:,.0f} | "
                      f"{r['pct_of_peak']:.1f} | {fmt(r['traffic_ratio'], '.4f')} | "
