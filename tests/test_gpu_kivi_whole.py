@@ -63,6 +63,18 @@ def test_full_size_llava_one_pass(inplace):
     wholecache.assert_whole(wholecache.fake_quantize(w, inplace=inplace), w)
 
 
+def test_long_single_slice():
+    """One key slice of 2^21 + 5 tokens at head_dim 128 (512 MiB, text rows at
+    both ends): far past eight workgroups' capacity, so the two-pass kernel
+    ranges and codes it alone; every byte against the oracle."""
+    T = (1 << 21) + 5
+    w = synthkv.Workload("kiviseq-long-slice", L=1, B=1, H=1, T=T, D=128, img_start=1000, img_len=T - 1777,
+                         bits=2, base="kivi", keys_only=0, n_protected=0, k_outliers=4, k_outlier_scale=10.0,
+                         kivi_group=0, seed=21)
+    assert T > 8 * capacity(128)
+    wholecache.assert_whole(wholecache.quantize_dequantize(w), w)
+
+
 def capacity(D):
     """Rows one workgroup of the partitioned kernel holds."""
     return 24 * 8192 // D
