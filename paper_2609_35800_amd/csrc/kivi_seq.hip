@@ -7,9 +7,10 @@
 // slice, so a slice must be fully read before any of its codes is formed.
 // Two kernels:
 //
-// Partitioned resident kernel (T at most 8 workgroups' capacity): a
+// Partitioned resident kernel (T at most 32 workgroups' capacity): a
 // persistent grid of 1024-thread workgroups, one per compute unit.  A group of
-// P workgroups takes one key slice (l, b, h) at a time; workgroup q of the
+// P workgroups (past 8, rounded up to 16 or 32, so that the groups fill every
+// compute unit) takes one key slice (l, b, h) at a time; workgroup q of the
 // group holds rows [q R, (q + 1) R) of the slice, every channel, on chip (9
 // row slots in LDS filled by buffer loads that write LDS directly, 15 in
 // registers), so each slice is read from HBM exactly once:
@@ -20,9 +21,11 @@
 //     workspace: each workgroup publishes its range of each channel as one
 //     64-bit word, the BF16 minimum and maximum tagged with the slice's
 //     sequence number in the group (relaxed device-scope atomics; a tagged
-//     word carries its own values, so no fence is needed), and polls each
-//     partner's word of the channel, a bounded number of times, until it
-//     carries that tag; two buffers alternate between consecutive slices,
+//     word carries its own values, so no fence is needed); every thread
+//     polls some partners' words of one channel (1024 / D threads per
+//     channel share the partners), a bounded number of times, until they
+//     carry that tag, and folds them into the workgroup's range in LDS; two
+//     buffers alternate between consecutive slices,
 //     and the words start at zero (cleared by the call's first kernel, the
 //     values' quantize or one-pass launch, or else by a kernel of their own);
 //  3. codes (or, for the one-pass simulated quantization, the BF16
@@ -185,7 +188,8 @@ constexpr int kPartWaves = kPartThreads / 64;
 constexpr int kPartLdsSlots = 9;
 constexpr int kPartRegSlots = 15;
 constexpr int kPartSlots = kPartLdsSlots + kPartRegSlots;
-constexpr int kMaxPartners = 8;
+constexpr int kMaxPartners = 32;    // a group's partners share one XCD's 32 compute units
+constexpr int kSerialPartners = 8;  // up to this many, one thread per channel polls every partner
 // Exchange area (u64 words): a header (word 0 counts waits that ran out of
 // polls), then [group][2 buffers][partner][D] tagged words for at most
 // kExMaxWgs workgroups.
@@ -314,7 +318,10 @@ __device__ __forceinline__ void fold_partner(const uint64_t* w, uint32_t gen, fl
   b = fmaxf(b, __uint_as_float((uint32_t)v & 0xFFFF0000u));
 }
 
-template <int D, int BITS, bool FAKE>
+// WIDE (more than kSerialPartners partners): every thread of the workgroup
+// polls partners; else one thread per channel polls them all (its own
+// instantiation, so the common case keeps the smaller register footprint).
+template <int D, int BITS, bool FAKE, bool WIDE>
 __global__ __launch_bounds__(kPartThreads) __attribute__((amdgpu_waves_per_eu(4)))
 void kivi_part_kernel(const Params p, uint32_t n_items, uint32_t groups, uint32_t parts, uint32_t rows_per_part,
                       uint64_t* __restrict__ ex) {
@@ -437,11 +444,33 @@ void kivi_part_kernel(const Params p, uint32_t n_items, uint32_t groups, uint32_
     __syncthreads();
     // 2. the slice's range from the partners' partial ranges, and its scales
     const size_t slab = (size_t)item;  // [slot][B] with slot = item / B
+    if constexpr (WIDE) {
+      // Each thread polls every (kPartThreads / D)-th partner for one channel
+      // and folds what it found into the workgroup's range in LDS (min and
+      // max are idempotent, so a published range that already holds some
+      // partners' values is still exact).
+      const uint32_t gen = seq + 1;
+      uint64_t* buf = ex + kExHeader + ((size_t)g * 2u + (seq & 1u)) * parts * D;
+      if (tid < D)
+        __hip_atomic_store(buf + (size_t)q * D + tid, tagged_range(red[tid], red[D + tid], gen), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      const int chx = tid % D;
+      float a = __builtin_inff(), b = -__builtin_inff();
+      uint32_t timeouts = 0;
+      for (uint32_t r = (uint32_t)tid / D; r < parts; r += kPartThreads / D)
+        if (r != q) fold_partner(buf + (size_t)r * D + chx, gen, a, b, timeouts);
+      if (timeouts) __hip_atomic_fetch_add(ex, (uint64_t)timeouts, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (a <= b) {
+        atomicMin(&red[chx], a);
+        atomicMax(&red[D + chx], b);
+      }
+      __syncthreads();
+    }
     if (tid < D) {
       float a = red[tid], b = red[D + tid];
       red[tid] = __builtin_inff();  // reset for the next slice (several barriers away)
       red[D + tid] = -__builtin_inff();
-      if (parts > 1) {
+      if (!WIDE && parts > 1) {
         const uint32_t gen = seq + 1;
         uint64_t* buf = ex + kExHeader + ((size_t)g * 2u + (seq & 1u)) * parts * D;
         __hip_atomic_store(buf + (size_t)q * D + tid, tagged_range(a, b, gen), __ATOMIC_RELAXED,
@@ -552,10 +581,16 @@ __global__ void zero_words_kernel(uint64_t* w, uint32_t n) {
 
 int kivi_part_capacity(int D) { return kPartSlots * kPartWaves * (512 / D); }
 
+// Workgroups per slice of the resident kernel, 0 for the two-pass kernel.  A
+// grid holds 8 groups per 8 P workgroups, so past 8 partners P is rounded up
+// to 16 or 32, which fill every compute unit; each partner keeps at least one
+// row ((P - 1) ceil(T / P) < T holds for T > (P - 1)^2).
 int kivi_partners(int T, int D) {
   const int cap = kivi_part_capacity(D);
-  const int parts = (T + cap - 1) / cap;
+  int parts = (T + cap - 1) / cap;
   if (parts > kMaxPartners || (uint64_t)T * D * 2 >= (1ull << 31)) return 0;  // two-pass kernel
+  if (parts > kSerialPartners) parts = parts <= 16 ? 16 : 32;
+  if ((uint64_t)(parts - 1) * (uint64_t)((T + parts - 1) / parts) >= (uint64_t)T) return 0;
   return parts;
 }
 
@@ -600,17 +635,21 @@ static hipError_t plan_k(const Params& p, bool has_ws, KiviPlan* pl) {
   const int parts = kivi_partners(p.T, D);
   if (parts > 0 && (parts == 1 || has_ws)) {
     int per_cu = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kivi_part_kernel<D, BITS, FAKE>, kPartThreads, 0);
+    e = parts > kSerialPartners
+            ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kivi_part_kernel<D, BITS, FAKE, true>, kPartThreads, 0)
+            : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kivi_part_kernel<D, BITS, FAKE, false>, kPartThreads,
+                                                           0);
     if (e != hipSuccess) return e;
     const uint32_t resident = (uint32_t)std::max(per_cu, 0) * (uint32_t)cus;  // workgroups held at once
     uint32_t cap = resident / (uint32_t)parts;
     if (parts > 1) cap = std::min(cap, (uint32_t)(kExMaxWgs / parts));
     cap = cap / 8u * 8u;
-    if (cap > 0) {
+    const uint32_t rows_per_part = (uint32_t)((p.T + parts - 1) / parts);
+    if (cap > 0 && rows_per_part <= (uint32_t)kivi_part_capacity(D)) {  // every row fits a slot
       pl->resident = true;
       pl->parts = parts;
       pl->groups = std::min((pl->n_items + 7u) / 8u * 8u, cap);
-      pl->rows_per_part = (uint32_t)((p.T + parts - 1) / parts);
+      pl->rows_per_part = rows_per_part;
       if (parts > 1) pl->clear_words = (uint32_t)(kExHeader + (uint64_t)pl->groups * 2 * parts * D);
       return hipSuccess;
     }
@@ -631,8 +670,13 @@ static hipError_t launch_k(const Params& p, void* ws, bool cleared, hipStream_t 
     if (e != hipSuccess) return e;
   }
   if (pl.resident) {
-    hipLaunchKernelGGL((kivi_part_kernel<D, BITS, FAKE>), dim3(pl.groups * (uint32_t)pl.parts), dim3(kPartThreads),
-                       0, stream, p, pl.n_items, pl.groups, (uint32_t)pl.parts, pl.rows_per_part, (uint64_t*)ws);
+    const dim3 grid(pl.groups * (uint32_t)pl.parts);
+    if (pl.parts > kSerialPartners)
+      hipLaunchKernelGGL((kivi_part_kernel<D, BITS, FAKE, true>), grid, dim3(kPartThreads), 0, stream, p, pl.n_items,
+                         pl.groups, (uint32_t)pl.parts, pl.rows_per_part, (uint64_t*)ws);
+    else
+      hipLaunchKernelGGL((kivi_part_kernel<D, BITS, FAKE, false>), grid, dim3(kPartThreads), 0, stream, p, pl.n_items,
+                         pl.groups, (uint32_t)pl.parts, pl.rows_per_part, (uint64_t*)ws);
     return hipGetLastError();
   }
   int cus = 0;

@@ -4,14 +4,15 @@ against the oracle: codes, metadata, side store and reconstruction
 bit-exact for quantize / dequantize and for the one-pass simulated
 quantization; every slice of the full LLaVA-NeXT-7B-shaped cache.
 
-Slices of up to 8 workgroups' capacity (24 slots of 8192/D rows: 3072,
+Slices of up to 32 workgroups' capacity (24 slots of 8192/D rows: 3072,
 1536 and 768 rows at head_dim 64, 128 and 256) go through the partitioned
 resident kernel: P workgroups each hold a run of a slice's rows on chip and
-combine their partial ranges through the call's workspace; longer slices go
-through the two-pass kernel.  Covered: one to eight workgroups per slice and
-the capacity boundaries, several slices per group (with the grid shrunk
-through the HG_TEST_CUS hook), identical bytes for different grid sizes, and
-no exchange wait running out of polls."""
+combine their partial ranges through the call's workspace (past 8, P is
+rounded up to 16 or 32); longer slices go through the two-pass kernel.
+Covered: one to eight, 16 and 32 workgroups per slice and the capacity
+boundaries, several slices per group (with the grid shrunk through the
+HG_TEST_CUS hook), identical bytes for different grid sizes, and no exchange
+wait running out of polls."""
 import numpy as np
 import pytest
 import torch
@@ -65,7 +66,7 @@ def test_full_size_llava_one_pass(inplace):
 
 def test_long_single_slice():
     """One key slice of 2^21 + 5 tokens at head_dim 128 (512 MiB, text rows at
-    both ends): far past eight workgroups' capacity, so the two-pass kernel
+    both ends): far past 32 workgroups' capacity, so the two-pass kernel
     ranges and codes it alone; every byte against the oracle."""
     T = (1 << 21) + 5
     w = synthkv.Workload("kiviseq-long-slice", L=1, B=1, H=1, T=T, D=128, img_start=1000, img_len=T - 1777,
@@ -119,8 +120,9 @@ def test_grid_size_does_not_change_the_bytes(cus, monkeypatch):
 
 
 # Slices at each workgroup count's capacity and one row past it (one to eight
-# workgroups per slice; past eight, the two-pass kernel), spans at the
-# start, in the middle and at the end of the slice.
+# workgroups per slice, then 16 and 32; past 32 workgroups' capacity, the
+# two-pass kernel), spans at the start, in the middle and at the end of the
+# slice (the middle only for the longest slices).
 def _boundary_cases():
     out = []
     for D in (64, 128, 256):
@@ -128,6 +130,8 @@ def _boundary_cases():
         for T in (c, c + 1, 2 * c + 1, 3 * c - 5, 8 * c, 8 * c + 1):
             for img_start, img_len in ((0, T), (T // 3, T // 2), (T - 40, 40)):
                 out.append((D, T, img_len, img_start))
+        for T in (16 * c, 16 * c + 1, 32 * c, 32 * c + 1):
+            out.append((D, T, T // 2, T // 3))
     return out
 
 
@@ -142,7 +146,7 @@ def test_capacity_boundary(D, T, img_len, img_start):
     _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), f"D{D}-T{T}-n{img_len}-s{img_start}")
 
 
-@pytest.mark.parametrize("T", [1536, 1537, 3008, 12288, 12289])
+@pytest.mark.parametrize("T", [1536, 1537, 3008, 12288, 12289, 24577, 49152, 49153])
 @pytest.mark.parametrize("inplace", [False, True])
 def test_capacity_boundary_fake(T, inplace):
     w = small("kivi", 128, 2, 1, img_len=T - 60, img_start=20, text=40,

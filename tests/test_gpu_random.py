@@ -28,7 +28,7 @@ def draw(i: int) -> synthkv.Workload:
         L, B, H = 1, int(rng.integers(1, 3)), int(rng.integers(1, 4))
         # one workgroup holds 24 slots of 512 / D rows per wavefront, 16
         # wavefronts: up to 1.2x, 2.5x or 9x that (several partners per
-        # slice, and past eight, the two-pass kernel)
+        # slice, and past eight, 16 workgroups per slice)
         rows = 24 * 16 * (512 // D)
         T = int(rng.integers(1, int(rows * float(rng.choice([1.2, 2.5, 9.0])))))
     else:
