@@ -4,7 +4,8 @@ and in place) is captured once (the calls only launch kernels on the given
 stream: no allocation, no synchronisation, no memset) and replayed several
 times, with the outputs cleared by eager work in between; every replay must
 write exactly the bytes of the eager calls.  Covers the per-token, KIVI
-(grouped and whole-sequence) and AKVQ-with-retention paths."""
+(grouped and whole-sequence, with one, 2 and 16 workgroups per slice) and
+AKVQ-with-retention paths."""
 import numpy as np
 import pytest
 import torch
@@ -16,6 +17,10 @@ pytestmark = pytest.mark.gpu
 
 CASES = [small("minmax", img_len=300), small("kivi", keys_only=1, img_len=300),
          small("kivi", img_len=300).with_(kivi_group=0, name="kivi-whole"),
+         # whole-sequence keys held by 2 and by 16 workgroups per slice (the
+         # exchange words cleared inside the graph on every replay)
+         small("kivi", img_len=3000, H=2).with_(kivi_group=0, name="kivi-whole-2-partners"),
+         small("kivi", img_len=12500, L=1, H=2, n_protected=1).with_(kivi_group=0, name="kivi-whole-16-partners"),
          small("akvq", img_len=300).with_(retain_permille=50, name="akvq-retain")]
 
 
@@ -75,7 +80,8 @@ def test_capture_one_pass(w, inplace):
     K, V = K0.clone(), V0.clone()
     Ko, Vo = (K, V) if inplace else (torch.zeros_like(K), torch.zeros_like(V))
     ws = hg.alloc_fake_workspace(cfg, mask)
-    assert (ws is not None) == (w.retain_permille > 0)
+    # retention's lists, or the exchange area of several workgroups per slice
+    assert (ws is not None) == (w.retain_permille > 0 or "partners" in w.name)
 
     def reset():
         K.copy_(K0)

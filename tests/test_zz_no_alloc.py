@@ -51,10 +51,11 @@ def _one_pass(hg, w, mask, inplace, noalloc):
 
 def _kivi_whole(big):
     # the workgroups holding a slice exchange their partial ranges through the
-    # workspace (4 MiB at head_dim 128)
+    # workspace (2 MiB at head_dim 128): 2 workgroups per slice on the larger
+    # cache, 16 on the smaller one
     if big:
         return synthkv.WORKLOADS["llava-next-7b"].with_(kivi_group=0, L=8)
-    w = small("kivi", D=128, bits=2, img_len=1700, img_start=5, text=11, L=2, B=2, H=4, n_protected=1)
+    w = small("kivi", D=128, bits=2, img_len=12500, img_start=5, text=11, L=1, B=2, H=2, n_protected=1)
     return w.with_(kivi_group=0, name="small-kivi-whole")
 
 
