@@ -74,7 +74,9 @@
  * KIVI keys over the whole sequence (kivi_group = 0): when a key slice is
  * longer than one workgroup holds on chip, several co-resident workgroups
  * hold it together and exchange partial ranges through the caller's
- * workspace, waiting for one another (a bounded number of polls).  The
+ * workspace, waiting for one another (a bounded number of polls); past 32
+ * workgroups' rows, chunks of each slice merge their ranges into the same
+ * workspace with atomics and a second launch writes the codes.  The
  * kernel is sized to be resident on an otherwise idle device: a kernel
  * running concurrently on another stream can delay it, and one that keeps
  * compute units busy long enough makes waits run out (the workspace's first
@@ -140,7 +142,9 @@ typedef struct {
   uint64_t norm_k, ret_idx, ret_k, ret_v;  /* bytes; 0 without token retention    */
   uint64_t workspace;          /* bytes of hg_quantize's workspace: the exchange
                                   area of KIVI keys over the whole sequence when
-                                  a slice spans several workgroups; else 0      */
+                                  a slice is longer than one workgroup holds
+                                  (3072 / 1536 / 768 rows at D = 64 / 128 /
+                                  256) and some key is quantized; else 0      */
   uint64_t fake_workspace;     /* bytes of hg_fake_quantize's workspace: the key
                                   norms, token lists and (in place) saved rows
                                   of token retention, or the same exchange area

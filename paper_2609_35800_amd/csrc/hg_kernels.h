@@ -103,12 +103,14 @@ hipError_t launch_fake_quantize(const Params& p, int base, int D, int bits, bool
 // slices; each slice is held on chip by a group of workgroups (each a run of
 // its rows, every channel) that combine their partial ranges through the
 // exchange workspace `ws` (kivi_workspace_bytes; unused with one workgroup
-// per slice), or, for longer slices, a range pass and a code pass per slice.
+// per slice), or, for longer slices, a range launch over chunks of every
+// slice merging into `ws` and a code launch (without `ws`: a range pass and a
+// code pass per slice by one workgroup).
 // `cleared`: the words kivi_seq_clear_words gives were set to zero by an
 // earlier launch of the call (else the launch clears them itself).
 hipError_t launch_kivi_seq(const Params& p, int D, int bits, bool fake, void* ws, bool cleared, hipStream_t stream);
 hipError_t kivi_seq_clear_words(const Params& p, int D, int bits, bool fake, void* ws, uint32_t* words);
-// Workgroups per slice of the resident kernel (0: the two-pass kernel), and
+// Workgroups per slice of the resident kernel (0: the split kernels), and
 // the exchange workspace bytes a call with T rows per slice needs (0: none).
 int kivi_partners(int T, int D);
 uint64_t kivi_workspace_bytes(int T, int D);

@@ -5,7 +5,7 @@
 //
 // Every code depends on the range of its channel over all T rows of the
 // slice, so a slice must be fully read before any of its codes is formed.
-// Two kernels:
+// Three forms:
 //
 // Partitioned resident kernel (T at most 32 workgroups' capacity): a
 // persistent grid of 1024-thread workgroups, one per compute unit.  A group of
@@ -38,12 +38,18 @@
 // counted in the workspace's first word.  (Two 512-thread workgroups per
 // compute unit, each holding half as many rows, measured 1 % slower.)
 //
-// Two-pass kernel (longer slices): a persistent grid of kSeqBlocksPerCU
-// workgroups of kSeqThreads threads per compute unit walks the key slices;
-// per slice a range pass over all T rows, the wavefronts' partial ranges
-// combined through LDS, then a second pass over the image rows for the codes.
-// The grid is sized so that the slices in flight at once stay within the
-// 256 MB Infinity Cache, which then serves much of the second read.
+// Split kernels (longer slices, or too few compute units for a group of
+// eight): a range launch over chunks of every slice, whose per-channel ranges
+// are merged into the workspace by atomic maxima, then a code launch over
+// chunks of the image rows; each slice is read twice, but every compute unit
+// works on it.
+//
+// Two-pass kernel (a slice one workgroup holds, with no workspace, on a
+// device of fewer than 8 compute units): a persistent grid of
+// kSeqBlocksPerCU workgroups of kSeqThreads threads per compute unit walks
+// the key slices; per slice a range pass over all T rows, the wavefronts'
+// partial ranges combined through LDS, then a second pass over the image rows
+// for the codes.
 //
 // Values, protected slices and the rest of the cache are handled by the
 // regular kernels of the same call.
@@ -62,34 +68,32 @@ constexpr int kSeqBlocksPerCU = 2;
 constexpr int kSeqUnroll1 = 4;  // rows in flight per lane, range pass
 constexpr int kSeqUnroll2 = 4;  // rows in flight per lane, code pass
 
-template <int D, int BITS, bool FAKE, int WAVES>
-__device__ __forceinline__ void kivi_seq_slice(const Params& p, uint32_t s, const SliceRoute& route,
-                                               float (&part)[2][WAVES][D]) {
+// Per-channel range, over rows [t_begin, t_end) of a slice, of the 8
+// channels this lane loads (lane i: channels 8 (i % (D/8)) on, row i / (D/8)
+// of each WAVES * 64 / (D/8) rows), reduced over the wavefront's rows by
+// shuffles; rows past the end re-read the last row, which leaves the range
+// unchanged.  t_end > t_begin.
+template <int D, int WAVES, int U = kSeqUnroll1>
+__device__ __forceinline__ void range_rows(const uint16_t* __restrict__ slice, int t_begin, int t_end, float (&mn)[8],
+                                           float (&mx)[8]) {
   constexpr int CPT = D / 8;
   constexpr int RPL = 64 / CPT;
   constexpr int STEP = WAVES * RPL;
-  constexpr int LEVELS = (1 << BITS) - 1;
-  constexpr int ROW = D * BITS / 8;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c8 = lane % CPT;
-  const int r = lane / CPT;
-  const uint16_t* slice = p.cache[0] + (size_t)s * p.T * D;
-
-  // 1. ranges over all T rows
-  float mn[8], mx[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     mn[e] = __builtin_inff();
     mx[e] = -__builtin_inff();
   }
-  for (int t0 = wave * RPL + r; t0 < p.T; t0 += kSeqUnroll1 * STEP) {
-    u32x4 v[kSeqUnroll1];
+  for (int t0 = t_begin + wave * RPL + lane / CPT; t0 < t_end; t0 += U * STEP) {
+    u32x4 v[U];
 #pragma unroll
-    for (int u = 0; u < kSeqUnroll1; ++u) v[u] = *(const u32x4*)(slice + (size_t)min(t0 + u * STEP, p.T - 1) * D + 8 * c8);
+    for (int u = 0; u < U; ++u)
+      v[u] = *(const u32x4*)(slice + (size_t)min(t0 + u * STEP, t_end - 1) * D + 8 * c8);
 #pragma unroll
-    for (int u = 0; u < kSeqUnroll1; ++u) {
-      // rows past the end re-read the last row: the range is unchanged
+    for (int u = 0; u < U; ++u) {
       const float x[8] = {bf16_lo(v[u].x), bf16_hi(v[u].x), bf16_lo(v[u].y), bf16_hi(v[u].y),
                           bf16_lo(v[u].z), bf16_hi(v[u].z), bf16_lo(v[u].w), bf16_hi(v[u].w)};
 #pragma unroll
@@ -107,6 +111,65 @@ __device__ __forceinline__ void kivi_seq_slice(const Params& p, uint32_t s, cons
       mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], off));
     }
   }
+}
+
+// Codes (or, FAKE, the BF16 reconstruction) of image rows [t_begin, t_end)
+// of a slice (`rows`: its first image row; `codes` / `out`: the slice's
+// packed rows / reconstructed image rows), this lane's 8 channels with
+// scales g (S: the scales as floats).  t_end > t_begin.
+template <int D, int BITS, bool FAKE, int WAVES, int U = kSeqUnroll2>
+__device__ __forceinline__ void code_rows(const uint16_t* __restrict__ rows, uint8_t* codes, uint16_t* out,
+                                          int t_begin, int t_end, const GroupScale (&g)[8], const float (&S)[8]) {
+  constexpr int CPT = D / 8;
+  constexpr int RPL = 64 / CPT;
+  constexpr int STEP = WAVES * RPL;
+  constexpr int ROW = D * BITS / 8;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int c8 = lane % CPT;
+  for (int t0 = t_begin + wave * RPL + lane / CPT; t0 < t_end; t0 += U * STEP) {
+    u32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      v[u] = *(const u32x4*)(rows + (size_t)min(t0 + u * STEP, t_end - 1) * D + 8 * c8);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int t = t0 + u * STEP;
+      const float x[8] = {bf16_lo(v[u].x), bf16_hi(v[u].x), bf16_lo(v[u].y), bf16_hi(v[u].y),
+                          bf16_lo(v[u].z), bf16_hi(v[u].z), bf16_lo(v[u].w), bf16_hi(v[u].w)};
+      if constexpr (FAKE) {
+        float y[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf(__builtin_rintf(code_scaled(x[e], g[e])), S[e], g[e].m);
+        const u32x4 o = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
+                         pack_bf16x2_hw(y[6], y[7])};
+        if (t < t_end) store_nt((u32x4*)(out + (size_t)t * D + 8 * c8), o);
+      } else {
+        uint32_t cq[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cq[e] = code_bits(x[e], g[e]);
+        const Packed<8, BITS> pk = pack_code_bits<8, BITS>(cq);
+        if (t < t_end) store_packed<8, BITS>(codes + (size_t)t * ROW + c8 * BITS, pk);
+      }
+    }
+  }
+}
+
+template <int D, int BITS, bool FAKE, int WAVES>
+__device__ __forceinline__ void kivi_seq_slice(const Params& p, uint32_t s, const SliceRoute& route,
+                                               float (&part)[2][WAVES][D]) {
+  constexpr int CPT = D / 8;
+  constexpr int LEVELS = (1 << BITS) - 1;
+  constexpr int ROW = D * BITS / 8;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int c8 = lane % CPT;
+  const int r = lane / CPT;
+  const uint16_t* slice = p.cache[0] + (size_t)s * p.T * D;
+
+  // 1. ranges over all T rows
+  float mn[8], mx[8];
+  range_rows<D, WAVES>(slice, 0, p.T, mn, mx);
 
   // 2. combine the wavefronts and form the scales (the barrier first: the
   //    previous slice's readers of `part` are done)
@@ -140,34 +203,9 @@ __device__ __forceinline__ void kivi_seq_slice(const Params& p, uint32_t s, cons
   }
 
   // 3. the image rows: codes, or their reconstruction
-  const uint16_t* rows = slice + (size_t)p.s0 * D;
-  uint8_t* codes = FAKE ? nullptr : p.codes[0] + slab * p.n * ROW;
-  uint16_t* out = FAKE ? p.out[0] + (size_t)s * p.T * D + (size_t)p.s0 * D : nullptr;
-  for (int t0 = wave * RPL + r; t0 < p.n; t0 += kSeqUnroll2 * STEP) {
-    u32x4 v[kSeqUnroll2];
-#pragma unroll
-    for (int u = 0; u < kSeqUnroll2; ++u) v[u] = *(const u32x4*)(rows + (size_t)min(t0 + u * STEP, p.n - 1) * D + 8 * c8);
-#pragma unroll
-    for (int u = 0; u < kSeqUnroll2; ++u) {
-      const int t = t0 + u * STEP;
-      const float x[8] = {bf16_lo(v[u].x), bf16_hi(v[u].x), bf16_lo(v[u].y), bf16_hi(v[u].y),
-                          bf16_lo(v[u].z), bf16_hi(v[u].z), bf16_lo(v[u].w), bf16_hi(v[u].w)};
-      if constexpr (FAKE) {
-        float y[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf(__builtin_rintf(code_scaled(x[e], g[e])), S[e], g[e].m);
-        const u32x4 o = {pack_bf16x2_hw(y[0], y[1]), pack_bf16x2_hw(y[2], y[3]), pack_bf16x2_hw(y[4], y[5]),
-                         pack_bf16x2_hw(y[6], y[7])};
-        if (t < p.n) store_nt((u32x4*)(out + (size_t)t * D + 8 * c8), o);
-      } else {
-        uint32_t cq[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) cq[e] = code_bits(x[e], g[e]);
-        const Packed<8, BITS> pk = pack_code_bits<8, BITS>(cq);
-        if (t < p.n) store_packed<8, BITS>(codes + (size_t)t * ROW + c8 * BITS, pk);
-      }
-    }
-  }
+  if (p.n > 0)
+    code_rows<D, BITS, FAKE, WAVES>(slice + (size_t)p.s0 * D, FAKE ? nullptr : p.codes[0] + slab * p.n * ROW,
+                                    FAKE ? p.out[0] + (size_t)s * p.T * D + (size_t)p.s0 * D : nullptr, 0, p.n, g, S);
 }
 
 template <int D, int BITS, bool FAKE>
@@ -571,6 +609,109 @@ void kivi_part_kernel(const Params p, uint32_t n_items, uint32_t groups, uint32_
   }
 }
 
+// ------------------------------------------------------------ split kernels
+//
+// Slices too long for the resident kernel (or a device with too few compute
+// units for a group): every slice is cut into chunks of kSplitRows rows, so
+// all compute units share even a few long slices.  A range launch takes one
+// (slice, chunk) per workgroup and merges the chunk's per-channel minimum and
+// maximum into two words per channel of the workspace with device-scope
+// atomic maxima on order-preserving images of the floats (the minimum as the
+// complement of its image), so zero is the identity of both and the order of
+// the merges cannot change the result; a code launch then takes one (slice,
+// image chunk) per workgroup, forms the scales from the words and writes its
+// rows' codes (its first chunk also the metadata).  Work items are taken in
+// batches of kSplitBatch slices, whose words are cleared before their range
+// launch.
+
+constexpr int kSplitThreads = 512;
+constexpr int kSplitWaves = kSplitThreads / 64;
+constexpr int kSplitRows = 2048;
+constexpr int kSplitRangeUnroll = 8;  // rows in flight per lane
+constexpr int kSplitCodeUnroll = 16;
+constexpr uint32_t kSplitBatch = 2 * kExMaxWgs;  // slices of 2D 32-bit words in the exchange area
+
+// Order-preserving unsigned image of a float (finite or infinite): a < b
+// implies ord(a) < ord(b), and every image is above 0.
+__device__ __forceinline__ uint32_t ord_image(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float from_ord_image(uint32_t o) {
+  return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
+}
+
+template <int D>
+__global__ __launch_bounds__(kSplitThreads) void kivi_split_range_kernel(const Params p, uint32_t item0,
+                                                                         uint32_t n_items, uint32_t chunks,
+                                                                         uint32_t* __restrict__ words) {
+  constexpr int CPT = D / 8;
+  __shared__ float red[2 * D];
+  const int tid = threadIdx.x;
+  const uint32_t local = blockIdx.x / chunks, chunk = blockIdx.x % chunks;
+  const ResItem it = res_item(p, item0 + local, n_items);  // valid: the grid covers the batch exactly
+  for (int i = tid; i < 2 * D; i += kSplitThreads) red[i] = i < D ? __builtin_inff() : -__builtin_inff();
+  __syncthreads();
+  const int t_begin = (int)chunk * kSplitRows;
+  const int t_end = min(p.T, t_begin + kSplitRows);
+  float mn[8], mx[8];
+  range_rows<D, kSplitWaves, kSplitRangeUnroll>(p.cache[0] + (size_t)it.s * p.T * D, t_begin, t_end, mn, mx);
+  const int lane = tid & 63;
+  if (lane < CPT) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      atomicMin(&red[8 * lane + e], mn[e]);
+      atomicMax(&red[D + 8 * lane + e], mx[e]);
+    }
+  }
+  __syncthreads();
+  if (tid < D) {
+    uint32_t* w = words + (size_t)local * 2 * D;
+    __hip_atomic_fetch_max(w + tid, ~ord_image(red[tid]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_max(w + D + tid, ord_image(red[D + tid]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+template <int D, int BITS, bool FAKE>
+__global__ __launch_bounds__(kSplitThreads) void kivi_split_code_kernel(const Params p, uint32_t item0,
+                                                                        uint32_t n_items, uint32_t chunks,
+                                                                        const uint32_t* __restrict__ words) {
+  constexpr int CPT = D / 8;
+  constexpr int LEVELS = (1 << BITS) - 1;
+  constexpr int ROW = D * BITS / 8;
+  __shared__ uint32_t g_meta[D];
+  __shared__ float g_inv[D];
+  const int tid = threadIdx.x;
+  const uint32_t local = blockIdx.x / chunks, chunk = blockIdx.x % chunks;
+  const uint32_t item = item0 + local;
+  const ResItem it = res_item(p, item, n_items);
+  const size_t slab = (size_t)item;  // [slot][B] with slot = item / B
+  if (tid < D) {
+    const uint32_t* w = words + (size_t)local * 2 * D;
+    const GroupScale gs = group_scale<LEVELS>(from_ord_image(~w[tid]), from_ord_image(w[D + tid]));
+    g_meta[tid] = gs.meta;
+    g_inv[tid] = gs.inv;
+    if (!FAKE && chunk == 0) __builtin_nontemporal_store(gs.meta, p.meta[0] + slab * D + tid);
+  }
+  __syncthreads();
+  const int c8 = (tid & 63) % CPT;
+  GroupScale g[8];
+  float S[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    g[e].meta = g_meta[8 * c8 + e];
+    g[e].m = bf16_as_float(g[e].meta >> 16);
+    g[e].inv = g_inv[8 * c8 + e];
+    S[e] = bf16_as_float(g[e].meta & 0xFFFFu);
+  }
+  const int t_begin = (int)chunk * kSplitRows;
+  const int t_end = min(p.n, t_begin + kSplitRows);
+  code_rows<D, BITS, FAKE, kSplitWaves, kSplitCodeUnroll>(p.cache[0] + ((size_t)it.s * p.T + p.s0) * D,
+                                        FAKE ? nullptr : p.codes[0] + slab * p.n * ROW,
+                                        FAKE ? p.out[0] + ((size_t)it.s * p.T + p.s0) * D : nullptr, t_begin, t_end,
+                                        g, S);
+}
+
 // Zeroes the exchange words a launch uses (a kernel rather than a memset, so
 // the call can be captured in a graph).
 __global__ void zero_words_kernel(uint64_t* w, uint32_t n) {
@@ -581,21 +722,24 @@ __global__ void zero_words_kernel(uint64_t* w, uint32_t n) {
 
 int kivi_part_capacity(int D) { return kPartSlots * kPartWaves * (512 / D); }
 
-// Workgroups per slice of the resident kernel, 0 for the two-pass kernel.  A
+// Workgroups per slice of the resident kernel, 0 for the split kernels.  A
 // grid holds 8 groups per 8 P workgroups, so past 8 partners P is rounded up
 // to 16 or 32, which fill every compute unit; each partner keeps at least one
 // row ((P - 1) ceil(T / P) < T holds for T > (P - 1)^2).
 int kivi_partners(int T, int D) {
   const int cap = kivi_part_capacity(D);
   int parts = (T + cap - 1) / cap;
-  if (parts > kMaxPartners || (uint64_t)T * D * 2 >= (1ull << 31)) return 0;  // two-pass kernel
+  if (parts > kMaxPartners || (uint64_t)T * D * 2 >= (1ull << 31)) return 0;  // split kernels
   if (parts > kSerialPartners) parts = parts <= 16 ? 16 : 32;
   if ((uint64_t)(parts - 1) * (uint64_t)((T + parts - 1) / parts) >= (uint64_t)T) return 0;
   return parts;
 }
 
+// The exchange area: the resident kernel's partial ranges when several
+// workgroups hold a slice, else (longer slices) the split kernels' range
+// words; a slice that one workgroup holds needs none.
 uint64_t kivi_workspace_bytes(int T, int D) {
-  return kivi_partners(T, D) > 1 ? ((uint64_t)kExHeader + (uint64_t)kExMaxWgs * 2 * D) * 8 : 0;
+  return T > kivi_part_capacity(D) ? ((uint64_t)kExHeader + (uint64_t)kExMaxWgs * 2 * D) * 8 : 0;
 }
 
 // Compute units the persistent grids are sized for: the device's, or fewer
@@ -613,12 +757,15 @@ static hipError_t grid_cus(int* cus) {
 
 // Launch plan of one call's key kernels: the resident kernel when every
 // workgroup of its grid can be resident at once (and, with several per slice,
-// an exchange workspace is given), else the two-pass kernel; and the leading
+// an exchange workspace is given), else, with a workspace, the split range
+// and code kernels, and without one (a slice one workgroup holds, on a device
+// with fewer than 8 compute units) the two-pass kernel; and the leading
 // workspace words to clear before it (the exchange words the resident grid
-// uses, or the header alone, whose first word then reads 0: the two-pass
-// kernel waits for nothing).
+// uses, or the header and the first batch's range words: the split kernels
+// wait for nothing, so the header's first word then reads 0).
 struct KiviPlan {
   bool resident = false;
+  bool split = false;
   int parts = 0;
   uint32_t n_items = 0, groups = 0, rows_per_part = 0;
   uint32_t clear_words = 0;
@@ -654,7 +801,10 @@ static hipError_t plan_k(const Params& p, bool has_ws, KiviPlan* pl) {
       return hipSuccess;
     }
   }
-  if (has_ws) pl->clear_words = (uint32_t)kExHeader;
+  if (has_ws) {
+    pl->split = true;
+    pl->clear_words = (uint32_t)(kExHeader + (uint64_t)std::min(pl->n_items, kSplitBatch) * D);
+  }
   return hipSuccess;
 }
 
@@ -678,6 +828,26 @@ static hipError_t launch_k(const Params& p, void* ws, bool cleared, hipStream_t 
       hipLaunchKernelGGL((kivi_part_kernel<D, BITS, FAKE, false>), grid, dim3(kPartThreads), 0, stream, p, pl.n_items,
                          pl.groups, (uint32_t)pl.parts, pl.rows_per_part, (uint64_t*)ws);
     return hipGetLastError();
+  }
+  if (pl.split) {
+    uint32_t* words = (uint32_t*)((uint64_t*)ws + kExHeader);
+    const uint32_t range_chunks = (uint32_t)((p.T + kSplitRows - 1) / kSplitRows);
+    const uint32_t code_chunks = (uint32_t)((p.n + kSplitRows - 1) / kSplitRows);
+    for (uint32_t i0 = 0; i0 < pl.n_items; i0 += kSplitBatch) {
+      const uint32_t nb = std::min(kSplitBatch, pl.n_items - i0);
+      if (i0 > 0) {  // the first batch's words were cleared with the header
+        const uint32_t n64 = nb * (uint32_t)D;  // 2D 32-bit words per slice
+        hipLaunchKernelGGL(zero_words_kernel, dim3(std::min<uint32_t>((n64 + 255) / 256, 1024)), dim3(256), 0, stream,
+                           (uint64_t*)words, n64);
+      }
+      hipLaunchKernelGGL((kivi_split_range_kernel<D>), dim3(nb * range_chunks), dim3(kSplitThreads), 0, stream, p, i0,
+                         pl.n_items, range_chunks, words);
+      hipLaunchKernelGGL((kivi_split_code_kernel<D, BITS, FAKE>), dim3(nb * code_chunks), dim3(kSplitThreads), 0,
+                         stream, p, i0, pl.n_items, code_chunks, (const uint32_t*)words);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
   }
   int cus = 0;
   e = grid_cus(&cus);

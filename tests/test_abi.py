@@ -89,14 +89,14 @@ def test_sizes_match_oracle(seed):
 def kivi_exchange_bytes(f, sizes):
     """Closed form of hg_quantize's workspace: KIVI keys over the whole
     sequence, some key slice quantized, and a slice longer than one
-    workgroup's 24 slots of 16 * 512/D rows (at most 32 workgroups per slice):
-    a 64-word header plus 1024 workgroups x 2 buffers x D tagged words (one
-    per channel)."""
+    workgroup's 24 slots of 16 * 512/D rows: a 64-word header plus 1024
+    workgroups x 2 buffers x D tagged words (one per channel); past 32
+    workgroups' rows the same area holds the split kernels' range words."""
     if f["base"] != 1 or f["kivi_group"] != 0 or f["img_len"] == 0 or sizes["n_unprot_k"] == 0:
         return 0
     cap = 24 * 8192 // f["D"]
     parts = -(-f["T"] // cap)
-    if parts < 2 or parts > 32:
+    if parts < 2:
         return 0
     return (64 + 1024 * 2 * f["D"]) * 8
 
@@ -105,9 +105,9 @@ def test_workspace_of_whole_sequence_kivi_keys():
     mask = np.zeros(8, np.uint8)
     ws = lambda D: (64 + 2048 * D) * 8  # noqa: E731
     for T, D, want in ((3008, 128, ws(128)), (1536, 128, 0), (1537, 128, ws(128)), (12288, 128, ws(128)),
-                       (12289, 128, ws(128)), (49152, 128, ws(128)), (49153, 128, 0), (3008, 64, 0),
-                       (3073, 64, ws(64)), (98304, 64, ws(64)), (98305, 64, 0), (3008, 256, ws(256)),
-                       (24576, 256, ws(256)), (24577, 256, 0)):
+                       (12289, 128, ws(128)), (49152, 128, ws(128)), (49153, 128, ws(128)), (3008, 64, 0),
+                       (3073, 64, ws(64)), (98305, 64, ws(64)), (3008, 256, ws(256)), (24577, 256, ws(256)),
+                       (1 << 24, 128, ws(128))):
         f = _cfg(base=1, kivi_group=0, T=T, D=D, img_start=0, img_len=T)
         got = hg.hg_packed_sizes(hg.make_config(**f), mask)
         assert got["workspace"] == want == got["fake_workspace"], (T, D, got["workspace"], want)

@@ -8,7 +8,10 @@ Slices of up to 32 workgroups' capacity (24 slots of 8192/D rows: 3072,
 1536 and 768 rows at head_dim 64, 128 and 256) go through the partitioned
 resident kernel: P workgroups each hold a run of a slice's rows on chip and
 combine their partial ranges through the call's workspace (past 8, P is
-rounded up to 16 or 32); longer slices go through the two-pass kernel.
+rounded up to 16 or 32); longer slices go through the split kernels (a
+range launch over chunks of every slice merging per-channel ranges into the
+workspace, then a code launch), and a slice one workgroup holds, on a device
+too small for a group, through the two-pass kernel (no workspace).
 Covered: one to eight, 16 and 32 workgroups per slice and the capacity
 boundaries, several slices per group (with the grid shrunk through the
 HG_TEST_CUS hook), identical bytes for different grid sizes, and no exchange
@@ -66,14 +69,31 @@ def test_full_size_llava_one_pass(inplace):
 
 def test_long_single_slice():
     """One key slice of 2^21 + 5 tokens at head_dim 128 (512 MiB, text rows at
-    both ends): far past 32 workgroups' capacity, so the two-pass kernel
-    ranges and codes it alone; every byte against the oracle."""
+    both ends): far past 32 workgroups' capacity, so the split kernels range
+    and code it in 1025 and 1024 chunks; every byte against the oracle."""
     T = (1 << 21) + 5
     w = synthkv.Workload("kiviseq-long-slice", L=1, B=1, H=1, T=T, D=128, img_start=1000, img_len=T - 1777,
                          bits=2, base="kivi", keys_only=0, n_protected=0, k_outliers=4, k_outlier_scale=10.0,
                          kivi_group=0, seed=21)
     assert T > 8 * capacity(128)
     wholecache.assert_whole(wholecache.quantize_dequantize(w), w)
+
+
+@pytest.mark.parametrize("fake", [False, True])
+def test_two_pass_without_workspace(fake, monkeypatch):
+    """Slices one workgroup holds need no workspace; on a device with fewer
+    than 8 compute units (the grid hook) there is no group of 8 to run them, so
+    the two-pass kernel takes them."""
+    monkeypatch.setenv("HG_TEST_CUS", "4")
+    w = small("kivi", 128, 3, 0, img_len=1000, img_start=9, text=20, L=2, B=3, H=2,
+              n_protected=1).with_(kivi_group=0, name="kiviseq-two-pass")
+    assert w.T <= capacity(128)
+    K, V = synthkv.gen_kv(w)
+    mask = synthkv.protect_mask(w)
+    if fake:
+        check_fake(w, K, V, mask, False)
+    else:
+        _assert_exact(compare_full(w, K, V, mask), w.name)
 
 
 def capacity(D):
@@ -110,7 +130,7 @@ def test_resident_streams_fake(w, inplace, monkeypatch):
 def test_grid_size_does_not_change_the_bytes(cus, monkeypatch):
     """The same cache (two workgroups per slice) under persistent grids sized
     for 256 down to 1 compute units (fewer than 16 are too few workgroups for
-    a multiple of 8 groups: the two-pass kernel takes over), and once more with
+    a multiple of 8 groups: the split kernels take over), and once more with
     the full grid: every run equals the oracle."""
     w = small("kivi", 128, 2, 0, img_len=3000, img_start=5, text=3, L=2, B=6, H=5,
               n_protected=2).with_(kivi_group=0)
@@ -121,7 +141,7 @@ def test_grid_size_does_not_change_the_bytes(cus, monkeypatch):
 
 # Slices at each workgroup count's capacity and one row past it (one to eight
 # workgroups per slice, then 16 and 32; past 32 workgroups' capacity, the
-# two-pass kernel), spans at the start, in the middle and at the end of the
+# split kernels), spans at the start, in the middle and at the end of the
 # slice (the middle only for the longest slices).
 def _boundary_cases():
     out = []
@@ -186,7 +206,7 @@ STALE_CASE = next(w for w in STREAM_CASES
 
 
 # Resident kernel with several slices per group (32 and 256 compute units'
-# grids) and the two-pass fallback (8), every call on a workspace holding
+# grids) and the split kernels (8), every call on a workspace holding
 # stale tagged words: the call must clear them before the key kernel reads.
 @pytest.mark.parametrize("cus", ["32", "", "8"])
 def test_stale_exchange_words(cus, monkeypatch):
