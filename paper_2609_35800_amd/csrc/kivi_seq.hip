@@ -834,8 +834,13 @@ static hipError_t launch_k(const Params& p, void* ws, bool cleared, hipStream_t 
     uint32_t* words = (uint32_t*)((uint64_t*)ws + kExHeader);
     const uint32_t range_chunks = (uint32_t)((p.T + kSplitRows - 1) / kSplitRows);
     const uint32_t code_chunks = (uint32_t)((p.n + kSplitRows - 1) / kSplitRows);
-    for (uint32_t i0 = 0; i0 < pl.n_items; i0 += kSplitBatch) {
-      const uint32_t nb = std::min(kSplitBatch, pl.n_items - i0);
+    // slices per launch pair: the words area's, and few enough that a launch
+    // stays under 2^32 work-items
+    const uint64_t chunks = std::max(range_chunks, code_chunks);
+    const uint32_t batch = (uint32_t)std::max<uint64_t>(
+        1, std::min<uint64_t>(kSplitBatch, (0xFFFFFFFFull / kSplitThreads) / chunks));
+    for (uint32_t i0 = 0; i0 < pl.n_items; i0 += batch) {
+      const uint32_t nb = std::min(batch, pl.n_items - i0);
       if (i0 > 0) {  // the first batch's words were cleared with the header
         const uint32_t n64 = nb * (uint32_t)D;  // 2D 32-bit words per slice
         hipLaunchKernelGGL(zero_words_kernel, dim3(std::min<uint32_t>((n64 + 255) / 256, 1024)), dim3(256), 0, stream,
