@@ -3,7 +3,8 @@ allocate device memory; its workspace is the library's own device array)
 against hg_fake_quantize with a caller workspace: the same bytes, on two calls
 in a row, the second on a smaller cache, in place and out of place, with and
 without token retention, and with whole-sequence KIVI keys (whose workgroups
-exchange partial ranges through the workspace).  A cache whose workspace
+exchange partial ranges through the workspace, or, for long slices, merge
+chunk ranges into it).  A cache whose workspace
 would exceed the array is refused before any device work."""
 import ctypes as C
 
@@ -49,20 +50,25 @@ def _one_pass(hg, w, mask, inplace, noalloc):
     return Ko.view(torch.int16).clone(), Vo.view(torch.int16).clone()
 
 
-def _kivi_whole(big):
+def _kivi_whole(kind):
     # the workgroups holding a slice exchange their partial ranges through the
-    # workspace (2 MiB at head_dim 128): 2 workgroups per slice on the larger
-    # cache, 16 on the smaller one
-    if big:
+    # workspace (2 MiB at head_dim 128): 2 workgroups per slice on the
+    # LLaVA-NeXT-shaped cache, 16 on the smaller one; slices past 32
+    # workgroups' rows merge chunk ranges into the same area
+    if kind == "big":
         return synthkv.WORKLOADS["llava-next-7b"].with_(kivi_group=0, L=8)
+    if kind == "long":
+        w = small("kivi", D=128, bits=2, img_len=60000, img_start=5, text=11, L=2, B=2, H=2, n_protected=1)
+        return w.with_(kivi_group=0, name="long-kivi-whole")
     w = small("kivi", D=128, bits=2, img_len=12500, img_start=5, text=11, L=1, B=2, H=2, n_protected=1)
     return w.with_(kivi_group=0, name="small-kivi-whole")
 
 
+@pytest.mark.parametrize("first", ["big", "long"])
 @pytest.mark.parametrize("inplace", [False, True])
-def test_whole_sequence_kivi_keys_on_two_calls(inplace):
+def test_whole_sequence_kivi_keys_on_two_calls(inplace, first):
     import paper_2609_35800_amd as hg
-    for w in (_kivi_whole(True), _kivi_whole(False)):
+    for w in (_kivi_whole(first), _kivi_whole("small")):
         mask = synthkv.protect_mask(w)
         need = hg.hg_packed_sizes(hg.make_config(**w.config_fields()), mask)["fake_workspace"]
         assert 0 < need <= hg.HG_NOALLOC_SCRATCH_BYTES
