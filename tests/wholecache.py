@@ -29,7 +29,7 @@ import synthkv
 from hgtest import PAD, alloc_with_canary, canaries_intact, exchange_timeouts
 
 SENTINEL = 0x7FBF
-# oracle threads: the host's cores, at most 16 (a GPU machine's CPU share)
+# oracle threads: the host's cores, at most 16
 THREADS = max(1, min(os.cpu_count() or 1, 16))
 
 
