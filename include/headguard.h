@@ -222,7 +222,8 @@ int hg_fake_quantize(const hg_config* cfg, const uint16_t* K, const uint16_t* V,
 
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, serving loops, harnesses that forbid allocation): hg_fake_quantize
- * with its token-retention workspace taken from a device array inside the
+ * with its workspace (token retention's lists, or the whole-sequence KIVI key
+ * exchange area) taken from a device array inside the
  * library, HG_NOALLOC_SCRATCH_BYTES per GPU, held until the process ends,
  * instead of a caller buffer.  Same arguments, results and errors as
  * hg_fake_quantize otherwise; a call whose workspace would exceed the array

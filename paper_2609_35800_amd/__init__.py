@@ -167,7 +167,8 @@ def hg_fake_quantize(cfg: hg_config, K: torch.Tensor, V: torch.Tensor, protect_m
     """Enqueue the one-pass quantize-and-reconstruct of the image rows of K, V
     into K_out, V_out (which may be K, V themselves).  `workspace`: a device
     buffer of at least hg_packed_sizes(...)["fake_workspace"] bytes, needed
-    with token retention (see alloc_fake_workspace)."""
+    with token retention and with whole-sequence KIVI keys longer than one
+    workgroup holds (see alloc_fake_workspace)."""
     m = _mask_arg(protect_mask)
     ws = _ptr(workspace)
     nbytes = workspace.numel() * workspace.element_size() if ws is not None else 0
@@ -177,8 +178,9 @@ def hg_fake_quantize(cfg: hg_config, K: torch.Tensor, V: torch.Tensor, protect_m
 
 def hg_fake_quantize_noalloc(cfg: hg_config, K: torch.Tensor, V: torch.Tensor, protect_mask,
                              K_out: torch.Tensor, V_out: torch.Tensor, stream=None) -> None:
-    """hg_fake_quantize with the retention workspace taken from the library's
-    own device array (HG_NOALLOC_SCRATCH_BYTES per GPU): nothing is allocated;
+    """hg_fake_quantize with its workspace (retention lists, or the
+    whole-sequence key exchange area) taken from the library's own device
+    array (HG_NOALLOC_SCRATCH_BYTES per GPU): nothing is allocated;
     overlapping calls on one GPU race on that array."""
     m = _mask_arg(protect_mask)
     _check(_lib.hg_fake_quantize_noalloc(C.byref(cfg), _ptr(K), _ptr(V), m.ctypes.data_as(C.c_void_p),
