@@ -75,7 +75,8 @@ class Workload:
 # VLMs (Qwen2.5-VL-7B, LLaVA-NeXT-7B, InternVL3-8B, a 72B model) with image
 # spans of 1296-6400 tokens; LLaVA-1.5-7B- and Gemma-3-12B-shaped caches
 # (576-token spans; head_dim 256); and
-# one GPU's share of the 72B cache under an eight-way split by KV head.
+# one GPU's share of the 72B cache under an eight-way split by KV head; and a
+# Qwen2.5-VL-7B-shaped 128K-token context with whole-sequence KIVI keys.
 WORKLOADS: Dict[str, Workload] = {
     "tiny": Workload("tiny", L=2, B=1, H=4, T=288, D=64, img_start=16, img_len=256,
                      bits=2, base="minmax", keys_only=1, n_protected=1,
@@ -107,6 +108,13 @@ WORKLOADS: Dict[str, Workload] = {
     "72b-long-tp8": Workload("72b-long-tp8", L=80, B=2, H=1, T=6656, D=128, img_start=128,
                              img_len=6400, bits=2, base="minmax", keys_only=0,
                              n_protected=10, k_outliers=8, k_outlier_scale=20.0),
+    # Qwen2.5-VL-7B-shaped heads over a 128K-token context (a long video),
+    # KIVI-style keys over the whole sequence: slices longer than 32
+    # workgroups hold
+    "qwen2.5-vl-7b-128k": Workload("qwen2.5-vl-7b-128k", L=28, B=1, H=4, T=131072, D=128,
+                                   img_start=536, img_len=130000, bits=2, base="kivi",
+                                   keys_only=1, n_protected=14, k_outliers=4,
+                                   k_outlier_scale=10.0, kivi_group=0),
 }
 
 

@@ -1,5 +1,5 @@
-"""GPU parity at the full sizes of the five workloads (and three more cache
-shapes), in the launch configuration the bench times: the whole cache is
+"""GPU parity at the full sizes of the five workloads (and four more cache
+shapes, one a 128K-token context), in the launch configuration the bench times: the whole cache is
 quantized and dequantized on the GPU, then every (tensor, layer, batch row,
 head) slice is recomputed by the CPU oracle — codes, metadata, BF16 side
 store, retention outputs and reconstruction, text rows included — and must be
@@ -16,7 +16,7 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("name", ["tiny", "qwen2.5-vl-7b", "llava-next-7b", "internvl-8b", "gemma-3-12b",
-                                  "llava-1.5-7b", "72b-long-tp8"])
+                                  "llava-1.5-7b", "72b-long-tp8", "qwen2.5-vl-7b-128k"])
 def test_workload(name):
     w = synthkv.WORKLOADS[name]
     wholecache.assert_whole(wholecache.quantize_dequantize(w), w)
