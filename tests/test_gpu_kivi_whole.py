@@ -96,6 +96,19 @@ def test_two_pass_without_workspace(fake, monkeypatch):
         _assert_exact(compare_full(w, K, V, mask), w.name)
 
 
+def test_split_batches(monkeypatch):
+    """More quantized key slices than the workspace holds range words for
+    (2048), through the split kernels (forced by the grid hook: 4 compute
+    units cannot hold a group of 8): the slices are taken in two batches, the
+    second batch's words cleared by a kernel of their own."""
+    monkeypatch.setenv("HG_TEST_CUS", "4")
+    w = small("kivi", 64, 2, 1, img_len=50, img_start=3000, text=23, L=8, B=3, H=128,
+              n_protected=24).with_(kivi_group=0, name="kiviseq-split-batches")
+    assert w.T > capacity(64) and (w.L * w.H - w.n_protected) * w.B > 2048
+    K, V = synthkv.gen_kv(w)
+    _assert_exact(compare_full(w, K, V, synthkv.protect_mask(w)), w.name)
+
+
 def capacity(D):
     """Rows one workgroup of the partitioned kernel holds."""
     return 24 * 8192 // D
