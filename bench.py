@@ -43,14 +43,15 @@ KERNEL_SOURCES = {
 KIVI_WHOLE_SOURCE = _CSRC + "kivi_seq.hip"
 RETAIN_SOURCE = _CSRC + "retain.hip"
 # The measured-results table: the five workloads (the 72B-shaped one at each
-# bit width), the whole-sequence KIVI keys and the 2 % token retention, each as
-# a quantize + dequantize step, and the one-pass mode on three of them:
-# (workload, option overrides, op).
+# bit width), the whole-sequence KIVI keys, the 2 % token retention and a
+# 128K-token context with whole-sequence keys, each as a quantize + dequantize
+# step, and the one-pass mode on three of them: (workload, option overrides,
+# op).
 TABLE_ROWS = (
     ("tiny", {}, "step"), ("qwen2.5-vl-7b", {}, "step"), ("llava-next-7b", {}, "step"),
     ("internvl-8b", {}, "step"), ("72b-long", {"bits": 2}, "step"), ("72b-long", {"bits": 3}, "step"),
     ("72b-long", {"bits": 4}, "step"), ("llava-next-7b", {"kivi_group": 0}, "step"),
-    ("internvl-8b", {"retain_permille": 20}, "step"),
+    ("internvl-8b", {"retain_permille": 20}, "step"), ("qwen2.5-vl-7b-128k", {}, "step"),
     ("qwen2.5-vl-7b", {}, "fakequant"), ("llava-next-7b", {"kivi_group": 0}, "fakequant"),
     ("internvl-8b", {"retain_permille": 20}, "fakequant"),
 )
